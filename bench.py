@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of the BD-LoRA layer-shard forward on one MI355X.
+
+A step is one forward of a whole decoder-layer shard (all its projections:
+plan, shrink, base product with fused expand) over one batch of synthetic
+tokens, through the library's C ABI.  Default workload: Llama-3.1-8B layer
+shard at 1/8 tensor parallelism, 64 decode tokens, 32 resident adapters of
+rank 16, adapter ids Zipf(1.0).
+
+Timing: steps are captured into HIP graphs, each graph one pass over R
+rotated copies of every input (weights, adapter pool, activations, outputs)
+whose footprint exceeds twice the 256 MB Infinity Cache, so the data comes
+from HBM.  The K timed steps are bracketed by torch.cuda.synchronize(); the
+reported time is the wall clock over them.
+
+Prints one JSON line (rank 0).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 matrix, published
+MALL_BYTES = 256 << 20
+
+
+def algorithmic_bytes(spec, ids, ranks):
+    """Per-step bytes the method must move, split by kernel.
+
+    gemm: every base weight once, X and out once per projection, the B
+    factor of every adapter some token uses.  shrink: the A factor of every
+    adapter some token uses.  bf16 = 2 bytes.
+    """
+    active = sorted({int(a) for a in ids if a >= 0})
+    T = len(ids)
+    g = s = 0
+    for p in spec.projs:
+        n = sum(p.slices)
+        g += p.d_in * n + T * p.d_in + T * n
+        for a in active:
+            r = ranks[a]
+            g += r * n
+            s += len(p.slices) * p.d_in * r
+    return 2 * g, 2 * s, len(active)
+
+
+def algorithmic_flops(spec, ids, ranks):
+    T = len(ids)
+    g = s = 0
+    for p in spec.projs:
+        n = sum(p.slices)
+        g += 2 * T * p.d_in * n
+        for a in ids:
+            if a >= 0:
+                r = ranks[a]
+                g += 2 * r * n
+                s += 2 * len(p.slices) * p.d_in * r
+    return g, s
+
+
+def cpu_baseline(spec, layer, seconds):
+    """Time the oracle (fp64 numpy) on this host: whole steps until
+    ``seconds`` have passed."""
+    from oracle import bdlora
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    bdlora.layer_forward(layer)                     # warm-up
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        bdlora.layer_forward(layer)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {
+        "value": spec.T * n / el,
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{n} full steps of the same workload ({spec.T} tokens x {len(spec.projs)} "
+                  f"projections), fp64 numpy, {el:.1f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", type=int, default=1, help="workload index 0..4 (default 1)")
+    ap.add_argument("--rotate", type=int, default=0, help="input copies to rotate (0 = auto)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="time eager launches instead of graphs")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs one GPU's shard only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU path is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2510_23346_amd as bd
+    import workloads as wl
+    from workloads.gpu import DeviceLayer, load_adapters, make_pool
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    bd.lib()
+    spec = wl.workload(args.workload)
+    ids_np = wl.draw_ids(spec)
+    resident = list(range(spec.n_slots)) if spec.n_slots <= 128 else sorted(
+        int(s) for s in np.unique(ids_np) if s >= 0)
+    layer = wl.draw_layer(spec, slots=resident)
+    g_bytes, s_bytes, n_active = algorithmic_bytes(spec, ids_np, spec.ranks)
+    g_flops, s_flops = algorithmic_flops(spec, ids_np, spec.ranks)
+    step_bytes = g_bytes + s_bytes
+    decode = spec.T <= 256
+
+    # rotated copies: each is a pool with the same adapters plus its own tensors
+    pool0 = make_pool(spec)
+    load_adapters(pool0, spec, resident, cache=layer.adapters)
+    set_bytes = step_bytes + pool0.bytes
+    R = args.rotate or max(2, math.ceil(2 * MALL_BYTES / max(1, step_bytes)))
+    R = min(R, 16)
+    sets = []
+    for i in range(R):
+        pool = pool0 if i == 0 else make_pool(spec)
+        if i:
+            load_adapters(pool, spec, resident, cache=layer.adapters)
+        sets.append((pool, DeviceLayer(layer)))
+    projs = list(range(len(spec.projs)))
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        pool, dl = sets[i % R]
+        pool.forward_layer(projs, dl.X, dl.W, dl.out, dl.ids, stream=stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # graphs: one per pass over the R copies, plus one for a remainder
+    K = args.steps
+    graphs = []
+    if not args.eager:
+        def capture(n):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+                s = torch.cuda.current_stream()
+                for i in range(n):
+                    pool, dl = sets[i % R]
+                    pool.forward_layer(projs, dl.X, dl.W, dl.out, dl.ids, stream=s)
+            return g
+        full, rem = divmod(K, R)
+        g_full = capture(R) if full else None
+        g_rem = capture(rem) if rem else None
+        for _ in range(2):
+            if g_full:
+                g_full.replay()
+        torch.cuda.synchronize()
+        plan = [g_full] * full + ([g_rem] if g_rem else [])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    if args.eager:
+        for i in range(K):
+            step(i)
+    else:
+        for g in plan:
+            g.replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / K
+
+    # per-kernel durations with HIP events on the launch stream (eager)
+    n_prof = max(R, min(K, 400))
+    per_pool = math.ceil(n_prof / R)
+    for pool, _ in sets:
+        pool.profile_begin(per_pool)
+    for i in range(per_pool * R):
+        step(i)
+    torch.cuda.synchronize()
+    sums, cnt = [0.0, 0.0, 0.0], 0
+    for pool, _ in sets:
+        ms, n = pool.profile_end()
+        for k in range(3):
+            sums[k] += ms[k] * n
+        cnt += n
+    k_ms = [s / max(1, cnt) for s in sums]
+    gemm_s = k_ms[2] * 1e-3
+    if decode:
+        achieved = g_bytes / gemm_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        achieved = g_flops / gemm_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4), "traffic": None}
+    roof["kernel"] = "bdl::gemm_kernel (base product + fused expand)"
+    roof["kernel_ms"] = round(k_ms[2], 5)
+
+    out = {
+        "metric": "tokens/s per layer-shard",
+        "value": round(spec.T / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": spec.name,
+            "description": spec.description,
+            "tokens": spec.T,
+            "projections": [p.name for p in spec.projs],
+            "adapters_resident": len(resident),
+            "adapters_active": n_active,
+            "ranks": sorted(set(spec.ranks)),
+            "parallelism": "one tensor-parallel shard (1 of 8) on one GPU",
+            "timing": "eager launches" if args.eager else f"HIP graphs over {R} rotated input copies",
+        },
+        "step_hbm": {
+            "algorithmic_bytes": step_bytes,
+            "GB/s": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+            "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        },
+        "step_flops": g_flops + s_flops,
+        "kernel_ms": {"plan": round(k_ms[0], 5), "shrink": round(k_ms[1], 5), "gemm": round(k_ms[2], 5)},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(spec, layer, args.cpu_seconds)
+    for pool, _ in sets:
+        pool.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

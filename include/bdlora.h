@@ -1,0 +1,195 @@
+/*
+ * bdlora.h -- C ABI of the MI355X (gfx950) block-diagonal LoRA shard library.
+ *
+ * What it computes.  One GPU's tensor-parallel share of a LoRA-augmented
+ * projection, for a batch in which every token names its own adapter
+ * (unmerged multi-adapter serving, paper Sec. 1; the BD-LoRA sharding of
+ * Sec. 3 and Fig. 3; the per-device steps of Alg. 1 and Alg. 2):
+ *
+ *     out[t, :] = X[t, :] W_s^T + scale_a * (X[t, :] A_{s,a}) B_{s,a},  a = id(t)
+ *
+ * Column-parallel projections (q/k/v, gate, up): X is the replicated input,
+ * A_{s,a} is the shard's column slice of A and B_{s,a} the shard's diagonal
+ * block of the block-diagonal B, so the LoRA term lands on the shard's own
+ * output columns.  Row-parallel projections (o, down): X is the shard's input
+ * slice, A_{s,a} the shard's diagonal block of the block-diagonal A and
+ * B_{s,a} the shard's row slice of B; `out` is then a partial sum that the
+ * base model's all-reduce would add up (not run by this library).  A
+ * projection may have up to 4 slices (q, k, v): each slice has its own
+ * adapter factors and its outputs sit side by side.
+ *
+ * Conventions.
+ *  - Element type of X, W_s, out and of adapter factors: bfloat16, passed as
+ *    16-bit patterns (uint16_t on the host, any 2-byte type on the device).
+ *    Products accumulate in fp32; out is rounded once to bf16 (nearest-even).
+ *  - Layouts are row-major.  X: [T x d_in].  W_s: [d_out_s x d_in] (the
+ *    nn.Linear weight layout, d_in contiguous).  out: [T x d_out_s], slices
+ *    side by side.  Adapter factors are given in the paper's layout:
+ *    A: [d_in x rank], B: [rank x slice_out] per slice.
+ *  - Adapter ids: int32, one per token; -1 = no adapter (base only).  An id
+ *    that is out of range or names an empty slot is treated as -1 and raises
+ *    the pool's sticky device error flag (see bdlora_get_device_error).
+ *  - Device pointers are caller-owned and must stay valid until the work
+ *    enqueued on `stream` has finished.  `stream` is a hipStream_t (NULL =
+ *    the default stream).  Forward calls only enqueue; they never block.
+ *  - A pool owns the adapter memory and a workspace sized at creation.  All
+ *    forward calls on one pool must be issued on one stream (the workspace is
+ *    shared); use one pool per stream otherwise.  Loading or unloading an
+ *    adapter must not overlap a forward that uses it.
+ *  - Every int-returning call returns a status code below; on failure
+ *    bdlora_last_error() gives a message (thread-local).
+ */
+#ifndef BDLORA_H
+#define BDLORA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BDLORA_OK               0
+#define BDLORA_ERR_INVALID_ARG (-1)  /* null pointer, bad slot, bad value      */
+#define BDLORA_ERR_OOM         (-2)  /* device or host allocation failed       */
+#define BDLORA_ERR_BAD_ADAPTER (-3)  /* host-side id names no loaded adapter   */
+#define BDLORA_ERR_SHAPE       (-4)  /* sizes the kernels do not support       */
+#define BDLORA_ERR_HIP         (-5)  /* a HIP runtime call failed              */
+#define BDLORA_ERR_UNSUPPORTED (-6)  /* no gfx950 device / feature missing     */
+
+#define BDLORA_COLUMN 0
+#define BDLORA_ROW    1
+#define BDLORA_MAX_SLICES 4
+#define BDLORA_MAX_PROJS  8
+#define BDLORA_MAX_SLOTS  8192
+#define BDLORA_MAX_RANK   128
+
+typedef struct bdlora_pool* bdlora_pool_t;
+
+/* One projection on one shard.  d_in: local input width (K), a multiple of
+ * 32.  slice_out[i]: local output width of slice i, a multiple of 16.
+ * kind only documents the sharding (BDLORA_COLUMN / BDLORA_ROW); both kinds
+ * run the same per-shard computation (Alg. 1 first and second projection). */
+typedef struct {
+    int32_t kind;
+    int32_t d_in;
+    int32_t n_slices;
+    int32_t slice_out[BDLORA_MAX_SLICES];
+} bdlora_proj_desc;
+
+/* Create an adapter pool on HIP device `device` for the `n_projs`
+ * projections described by `projs` (1..BDLORA_MAX_PROJS).  The pool has
+ * `max_slots` adapter slots (1..BDLORA_MAX_SLOTS), each sized for rank
+ * `max_rank` (0..BDLORA_MAX_RANK) on every projection, plus a workspace for
+ * batches of up to `max_tokens` tokens.  Paper: the GPU-side adapter cache
+ * of App. C.2 / App. F (adapters loaded once, reused by every batch).
+ * All memory is allocated here; forward calls allocate nothing.
+ * On success *out receives the handle.  Errors: INVALID_ARG, SHAPE, OOM, HIP,
+ * UNSUPPORTED (device is not gfx950). */
+int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots,
+                       int32_t max_rank, int32_t max_tokens, int32_t device,
+                       bdlora_pool_t* out);
+
+/* Free every device and host resource of the pool (waits for its work). */
+int bdlora_destroy_pool(bdlora_pool_t pool);
+
+/* Copy one adapter into `slot` (0..max_slots-1) and pack it into the pool's
+ * kernel layout on the device.  rank: 0..max_rank (0 = an adapter that adds
+ * nothing).  scale: the factor of the LoRA term (rsLoRA-style gamma of Sec. 2;
+ * BD-LoRA training uses alpha*sqrt(N)/sqrt(r), Sec. 3), finite.
+ * A_host and B_host are arrays of host pointers indexed [proj][slice] in
+ * projection-major order (slice index runs fastest): A is [d_in x rank] and
+ * B is [rank x slice_out], bf16, row-major, the shard's own factors sliced as
+ * in App. C.2 (column: A column block + B diagonal block; row: A diagonal
+ * block + B row block).  Values must be finite.  The call is synchronous:
+ * host buffers may be freed on return.  Replaces any adapter in the slot.
+ * Errors: INVALID_ARG (bad slot/rank/scale, null pointer, non-finite value),
+ * HIP. */
+int bdlora_load_adapter(bdlora_pool_t pool, int32_t slot, int32_t rank, float scale,
+                        const uint16_t* const* A_host, const uint16_t* const* B_host);
+
+/* Mark `slot` empty; later ids naming it are invalid.  Errors: INVALID_ARG. */
+int bdlora_unload_adapter(bdlora_pool_t pool, int32_t slot);
+
+/* One projection call (Alg. 2 on one device; Alg. 1 first or second
+ * projection): out = X W_s^T + scale_a (X A_a) B_a per token.
+ * proj: index into the pool's projection list.  X: device [T x d_in];
+ * W: device [d_out_s x d_in]; ids: device int32 [T]; out: device [T x d_out_s].
+ * T: 0..max_tokens (T = 0 enqueues nothing).  Errors: INVALID_ARG, SHAPE, HIP. */
+int bdlora_forward_shard(bdlora_pool_t pool, int32_t proj, const void* X, const void* W,
+                         const int32_t* ids, int32_t T, void* out, void* stream);
+
+/* Several projection calls that share the token batch and its ids (the
+ * projections of one decoder layer), enqueued as one plan, one shrink and
+ * one base-plus-expand launch.  projs[i] indexes the pool's projection
+ * list; X[i], W[i], out[i] are device pointers as for bdlora_forward_shard
+ * (host arrays of n pointers).  n: 1..BDLORA_MAX_PROJS; the same projection
+ * may not appear twice.  Errors: as bdlora_forward_shard. */
+int bdlora_forward_layer(bdlora_pool_t pool, int32_t n, const int32_t* projs,
+                         const void* const* X, const void* const* W, void* const* out,
+                         const int32_t* ids, int32_t T, void* stream);
+
+/* Host-side plan of a batch (the integer bookkeeping of heterogeneous
+ * batching, Sec. 2 on S-LoRA), a pure host function: validates host ids
+ * against `loaded` (max_slots flags, nonzero = slot holds an adapter) and
+ * groups tokens by adapter.  Outputs (host arrays, caller-allocated):
+ *   vid[T]          validated id per token (-1 for none),
+ *   group_slot/group_start/group_count[n]  one entry per adapter in use,
+ *                   slots ascending, starts into perm,
+ *   perm[T]         tokens with an adapter, group after group, ascending
+ *                   inside each group,
+ *   *n_groups       number of groups.
+ * group arrays must hold min(T, max_slots) entries.  Returns BAD_ADAPTER
+ * (after filling the outputs, invalid ids mapped to -1) when some id other
+ * than -1 names no loaded slot. */
+int bdlora_build_plan(const int32_t* loaded, int32_t max_slots, const int32_t* ids_host, int32_t T,
+                      int32_t* vid, int32_t* group_slot, int32_t* group_start,
+                      int32_t* group_count, int32_t* perm, int32_t* n_groups);
+
+/* Run the device plan step that every forward call runs first, and copy its
+ * results to caller device buffers of the same shapes as bdlora_build_plan
+ * (n_groups is a device int32).  Inside a group the device lists tokens in
+ * ascending order as well.  Enqueued on `stream`.  Errors: INVALID_ARG,
+ * SHAPE, HIP. */
+int bdlora_plan_device(bdlora_pool_t pool, const int32_t* ids, int32_t T, int32_t* vid,
+                       int32_t* group_slot, int32_t* group_start, int32_t* group_count,
+                       int32_t* perm, int32_t* n_groups, void* stream);
+
+/* Synchronise `stream`, return the sticky device error flag in *flag (1 if
+ * some forward since the last call saw an invalid adapter id) and clear it. */
+int bdlora_get_device_error(bdlora_pool_t pool, void* stream, int32_t* flag);
+
+/* Adapter elements of one adapter of rank `rank` over the projections
+ * `projs` (true rank, no padding): sum over projections and slices of
+ * d_in*rank + rank*slice_out (the per-device factor shapes of Alg. 1/2).
+ * Pure host function. */
+int bdlora_adapter_elems(const bdlora_proj_desc* projs, int32_t n_projs, int32_t rank,
+                         int64_t* elems);
+
+/* Device memory a pool with these arguments would hold: adapter slabs
+ * (every slot sized for max_rank, ranks padded to multiples of 8) and the
+ * per-batch workspace.  Pure host function; validates the arguments as
+ * bdlora_create_pool does (except the device). */
+int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots,
+                     int32_t max_rank, int32_t max_tokens, int64_t* slab_bytes,
+                     int64_t* workspace_bytes);
+
+/* Device bytes the pool holds (adapter slabs + workspace). */
+int bdlora_pool_bytes(bdlora_pool_t pool, int64_t* bytes);
+
+/* Timing hooks.  bdlora_profile_begin(pool, n) makes the next n forward
+ * calls record HIP events around each of their three launches (plan, shrink,
+ * base-plus-expand) on the caller's stream.  bdlora_profile_end waits for
+ * them and writes the mean duration in milliseconds of each launch kind to
+ * ms[0..2] and the number of recorded calls to *n. */
+int bdlora_profile_begin(bdlora_pool_t pool, int32_t n);
+int bdlora_profile_end(bdlora_pool_t pool, float* ms, int32_t* n);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* bdlora_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BDLORA_H */

@@ -256,13 +256,20 @@ def rel_errors(y: np.ndarray, ref: np.ndarray) -> Dict[str, float]:
 
 
 def delta_errors(y: np.ndarray, y_base: np.ndarray, ref: np.ndarray,
-                 ref_base: np.ndarray) -> float:
-    """Pointwise error of the LoRA term alone, ``(y - y_base)`` against
-    ``(ref - ref_base)``, with the floor taken from the full output's rms."""
+                 ref_base: np.ndarray, rounding: float = 2.0 ** -8) -> float:
+    """Pointwise error of the LoRA term alone: ``(y - y_base)`` against
+    ``(ref - ref_base)``, with the floor taken from the full output's rms.
+
+    ``y`` and ``y_base`` are each rounded once to the output format; the
+    difference of two such numbers carries both roundings, so those
+    (``rounding`` times ``|y| + |y_base|``, 2^-8 for bfloat16 round to
+    nearest) are removed from the discrepancy before it is compared."""
     d = _f64(y) - _f64(y_base)
     dr = _f64(ref) - _f64(ref_base)
     if dr.size == 0:
         return 0.0
     rms = float(np.sqrt(np.mean(_f64(ref) ** 2)))
     floor = max(rms, np.finfo(np.float64).tiny)
-    return float(np.max(np.abs(d - dr) / np.maximum(np.abs(dr), floor)))
+    allow = rounding * (np.abs(_f64(y)) + np.abs(_f64(y_base)))
+    excess = np.maximum(np.abs(d - dr) - allow, 0.0)
+    return float(np.max(excess / np.maximum(np.abs(dr), floor)))

@@ -1,0 +1,298 @@
+"""MI355X (gfx950) block-diagonal LoRA shard library -- Python binding.
+
+A thin ctypes layer over ``libbdlora.so`` (C ABI in ``include/bdlora.h``):
+it checks and marshals arguments (tensor pointers, shapes, the current HIP
+stream) and calls the library; every step of the computation runs in the
+library's HIP kernels.  PyTorch is used only for device memory and streams.
+The library must have been built (``python -m paper_2510_23346_amd.build``);
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+__all__ = [
+    "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
+    "adapter_elems", "pool_size", "HEADER_FUNCTIONS",
+]
+
+COLUMN, ROW = 0, 1
+MAX_SLICES = 4
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libbdlora.so")
+_LIB = None
+
+STATUS = {0: "OK", -1: "INVALID_ARG", -2: "OOM", -3: "BAD_ADAPTER", -4: "SHAPE", -5: "HIP",
+          -6: "UNSUPPORTED"}
+
+# functions the C header declares, with ctypes signatures
+_c = ctypes
+_P = _c.c_void_p
+_I = _c.c_int32
+_IP = _c.POINTER(_c.c_int32)
+_LP = _c.POINTER(_c.c_int64)
+
+
+class ProjDesc(ctypes.Structure):
+    _fields_ = [("kind", _c.c_int32), ("d_in", _c.c_int32), ("n_slices", _c.c_int32),
+                ("slice_out", _c.c_int32 * MAX_SLICES)]
+
+
+_SIGS = {
+    "bdlora_create_pool": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _I, _I, _c.POINTER(_P)]),
+    "bdlora_destroy_pool": (_I, [_P]),
+    "bdlora_load_adapter": (_I, [_P, _I, _I, _c.c_float, _c.POINTER(_P), _c.POINTER(_P)]),
+    "bdlora_unload_adapter": (_I, [_P, _I]),
+    "bdlora_forward_shard": (_I, [_P, _I, _P, _P, _P, _I, _P, _P]),
+    "bdlora_forward_layer": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _I, _P]),
+    "bdlora_build_plan": (_I, [_IP, _I, _IP, _I, _IP, _IP, _IP, _IP, _IP, _IP]),
+    "bdlora_plan_device": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P]),
+    "bdlora_get_device_error": (_I, [_P, _P, _IP]),
+    "bdlora_adapter_elems": (_I, [_c.POINTER(ProjDesc), _I, _I, _LP]),
+    "bdlora_pool_size": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _I, _LP, _LP]),
+    "bdlora_pool_bytes": (_I, [_P, _LP]),
+    "bdlora_profile_begin": (_I, [_P, _I]),
+    "bdlora_profile_end": (_I, [_P, _c.POINTER(_c.c_float), _IP]),
+    "bdlora_last_error": (_c.c_char_p, []),
+}
+HEADER_FUNCTIONS = tuple(_SIGS)
+
+
+class BDLoRAError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """Load ``libbdlora.so`` (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2510_23346_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _LIB = L
+    return _LIB
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise BDLoRAError(rc, lib().bdlora_last_error().decode())
+
+
+def _descs(projs) -> Tuple[ctypes.Array, List[Tuple[int, int, Tuple[int, ...]]]]:
+    norm = []
+    for p in projs:
+        if hasattr(p, "d_in"):               # workloads.ProjSpec or similar
+            kind = ROW if getattr(p, "kind", "column") in ("row", ROW) else COLUMN
+            norm.append((kind, int(p.d_in), tuple(int(s) for s in p.slices)))
+        else:
+            kind, d_in, slices = p
+            kind = ROW if kind in ("row", ROW) else COLUMN
+            norm.append((kind, int(d_in), tuple(int(s) for s in slices)))
+    arr = (ProjDesc * max(1, len(norm)))()
+    for i, (kind, d_in, slices) in enumerate(norm):
+        if not 1 <= len(slices) <= MAX_SLICES:
+            raise ValueError("a projection has 1..4 slices")
+        arr[i].kind = kind
+        arr[i].d_in = d_in
+        arr[i].n_slices = len(slices)
+        for j, s in enumerate(slices):
+            arr[i].slice_out[j] = s
+    return arr, norm
+
+
+def adapter_elems(projs, rank: int) -> int:
+    arr, norm = _descs(projs)
+    out = _c.c_int64()
+    _check(lib().bdlora_adapter_elems(arr, len(norm), int(rank), _c.byref(out)))
+    return out.value
+
+
+def pool_size(projs, max_slots: int, max_rank: int, max_tokens: int) -> Tuple[int, int]:
+    arr, norm = _descs(projs)
+    a, b = _c.c_int64(), _c.c_int64()
+    _check(lib().bdlora_pool_size(arr, len(norm), int(max_slots), int(max_rank), int(max_tokens),
+                                  _c.byref(a), _c.byref(b)))
+    return a.value, b.value
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(_IP)
+
+
+def build_plan(loaded: Sequence[int], ids: Sequence[int]):
+    """Host plan (see ``bdlora_build_plan``).  Returns ``(status, vid,
+    groups, perm)`` with ``groups`` a list of ``(slot, start, count)``."""
+    ld = np.ascontiguousarray(np.asarray(loaded, dtype=np.int32))
+    ids = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+    T = int(ids.size)
+    G = max(1, min(T, ld.size))
+    vid = np.empty(max(T, 1), np.int32)
+    perm = np.empty(max(T, 1), np.int32)
+    gs, gst, gc = (np.empty(G, np.int32) for _ in range(3))
+    ng = _c.c_int32(0)
+    rc = lib().bdlora_build_plan(_i32p(ld), int(ld.size), _i32p(ids) if T else None, T, _i32p(vid),
+                                 _i32p(gs), _i32p(gst), _i32p(gc), _i32p(perm), _c.byref(ng))
+    if rc not in (0, -3):
+        _check(rc)
+    n = ng.value
+    groups = [(int(gs[i]), int(gst[i]), int(gc[i])) for i in range(n)]
+    nperm = sum(c for _, _, c in groups)
+    return rc, vid[:T].copy(), groups, perm[:nperm].copy()
+
+
+def _ptr(x) -> int:
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return int(x.data_ptr())
+    raise TypeError(f"expected a device tensor or an int pointer, got {type(x)}")
+
+
+def _stream_handle(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+class Pool:
+    """A GPU-resident adapter pool for a fixed list of shard projections.
+
+    ``projs``: sequence of ``(kind, d_in, slices)`` (kind "column"/"row")
+    or objects with ``kind``, ``d_in`` and ``slices`` attributes.
+    """
+
+    def __init__(self, projs, max_slots: int, max_rank: int, max_tokens: int, device: int = 0):
+        self._arr, self.projs = _descs(projs)
+        self.max_slots, self.max_rank, self.max_tokens = int(max_slots), int(max_rank), int(max_tokens)
+        self.device = int(device)
+        h = _c.c_void_p()
+        _check(lib().bdlora_create_pool(self._arr, len(self.projs), self.max_slots, self.max_rank,
+                                        self.max_tokens, self.device, _c.byref(h)))
+        self._h = h
+        self.loaded = np.zeros(self.max_slots, np.int32)
+
+    # -- lifetime ---------------------------------------------------------
+    def close(self):
+        if getattr(self, "_h", None):
+            _check(lib().bdlora_destroy_pool(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def bytes(self) -> int:
+        out = _c.c_int64()
+        _check(lib().bdlora_pool_bytes(self._h, _c.byref(out)))
+        return out.value
+
+    # -- adapters ---------------------------------------------------------
+    def load_adapter(self, slot: int, rank: int, scale: float, A, B):
+        """``A[p][s]``: uint16 bf16 bits ``[d_in, rank]``; ``B[p][s]``:
+        ``[rank, slice_out]`` (paper layout), for every projection p and
+        slice s of the pool."""
+        flatA, flatB, keep = [], [], []
+        for p, (_, d_in, slices) in enumerate(self.projs):
+            for s, n in enumerate(slices):
+                a = np.ascontiguousarray(np.asarray(A[p][s]).view(np.uint16) if rank else np.zeros((d_in, 0), np.uint16))
+                b = np.ascontiguousarray(np.asarray(B[p][s]).view(np.uint16) if rank else np.zeros((0, n), np.uint16))
+                if a.shape != (d_in, rank) or b.shape != (rank, n):
+                    raise ValueError(f"adapter factor shapes {a.shape}, {b.shape} do not match "
+                                     f"({d_in}, {rank}), ({rank}, {n})")
+                keep += [a, b]
+                flatA.append(a.ctypes.data)
+                flatB.append(b.ctypes.data)
+        pa = (_c.c_void_p * max(1, len(flatA)))(*flatA)
+        pb = (_c.c_void_p * max(1, len(flatB)))(*flatB)
+        _check(lib().bdlora_load_adapter(self._h, int(slot), int(rank), float(scale), pa, pb))
+        self.loaded[int(slot)] = 1
+        del keep
+
+    def unload_adapter(self, slot: int):
+        _check(lib().bdlora_unload_adapter(self._h, int(slot)))
+        self.loaded[int(slot)] = 0
+
+    # -- forward ----------------------------------------------------------
+    def _check_io(self, p, X, W, out, T):
+        if not 0 <= int(p) < len(self.projs):
+            return                               # the library reports the bad index
+        kind, d_in, slices = self.projs[p]
+        n = sum(slices)
+        for name, t, shape in (("X", X, (T, d_in)), ("W", W, (n, d_in)), ("out", out, (T, n))):
+            if hasattr(t, "shape"):
+                if tuple(t.shape) != shape:
+                    raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+                if t.element_size() != 2 or not t.is_contiguous():
+                    raise ValueError(f"{name} must be a contiguous 2-byte (bf16) tensor")
+
+    def forward_shard(self, proj: int, X, W, ids, out, T: Optional[int] = None, stream=None):
+        """One projection: ``out = X W^T + scale (X A) B`` per token."""
+        T = int(ids.shape[0]) if T is None else int(T)
+        self._check_io(proj, X, W, out, T)
+        _check(lib().bdlora_forward_shard(self._h, int(proj), _ptr(X), _ptr(W), _ptr(ids), T, _ptr(out),
+                                          _stream_handle(stream)))
+
+    def forward_layer(self, projs: Sequence[int], Xs, Ws, outs, ids, T: Optional[int] = None, stream=None):
+        """Several projections sharing the token batch, in one launch set."""
+        T = int(ids.shape[0]) if T is None else int(T)
+        n = len(projs)
+        for i, p in enumerate(projs):
+            self._check_io(p, Xs[i], Ws[i], outs[i], T)
+        pr = (_c.c_int32 * n)(*[int(p) for p in projs])
+        xs = (_c.c_void_p * n)(*[_ptr(x) for x in Xs])
+        ws = (_c.c_void_p * n)(*[_ptr(w) for w in Ws])
+        os_ = (_c.c_void_p * n)(*[_ptr(o) for o in outs])
+        _check(lib().bdlora_forward_layer(self._h, n, pr, xs, ws, os_, _ptr(ids), T, _stream_handle(stream)))
+
+    def plan_device(self, ids, vid, gslot, gstart, gcount, perm, n_groups, T: Optional[int] = None, stream=None):
+        T = int(ids.shape[0]) if T is None else int(T)
+        _check(lib().bdlora_plan_device(self._h, _ptr(ids), T, _ptr(vid), _ptr(gslot), _ptr(gstart),
+                                        _ptr(gcount), _ptr(perm), _ptr(n_groups), _stream_handle(stream)))
+
+    def device_error(self, stream=None) -> int:
+        f = _c.c_int32(0)
+        _check(lib().bdlora_get_device_error(self._h, _stream_handle(stream), _c.byref(f)))
+        return f.value
+
+    # -- timing hooks -----------------------------------------------------
+    def profile_begin(self, n: int):
+        _check(lib().bdlora_profile_begin(self._h, int(n)))
+
+    def profile_end(self) -> Tuple[List[float], int]:
+        ms = (_c.c_float * 3)()
+        n = _c.c_int32()
+        _check(lib().bdlora_profile_end(self._h, ms, _c.byref(n)))
+        return [ms[0], ms[1], ms[2]], n.value

@@ -1,0 +1,649 @@
+// C ABI of the BD-LoRA shard library: adapter pool, validation, host plan,
+// and the forward launch sequence (plan -> shrink -> base GEMM + expand).
+#include "bdlora.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "bdl_launch.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+#define BDL_HIP(expr)                                                                        \
+    do {                                                                                     \
+        hipError_t e_ = (expr);                                                              \
+        if (e_ != hipSuccess) return fail(BDLORA_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+constexpr long long kAlign = 128;  // elements (256 bytes)
+
+long long round_up(long long v, long long m) { return (v + m - 1) / m * m; }
+int rank8(int r) { return (r + 7) / 8 * 8; }
+
+struct ProjInfo {
+    int kind, K, S, N, zs;
+    int slice_out[bdl::kMaxSlices];
+    int slice_col[bdl::kMaxSlices + 1];
+    long long a_off, b_off;           // element offsets inside a slot
+};
+
+struct Layout {
+    int n_projs = 0;
+    ProjInfo proj[bdl::kMaxProjs];
+    int max_slots = 0, max_rank = 0, r8max = 0, max_tokens = 0;
+    long long slot_stride = 0;         // elements
+    long long slab_bytes = 0, ws_bytes = 0;
+    long long z_elems[bdl::kMaxProjs];
+};
+
+// Validates the pool arguments and computes the memory layout.
+int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int max_rank,
+                int max_tokens, Layout* L) {
+    if (!projs || !L) return fail(BDLORA_ERR_INVALID_ARG, "null projection list");
+    if (n_projs < 1 || n_projs > BDLORA_MAX_PROJS)
+        return fail(BDLORA_ERR_INVALID_ARG, "n_projs must be 1..8");
+    if (max_slots < 1 || max_slots > BDLORA_MAX_SLOTS)
+        return fail(BDLORA_ERR_INVALID_ARG, "max_slots must be 1..8192");
+    if (max_rank < 0 || max_rank > BDLORA_MAX_RANK)
+        return fail(BDLORA_ERR_INVALID_ARG, "max_rank must be 0..128");
+    if (max_tokens < 1 || max_tokens > (1 << 24))
+        return fail(BDLORA_ERR_INVALID_ARG, "max_tokens must be 1..16777216");
+    L->n_projs = n_projs;
+    L->max_slots = max_slots;
+    L->max_rank = max_rank;
+    L->r8max = std::max(8, rank8(max_rank));
+    L->max_tokens = max_tokens;
+    long long off = 0;
+    for (int p = 0; p < n_projs; ++p) {
+        const bdlora_proj_desc& d = projs[p];
+        ProjInfo& P = L->proj[p];
+        if (d.kind != BDLORA_COLUMN && d.kind != BDLORA_ROW)
+            return fail(BDLORA_ERR_INVALID_ARG, "projection kind must be COLUMN or ROW");
+        if (d.d_in < 32 || d.d_in % 32 || d.d_in > (1 << 20))
+            return fail(BDLORA_ERR_SHAPE, "d_in must be a positive multiple of 32");
+        if (d.n_slices < 1 || d.n_slices > BDLORA_MAX_SLICES)
+            return fail(BDLORA_ERR_SHAPE, "n_slices must be 1..4");
+        P.kind = d.kind;
+        P.K = d.d_in;
+        P.S = d.n_slices;
+        int col = 0;
+        for (int s = 0; s < bdl::kMaxSlices; ++s) {
+            P.slice_out[s] = s < d.n_slices ? d.slice_out[s] : 0;
+            P.slice_col[s] = col;
+            if (s < d.n_slices) {
+                if (d.slice_out[s] < 16 || d.slice_out[s] % 16 || d.slice_out[s] > (1 << 20))
+                    return fail(BDLORA_ERR_SHAPE, "slice_out must be a positive multiple of 16");
+                col += d.slice_out[s];
+            }
+        }
+        P.slice_col[bdl::kMaxSlices] = col;
+        for (int s = d.n_slices; s <= bdl::kMaxSlices; ++s) P.slice_col[s] = col;
+        P.N = col;
+        P.zs = P.S * L->r8max;
+        P.a_off = off;
+        off = round_up(off + (long long)P.S * L->r8max * P.K, kAlign);
+        P.b_off = off;
+        off = round_up(off + (long long)P.N * L->r8max, kAlign);
+        L->z_elems[p] = 2LL * max_tokens * P.zs;      // hi and lo planes
+    }
+    L->slot_stride = off;
+    L->slab_bytes = (long long)max_slots * off * 2;
+    long long ws = 0;
+    ws += 8LL * max_tokens * 4;                                   // vid, perm (+ slack)
+    ws += 4LL * (max_slots + 2) * 4 + 2 * 4;                      // group tables, meta, err
+    for (int p = 0; p < n_projs; ++p) ws += L->z_elems[p] * 2;
+    ws += max_slots * 12LL;                                       // slot tables
+    L->ws_bytes = ws;
+    return BDLORA_OK;
+}
+
+struct DeviceGuard {
+    int old = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&old) == hipSuccess && hipSetDevice(dev) == hipSuccess) ok = true;
+    }
+    ~DeviceGuard() {
+        if (old >= 0) (void)hipSetDevice(old);
+    }
+};
+
+}  // namespace
+
+struct bdlora_pool {
+    int device = 0;
+    Layout L;
+    uint16_t* d_slabs = nullptr;
+    int* d_r8 = nullptr;
+    float* d_scale = nullptr;
+    int* d_loaded = nullptr;
+    std::vector<int> h_rank, h_r8, h_loaded;
+    std::vector<float> h_scale;
+    int* d_vid = nullptr;
+    int* d_perm = nullptr;
+    int* d_gslot = nullptr;
+    int* d_gstart = nullptr;
+    int* d_gcount = nullptr;
+    int* d_gitem = nullptr;
+    int* d_meta = nullptr;
+    int* d_err = nullptr;
+    uint16_t* d_Z[bdl::kMaxProjs] = {};
+    uint16_t* d_stage = nullptr;
+    long long stage_elems = 0;
+    hipStream_t load_stream = nullptr;
+    long long bytes = 0;
+    // timing hooks
+    int prof_left = 0;
+    int prof_used = 0;
+    std::vector<hipEvent_t> prof_ev;      // 6 per recorded call
+};
+
+namespace {
+
+void free_pool(bdlora_pool* P) {
+    if (!P) return;
+    auto f = [](void* p) {
+        if (p) (void)hipFree(p);
+    };
+    f(P->d_slabs);
+    f(P->d_r8);
+    f(P->d_scale);
+    f(P->d_loaded);
+    f(P->d_vid);
+    f(P->d_perm);
+    f(P->d_gslot);
+    f(P->d_gstart);
+    f(P->d_gcount);
+    f(P->d_gitem);
+    f(P->d_meta);
+    f(P->d_err);
+    for (auto z : P->d_Z) f(z);
+    f(P->d_stage);
+    for (auto e : P->prof_ev) (void)hipEventDestroy(e);
+    if (P->load_stream) (void)hipStreamDestroy(P->load_stream);
+    delete P;
+}
+
+template <typename T>
+int dev_alloc(T** p, long long elems, long long* total) {
+    const size_t bytes = (size_t)std::max(1LL, elems) * sizeof(T);
+    hipError_t e = hipMalloc((void**)p, bytes);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return fail(e == hipErrorOutOfMemory ? BDLORA_ERR_OOM : BDLORA_ERR_HIP,
+                    std::string("hipMalloc of ") + std::to_string(bytes) + " bytes: " + hipGetErrorString(e));
+    }
+    *total += (long long)bytes;
+    return BDLORA_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* bdlora_last_error(void) { return g_err.c_str(); }
+
+int bdlora_adapter_elems(const bdlora_proj_desc* projs, int32_t n_projs, int32_t rank, int64_t* elems) {
+    if (!elems) return fail(BDLORA_ERR_INVALID_ARG, "null output");
+    if (rank < 0) return fail(BDLORA_ERR_INVALID_ARG, "negative rank");
+    Layout L;
+    int rc = make_layout(projs, n_projs, 1, 0, 1, &L);
+    if (rc) return rc;
+    long long e = 0;
+    for (int p = 0; p < n_projs; ++p)
+        for (int s = 0; s < L.proj[p].S; ++s)
+            e += (long long)L.proj[p].K * rank + (long long)rank * L.proj[p].slice_out[s];
+    *elems = e;
+    return BDLORA_OK;
+}
+
+int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots, int32_t max_rank,
+                     int32_t max_tokens, int64_t* slab_bytes, int64_t* workspace_bytes) {
+    Layout L;
+    int rc = make_layout(projs, n_projs, max_slots, max_rank, max_tokens, &L);
+    if (rc) return rc;
+    if (slab_bytes) *slab_bytes = L.slab_bytes;
+    if (workspace_bytes) *workspace_bytes = L.ws_bytes;
+    return BDLORA_OK;
+}
+
+int bdlora_build_plan(const int32_t* loaded, int32_t max_slots, const int32_t* ids, int32_t T, int32_t* vid,
+                      int32_t* gslot, int32_t* gstart, int32_t* gcount, int32_t* perm, int32_t* n_groups) {
+    if (T < 0) return fail(BDLORA_ERR_INVALID_ARG, "negative T");
+    if (max_slots < 1 || max_slots > BDLORA_MAX_SLOTS) return fail(BDLORA_ERR_INVALID_ARG, "bad max_slots");
+    if (!loaded || !n_groups || (T > 0 && (!ids || !vid || !gslot || !gstart || !gcount || !perm)))
+        return fail(BDLORA_ERR_INVALID_ARG, "null pointer");
+    std::vector<int> cnt(max_slots, 0);
+    bool bad = false;
+    for (int t = 0; t < T; ++t) {
+        const int a = ids[t];
+        const bool ok = a >= 0 && a < max_slots && loaded[a] != 0;
+        if (!ok && a != -1) bad = true;
+        vid[t] = ok ? a : -1;
+        if (ok) ++cnt[a];
+    }
+    int g = 0, off = 0;
+    std::vector<int> cursor(max_slots, 0);
+    for (int s = 0; s < max_slots; ++s) {
+        cursor[s] = off;
+        if (cnt[s] > 0) {
+            gslot[g] = s;
+            gstart[g] = off;
+            gcount[g] = cnt[s];
+            ++g;
+        }
+        off += cnt[s];
+    }
+    for (int t = 0; t < T; ++t)
+        if (vid[t] >= 0) perm[cursor[vid[t]]++] = t;
+    *n_groups = g;
+    if (bad) return fail(BDLORA_ERR_BAD_ADAPTER, "an id names no loaded adapter slot");
+    return BDLORA_OK;
+}
+
+int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots, int32_t max_rank,
+                       int32_t max_tokens, int32_t device, bdlora_pool_t* out) {
+    if (!out) return fail(BDLORA_ERR_INVALID_ARG, "null output handle");
+    *out = nullptr;
+    Layout L;
+    int rc = make_layout(projs, n_projs, max_slots, max_rank, max_tokens, &L);
+    if (rc) return rc;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
+        (void)hipGetLastError();
+        return fail(BDLORA_ERR_UNSUPPORTED, "no HIP device");
+    }
+    if (device < 0 || device >= ndev) return fail(BDLORA_ERR_INVALID_ARG, "bad device index");
+    hipDeviceProp_t prop;
+    BDL_HIP(hipGetDeviceProperties(&prop, device));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(BDLORA_ERR_UNSUPPORTED, std::string("device is ") + prop.gcnArchName + ", need gfx950");
+    DeviceGuard guard(device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+
+    bdlora_pool* P = new bdlora_pool();
+    P->device = device;
+    P->L = L;
+    long long tot = 0;
+    const int S = max_slots, MT = max_tokens;
+#define BDL_TRY(x)         \
+    do {                   \
+        int r_ = (x);      \
+        if (r_) {          \
+            free_pool(P);  \
+            return r_;     \
+        }                  \
+    } while (0)
+    BDL_TRY(dev_alloc(&P->d_slabs, (long long)S * L.slot_stride, &tot));
+    BDL_TRY(dev_alloc(&P->d_r8, S, &tot));
+    BDL_TRY(dev_alloc(&P->d_scale, S, &tot));
+    BDL_TRY(dev_alloc(&P->d_loaded, S, &tot));
+    BDL_TRY(dev_alloc(&P->d_vid, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
+    BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
+    BDL_TRY(dev_alloc(&P->d_gcount, S + 1, &tot));
+    BDL_TRY(dev_alloc(&P->d_gitem, S + 2, &tot));
+    BDL_TRY(dev_alloc(&P->d_meta, 4, &tot));
+    BDL_TRY(dev_alloc(&P->d_err, 1, &tot));
+    long long stage = 0;
+    for (int p = 0; p < n_projs; ++p) {
+        BDL_TRY(dev_alloc(&P->d_Z[p], L.z_elems[p], &tot));
+        const ProjInfo& pi = L.proj[p];
+        stage = std::max(stage, (long long)pi.S * pi.K * std::max(1, max_rank) + (long long)std::max(1, max_rank) * pi.N);
+    }
+    BDL_TRY(dev_alloc(&P->d_stage, stage, &tot));
+    P->stage_elems = stage;
+    P->bytes = tot;
+    auto hipz = [&](void* p, size_t n) -> int {
+        hipError_t e = hipMemset(p, 0, n);
+        if (e != hipSuccess) {
+            free_pool(P);
+            return fail(BDLORA_ERR_HIP, std::string("hipMemset: ") + hipGetErrorString(e));
+        }
+        return BDLORA_OK;
+    };
+    // zero everything the kernels may read: slabs (padding), tables, Z, flags
+    if (int r = hipz(P->d_slabs, (size_t)S * L.slot_stride * 2)) return r;
+    if (int r = hipz(P->d_r8, (size_t)S * 4)) return r;
+    if (int r = hipz(P->d_scale, (size_t)S * 4)) return r;
+    if (int r = hipz(P->d_loaded, (size_t)S * 4)) return r;
+    if (int r = hipz(P->d_err, 4)) return r;
+    if (int r = hipz(P->d_meta, 16)) return r;
+    for (int p = 0; p < n_projs; ++p)
+        if (int r = hipz(P->d_Z[p], (size_t)std::max(1LL, L.z_elems[p]) * 2)) return r;
+    hipError_t e = hipStreamCreateWithFlags(&P->load_stream, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+        free_pool(P);
+        return fail(BDLORA_ERR_HIP, std::string("hipStreamCreate: ") + hipGetErrorString(e));
+    }
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        free_pool(P);
+        return fail(BDLORA_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(e));
+    }
+#undef BDL_TRY
+    P->h_rank.assign(S, 0);
+    P->h_r8.assign(S, 0);
+    P->h_loaded.assign(S, 0);
+    P->h_scale.assign(S, 0.f);
+    *out = P;
+    return BDLORA_OK;
+}
+
+int bdlora_destroy_pool(bdlora_pool_t P) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    DeviceGuard guard(P->device);
+    (void)hipDeviceSynchronize();
+    free_pool(P);
+    return BDLORA_OK;
+}
+
+int bdlora_pool_bytes(bdlora_pool_t P, int64_t* bytes) {
+    if (!P || !bytes) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    *bytes = P->bytes;
+    return BDLORA_OK;
+}
+
+static int upload_slot_tables(bdlora_pool_t P, int slot) {
+    BDL_HIP(hipMemcpyAsync(P->d_r8 + slot, &P->h_r8[slot], 4, hipMemcpyHostToDevice, P->load_stream));
+    BDL_HIP(hipMemcpyAsync(P->d_scale + slot, &P->h_scale[slot], 4, hipMemcpyHostToDevice, P->load_stream));
+    BDL_HIP(hipMemcpyAsync(P->d_loaded + slot, &P->h_loaded[slot], 4, hipMemcpyHostToDevice, P->load_stream));
+    BDL_HIP(hipStreamSynchronize(P->load_stream));
+    return BDLORA_OK;
+}
+
+int bdlora_load_adapter(bdlora_pool_t P, int32_t slot, int32_t rank, float scale, const uint16_t* const* A_host,
+                        const uint16_t* const* B_host) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    const Layout& L = P->L;
+    if (slot < 0 || slot >= L.max_slots) return fail(BDLORA_ERR_INVALID_ARG, "slot out of range");
+    if (rank < 0 || rank > L.max_rank) return fail(BDLORA_ERR_INVALID_ARG, "rank out of range 0..max_rank");
+    if (!std::isfinite(scale)) return fail(BDLORA_ERR_INVALID_ARG, "scale must be finite");
+    if (rank > 0 && (!A_host || !B_host)) return fail(BDLORA_ERR_INVALID_ARG, "null factor arrays");
+    const int r8 = rank8(rank);
+    // host-side checks first: every factor present and finite
+    int k = 0;
+    for (int p = 0; p < L.n_projs; ++p) {
+        const ProjInfo& pi = L.proj[p];
+        for (int s = 0; s < pi.S; ++s, ++k) {
+            if (rank == 0) continue;
+            const uint16_t* a = A_host[k];
+            const uint16_t* b = B_host[k];
+            if (!a || !b) return fail(BDLORA_ERR_INVALID_ARG, "null factor pointer");
+            const long long na = (long long)pi.K * rank, nb = (long long)rank * pi.slice_out[s];
+            for (long long i = 0; i < na; ++i)
+                if ((a[i] & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in A");
+            for (long long i = 0; i < nb; ++i)
+                if ((b[i] & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in B");
+        }
+    }
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    // mark the slot empty while it is rewritten
+    P->h_loaded[slot] = 0;
+    if (int rc = upload_slot_tables(P, slot)) return rc;
+    k = 0;
+    for (int p = 0; p < L.n_projs; ++p) {
+        const ProjInfo& pi = L.proj[p];
+        uint16_t* slab = P->d_slabs + (long long)slot * L.slot_stride;
+        if (rank > 0) {
+            long long off = 0;
+            for (int s = 0; s < pi.S; ++s) {
+                const long long n = (long long)pi.K * rank;
+                BDL_HIP(hipMemcpyAsync(P->d_stage + off, A_host[k + s], n * 2, hipMemcpyHostToDevice, P->load_stream));
+                off += n;
+            }
+            for (int s = 0; s < pi.S; ++s) {
+                const long long n = (long long)rank * pi.slice_out[s];
+                BDL_HIP(hipMemcpyAsync(P->d_stage + off, B_host[k + s], n * 2, hipMemcpyHostToDevice, P->load_stream));
+                off += n;
+            }
+            BDL_HIP(bdl::launch_pack(slab + pi.a_off, slab + pi.b_off, P->d_stage, pi.K, pi.S, pi.slice_out, rank,
+                                     r8, P->load_stream));
+            BDL_HIP(hipStreamSynchronize(P->load_stream));   // stage is reused by the next projection
+        }
+        k += pi.S;
+    }
+    P->h_rank[slot] = rank;
+    P->h_r8[slot] = r8;
+    P->h_scale[slot] = scale;
+    P->h_loaded[slot] = 1;
+    return upload_slot_tables(P, slot);
+}
+
+int bdlora_unload_adapter(bdlora_pool_t P, int32_t slot) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    if (slot < 0 || slot >= P->L.max_slots) return fail(BDLORA_ERR_INVALID_ARG, "slot out of range");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    P->h_loaded[slot] = 0;
+    P->h_rank[slot] = 0;
+    P->h_r8[slot] = 0;
+    return upload_slot_tables(P, slot);
+}
+
+static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::PlanArgs* a, int mts) {
+    a->ids = ids;
+    a->T = T;
+    a->loaded = P->d_loaded;
+    a->max_slots = P->L.max_slots;
+    a->mts = mts;
+    a->vid = P->d_vid;
+    a->perm = P->d_perm;
+    a->gslot = P->d_gslot;
+    a->gstart = P->d_gstart;
+    a->gcount = P->d_gcount;
+    a->gitem = P->d_gitem;
+    a->meta = P->d_meta;
+    a->err = P->d_err;
+}
+
+static int shrink_mb(int T) { return T <= 512 ? 1 : 4; }
+
+static int gemm_mb(int T) { return T <= 16 ? 1 : (T <= 32 ? 2 : 4); }
+
+static int gemm_nb(int /*T*/) { return 2; }
+
+int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
+                         const void* const* W, void* const* out, const int32_t* ids, int32_t T, void* stream) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    const Layout& L = P->L;
+    if (n < 1 || n > BDLORA_MAX_PROJS) return fail(BDLORA_ERR_INVALID_ARG, "n must be 1..8");
+    if (!projs || !X || !W || !out) return fail(BDLORA_ERR_INVALID_ARG, "null pointer array");
+    if (T < 0 || T > L.max_tokens) return fail(BDLORA_ERR_SHAPE, "T outside 0..max_tokens");
+    bool seen[bdl::kMaxProjs] = {};
+    for (int i = 0; i < n; ++i) {
+        if (projs[i] < 0 || projs[i] >= L.n_projs) return fail(BDLORA_ERR_INVALID_ARG, "projection index out of range");
+        if (seen[projs[i]]) return fail(BDLORA_ERR_INVALID_ARG, "projection listed twice");
+        seen[projs[i]] = true;
+        if (T > 0 && (!X[i] || !W[i] || !out[i])) return fail(BDLORA_ERR_INVALID_ARG, "null tensor pointer");
+        if (T > 0 && (!aligned16(X[i]) || !aligned16(W[i]) || !aligned16(out[i])))
+            return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
+    }
+    if (T == 0) return BDLORA_OK;
+    if (!ids) return fail(BDLORA_ERR_INVALID_ARG, "null ids");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+
+    const int mbs = shrink_mb(T), mts = 16 * mbs;
+    const int mb = gemm_mb(T), nb = gemm_nb(T);
+    const int MT = bdl::gemm_tile_rows(mb), NT = bdl::gemm_tile_cols(nb);
+
+    bdl::FwdArgs fa;
+    std::memset(&fa, 0, sizeof(fa));
+    // heavy projections first so the long-running tiles start early
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+        return (long long)L.proj[projs[x]].K * L.proj[projs[x]].N > (long long)L.proj[projs[y]].K * L.proj[projs[y]].N;
+    });
+    int n_loaded = 0;
+    for (int v : P->h_loaded) n_loaded += v != 0;
+    const int tiles_m = (T + MT - 1) / MT;
+    int tile = 0, cch = 1;
+    for (int q = 0; q < n; ++q) {
+        const int i = order[q];
+        const ProjInfo& pi = L.proj[projs[i]];
+        bdl::ProjLaunch& pl = fa.p[q];
+        pl.X = (const uint16_t*)X[i];
+        pl.W = (const uint16_t*)W[i];
+        pl.out = (uint16_t*)out[i];
+        pl.Z = P->d_Z[projs[i]];
+        pl.zplane = (long long)L.max_tokens * pi.zs;
+        pl.K = pi.K;
+        pl.N = pi.N;
+        pl.n_slices = pi.S;
+        pl.zs = pi.zs;
+        for (int s = 0; s <= bdl::kMaxSlices; ++s) pl.slice_col[s] = pi.slice_col[s];
+        pl.a_off = pi.a_off;
+        pl.b_off = pi.b_off;
+        pl.tiles_n = (pi.N + NT - 1) / NT;
+        pl.tile_base = tile;
+        tile += tiles_m * pl.tiles_n;
+        cch = std::max(cch, (pi.S * L.r8max + bdl::shrink_tile_cols() - 1) / bdl::shrink_tile_cols());
+    }
+    fa.n_proj = n;
+    fa.T = T;
+    fa.pool = P->d_slabs;
+    fa.slot_stride = L.slot_stride;
+    fa.max_slots = L.max_slots;
+    fa.r8max = L.r8max;
+    fa.r8 = P->d_r8;
+    fa.scale = P->d_scale;
+    fa.vid = P->d_vid;
+    fa.perm = P->d_perm;
+    fa.gslot = P->d_gslot;
+    fa.gstart = P->d_gstart;
+    fa.gcount = P->d_gcount;
+    fa.gitem = P->d_gitem;
+    fa.meta = P->d_meta;
+    fa.items_bound = std::min(T, std::max(n_loaded, 1)) + (T + mts - 1) / mts;
+    fa.cchunks = cch;
+    fa.mts = mts;
+    fa.tiles_m = tiles_m;
+    fa.total_tiles = tile;
+
+    bdl::PlanArgs pa;
+    fill_plan_args(P, ids, T, &pa, mts);
+
+    hipEvent_t* ev = nullptr;
+    if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * 6 <= P->prof_ev.size()) {
+        ev = &P->prof_ev[(size_t)P->prof_used * 6];
+        ++P->prof_used;
+        --P->prof_left;
+    }
+    if (ev) BDL_HIP(hipEventRecord(ev[0], s));
+    BDL_HIP(bdl::launch_plan(pa, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[1], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[2], s));
+    BDL_HIP(bdl::launch_shrink(fa, mbs, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[3], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[4], s));
+    BDL_HIP(bdl::launch_gemm(fa, mb, nb, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[5], s));
+    return BDLORA_OK;
+}
+
+int bdlora_forward_shard(bdlora_pool_t P, int32_t proj, const void* X, const void* W, const int32_t* ids, int32_t T,
+                         void* out, void* stream) {
+    const void* xs[1] = {X};
+    const void* ws[1] = {W};
+    void* os[1] = {out};
+    int32_t pr[1] = {proj};
+    return bdlora_forward_layer(P, 1, pr, xs, ws, os, ids, T, stream);
+}
+
+int bdlora_plan_device(bdlora_pool_t P, const int32_t* ids, int32_t T, int32_t* vid, int32_t* gslot, int32_t* gstart,
+                       int32_t* gcount, int32_t* perm, int32_t* n_groups, void* stream) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    if (T < 0 || T > P->L.max_tokens) return fail(BDLORA_ERR_SHAPE, "T outside 0..max_tokens");
+    if (!n_groups || (T > 0 && (!ids || !vid || !gslot || !gstart || !gcount || !perm)))
+        return fail(BDLORA_ERR_INVALID_ARG, "null pointer");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+    bdl::PlanArgs pa;
+    fill_plan_args(P, ids, T, &pa, 16 * shrink_mb(T));
+    BDL_HIP(bdl::launch_plan(pa, s));
+    const int G = std::min(T, P->L.max_slots);
+    if (T > 0) {
+        BDL_HIP(hipMemcpyAsync(vid, P->d_vid, (size_t)T * 4, hipMemcpyDeviceToDevice, s));
+        BDL_HIP(hipMemcpyAsync(perm, P->d_perm, (size_t)T * 4, hipMemcpyDeviceToDevice, s));
+    }
+    if (G > 0) {
+        BDL_HIP(hipMemcpyAsync(gslot, P->d_gslot, (size_t)G * 4, hipMemcpyDeviceToDevice, s));
+        BDL_HIP(hipMemcpyAsync(gstart, P->d_gstart, (size_t)G * 4, hipMemcpyDeviceToDevice, s));
+        BDL_HIP(hipMemcpyAsync(gcount, P->d_gcount, (size_t)G * 4, hipMemcpyDeviceToDevice, s));
+    }
+    BDL_HIP(hipMemcpyAsync(n_groups, P->d_meta, 4, hipMemcpyDeviceToDevice, s));
+    return BDLORA_OK;
+}
+
+int bdlora_get_device_error(bdlora_pool_t P, void* stream, int32_t* flag) {
+    if (!P || !flag) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+    int32_t v = 0;
+    BDL_HIP(hipMemcpyAsync(&v, P->d_err, 4, hipMemcpyDeviceToHost, s));
+    BDL_HIP(hipStreamSynchronize(s));
+    const int32_t zero = 0;
+    BDL_HIP(hipMemcpyAsync(P->d_err, &zero, 4, hipMemcpyHostToDevice, s));
+    BDL_HIP(hipStreamSynchronize(s));
+    *flag = v;
+    return BDLORA_OK;
+}
+
+int bdlora_profile_begin(bdlora_pool_t P, int32_t n) {
+    if (!P || n < 0 || n > 100000) return fail(BDLORA_ERR_INVALID_ARG, "bad arguments");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    while (P->prof_ev.size() < (size_t)n * 6) {
+        hipEvent_t e;
+        BDL_HIP(hipEventCreate(&e));
+        P->prof_ev.push_back(e);
+    }
+    P->prof_left = n;
+    P->prof_used = 0;
+    return BDLORA_OK;
+}
+
+int bdlora_profile_end(bdlora_pool_t P, float* ms, int32_t* n) {
+    if (!P || !ms || !n) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    double sum[3] = {0, 0, 0};
+    for (int i = 0; i < P->prof_used; ++i) {
+        hipEvent_t* ev = &P->prof_ev[(size_t)i * 6];
+        BDL_HIP(hipEventSynchronize(ev[5]));
+        for (int k = 0; k < 3; ++k) {
+            float t = 0.f;
+            BDL_HIP(hipEventElapsedTime(&t, ev[2 * k], ev[2 * k + 1]));
+            sum[k] += t;
+        }
+    }
+    for (int k = 0; k < 3; ++k) ms[k] = P->prof_used ? (float)(sum[k] / P->prof_used) : 0.f;
+    *n = P->prof_used;
+    P->prof_left = 0;
+    P->prof_used = 0;
+    return BDLORA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,116 @@
+"""CPU checks of the C ABI library: it loads, exports every function the
+header declares, and its pure host functions (plan, sizing, element counts)
+agree with the oracle.  No GPU call is made here."""
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2510_23346_amd as bd
+import workloads as wl
+from oracle import costs, plan as oplan
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(bd.lib_path()):
+        from paper_2510_23346_amd.build import build
+        build()
+    return bd.lib()
+
+
+def _header_functions():
+    text = open(os.path.join(ROOT, "include", "bdlora.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:int|const char\s*\*)\s+(bdlora_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_function(L):
+    names = _header_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(bd.HEADER_FUNCTIONS) == names
+
+
+def test_adapter_elems_reproduce_paper_counts(L):
+    # per-shard elements x N shards x layers = the paper's BD-LoRA counts
+    for model, tp, r_total, mill in [("llama-3.1-8b", 8, 32, 36.2), ("llama-3.1-8b", 8, 512, 578.8),
+                                     ("llama-3.1-70b", 8, 512, 2883.6), ("llama-3.2-1b", 4, 32, 11.1)]:
+        m = wl.MODELS[model]
+        per_shard = bd.adapter_elems(wl.model_projs(model, tp), r_total // tp)
+        assert abs(per_shard * tp * m.n_layers / 1e6 - mill) <= 0.05
+        assert per_shard * tp * m.n_layers == costs.bd_model_params(m.d_h, m.d_i, m.d_kv, m.n_layers, r_total, tp)
+
+
+def test_pool_size(L):
+    projs = wl.model_projs("llama-3.1-8b", 8)
+    slab, ws = bd.pool_size(projs, 32, 16, 64)
+    per_slot = slab // 32
+    assert slab % 32 == 0 and per_slot * 32 == slab
+    assert per_slot >= 2 * bd.adapter_elems(projs, 16)          # padded layout holds the adapter
+    assert per_slot <= 2 * bd.adapter_elems(projs, 16) * 1.01 + 32 * 256
+    assert ws > 0
+    slab4, _ = bd.pool_size(wl.model_projs("llama-3.1-70b", 8), 512, 64, 4288)
+    assert slab4 > 4e9                                           # 512 slots at rank 64
+
+
+@pytest.mark.parametrize("bad", [
+    [("column", 48, (16,))],          # d_in not a multiple of 32
+    [("column", 64, (24,))],          # slice not a multiple of 16
+    [("column", 64, (16, 16, 16, 16, 16))],
+])
+def test_shape_errors(L, bad):
+    with pytest.raises((bd.BDLoRAError, ValueError)):
+        bd.pool_size(bad, 4, 8, 16)
+
+
+def test_argument_errors(L):
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.pool_size([("column", 64, (16,))], 0, 8, 16)
+    assert e.value.code == -1
+    with pytest.raises(bd.BDLoRAError):
+        bd.pool_size([("column", 64, (16,))], 4, 129, 16)
+    assert "max_rank" in bd.lib().bdlora_last_error().decode()
+
+
+def test_host_plan_exhaustive(L):
+    loaded = np.array([1, 0, 1], np.int32)
+    for T in range(0, 6):
+        for ids in itertools.product([-2, -1, 0, 1, 2, 3], repeat=T) if T <= 3 else \
+                [np.random.default_rng(T * 100 + k).integers(-2, 4, size=T) for k in range(200)]:
+            ids = np.asarray(ids, np.int32)
+            rc, vid, groups, perm = bd.build_plan(loaded, ids)
+            ovid, oerr = oplan.validate(ids, loaded)
+            otab, operm = oplan.groups(ovid)
+            assert rc == (-3 if oerr else 0)
+            assert np.array_equal(vid, ovid)
+            assert groups == [tuple(x) for x in otab]
+            assert np.array_equal(perm, operm)
+
+
+def test_host_plan_large(L):
+    rng = np.random.default_rng(1)
+    loaded = (rng.random(512) < 0.9).astype(np.int32)
+    ids = rng.integers(-1, 520, size=5000).astype(np.int32)
+    rc, vid, groups, perm = bd.build_plan(loaded, ids)
+    ovid, oerr = oplan.validate(ids, loaded)
+    otab, operm = oplan.groups(ovid)
+    assert groups == [tuple(x) for x in otab] and np.array_equal(perm, operm)
+    assert rc == -3 and oerr
+
+
+def test_no_gpu_means_a_loud_error(L):
+    try:
+        import torch
+        has_gpu = torch.cuda.is_available()
+    except Exception:
+        has_gpu = False
+    if has_gpu:
+        pytest.skip("a GPU is present")
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.Pool([("column", 64, (16,))], 4, 8, 16)
+    assert e.value.code in (-6, -5)

@@ -1,0 +1,314 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Error rule (bf16 inputs, fp32 accumulation, bf16 output): every element must
+satisfy |y - ref| <= 1e-2 * max(|ref|, rms(ref)).  The LoRA term alone
+(y - y_base against ref - ref_base) is held to the same rule with the full
+output's rms as floor, after allowing the two bf16 output roundings the
+difference of two GPU outputs carries (2^-8 (|y| + |y_base|)).  Integer plan
+results are compared exactly.
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from workloads.gpu import DeviceLayer, device_to_float, load_adapters, make_pool
+from oracle import bdlora, plan as oplan
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-2
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2510_23346_amd as bd
+    bd.lib()                                   # loud failure if the library is missing
+    return torch
+
+
+def _run_layer(torch, spec, layer, pool, T=None):
+    dl = DeviceLayer(layer, T=T)
+    pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, dl.out, dl.ids)
+    torch.cuda.synchronize()
+    return dl, dl.outputs()
+
+
+def _base_only(torch, spec, dl, pool):
+    ids_none = torch.full_like(dl.ids, -1)
+    outs = [torch.empty_like(o) for o in dl.out]
+    pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, outs, ids_none)
+    torch.cuda.synchronize()
+    return [device_to_float(o) for o in outs]
+
+
+def _check(y, ref, y_base=None, ref_base=None, what=""):
+    e = bdlora.rel_errors(y, ref)
+    assert e["pointwise"] <= TOL, f"{what}: {e}"
+    if y_base is not None:
+        d = bdlora.delta_errors(y, y_base, ref, ref_base)
+        assert d <= TOL, f"{what}: LoRA-term error {d}"
+    return e
+
+
+def _oracle_base(layer, rows=None):
+    outs = []
+    for pi in layer.projs:
+        X = pi.X if rows is None else pi.X[rows]
+        outs.append(X.astype(np.float64) @ pi.W.astype(np.float64))
+    return outs
+
+
+# ---------------------------------------------------------------------------
+# small shapes: several tiles, ragged tails, odd ranks, id -1, rank 0
+# ---------------------------------------------------------------------------
+
+TINY_RANKS = [0, 1, 3, 8, 16, 24, 5, 32]
+
+
+@pytest.mark.parametrize("T", [1, 5, 16, 37, 64, 100, 300, 700])
+def test_tiny_parity(torch_cuda, T):
+    torch = torch_cuda
+    rng = np.random.default_rng(T)
+    ids = rng.integers(-1, len(TINY_RANKS), size=T)
+    spec = wl.custom_workload(f"tiny-{T}", wl.tiny_projs(), T, TINY_RANKS,
+                              scales=[0.5 + 0.25 * i for i in range(len(TINY_RANKS))], ids=ids, seed=T)
+    layer = wl.draw_layer(spec, slots=range(len(TINY_RANKS)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(TINY_RANKS)), cache=layer.adapters)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    yb = _base_only(torch, spec, dl, pool)
+    refs = bdlora.layer_forward(layer)
+    rb = _oracle_base(layer)
+    for p in range(len(spec.projs)):
+        _check(ys[p], refs[p], yb[p], rb[p], what=f"T={T} proj={spec.projs[p].name}")
+    assert pool.device_error() == 0
+    pool.close()
+
+
+def test_base_only_rows_equal_no_adapter_rows(torch_cuda):
+    torch = torch_cuda
+    T = 48
+    ids = np.array([(-1 if t % 3 == 0 else (0 if t % 3 == 1 else 1)) for t in range(T)])
+    spec = wl.custom_workload("r0", wl.tiny_projs(), T, [0, 8], ids=ids, seed=3)
+    layer = wl.draw_layer(spec, slots=[0, 1])
+    pool = make_pool(spec)
+    load_adapters(pool, spec, [0, 1], cache=layer.adapters)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    yb = _base_only(torch, spec, dl, pool)
+    for p in range(len(spec.projs)):
+        rows = np.nonzero(ids <= 0)[0]          # id -1 and the rank-0 adapter
+        assert np.array_equal(ys[p][rows], yb[p][rows])     # value equality (+0 == -0)
+        _check(yb[p], _oracle_base(layer)[p], what="base only")
+    pool.close()
+
+
+def test_deterministic_and_shard_equals_layer(torch_cuda):
+    torch = torch_cuda
+    T = 70
+    spec = wl.custom_workload("det", wl.tiny_projs(), T, [8, 16, 4], seed=5)
+    layer = wl.draw_layer(spec, slots=[0, 1, 2])
+    pool = make_pool(spec)
+    load_adapters(pool, spec, [0, 1, 2], cache=layer.adapters)
+    dl, y1 = _run_layer(torch, spec, layer, pool)
+    _, y2 = _run_layer(torch, spec, layer, pool)
+    for a, b in zip(y1, y2):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    for p in range(len(spec.projs)):
+        o = torch.empty_like(dl.out[p])
+        pool.forward_shard(p, dl.X[p], dl.W[p], dl.ids, o)
+        torch.cuda.synchronize()
+        assert np.array_equal(device_to_float(o).view(np.uint32), y1[p].view(np.uint32))
+    pool.close()
+
+
+# ---------------------------------------------------------------------------
+# plan: bit-exact against the host plan and the oracle; error flag
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,n_slots", [(1, 4), (64, 32), (333, 20), (4288, 512)])
+def test_plan_device_bit_exact(torch_cuda, T, n_slots):
+    torch = torch_cuda
+    import paper_2510_23346_amd as bd
+    rng = np.random.default_rng(T + n_slots)
+    ids = rng.integers(-1, n_slots, size=T).astype(np.int32)
+    ids[::17] = n_slots + 3                  # out of range
+    ids[1::29] = -7                          # negative, not -1
+    unloaded = {1, n_slots - 1}
+    projs = [("column", 64, (16,))]
+    pool = bd.Pool(projs, n_slots, 8, T)
+    z = np.zeros((64, 2), np.uint16)
+    zb = np.zeros((2, 16), np.uint16)
+    for s in range(n_slots):
+        if s not in unloaded:
+            pool.load_adapter(s, 2, 1.0, [[z]], [[zb]])
+    loaded = pool.loaded.copy()
+    ids_d = torch.from_numpy(ids).cuda()
+    G = min(T, n_slots)
+    vid = torch.empty(T, dtype=torch.int32, device="cuda")
+    perm = torch.empty(T, dtype=torch.int32, device="cuda")
+    gs, gst, gc = (torch.empty(G, dtype=torch.int32, device="cuda") for _ in range(3))
+    ng = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pool.plan_device(ids_d, vid, gs, gst, gc, perm, ng)
+    torch.cuda.synchronize()
+    ovid, oerr = oplan.validate(ids, loaded)
+    otab, operm = oplan.groups(ovid)
+    n = int(ng.item())
+    assert np.array_equal(vid.cpu().numpy(), ovid)
+    assert n == len(otab)
+    got = list(zip(gs.cpu().numpy()[:n].tolist(), gst.cpu().numpy()[:n].tolist(), gc.cpu().numpy()[:n].tolist()))
+    assert got == [tuple(x) for x in otab]
+    assert np.array_equal(perm.cpu().numpy()[:len(operm)], operm)
+    rc, hvid, htab, hperm = bd.build_plan(loaded, ids)
+    assert rc == (-3 if oerr else 0)
+    assert np.array_equal(hvid, ovid) and htab == [tuple(x) for x in otab] and np.array_equal(hperm, operm)
+    assert pool.device_error() == int(oerr)
+    assert pool.device_error() == 0          # cleared by the read
+    pool.close()
+
+
+def test_invalid_ids_are_base_only_and_flagged(torch_cuda):
+    torch = torch_cuda
+    T = 40
+    ids = np.array([t % 4 for t in range(T)])
+    ids[5] = 99
+    ids[6] = 3                                # slot 3 will be unloaded
+    spec = wl.custom_workload("bad", wl.tiny_projs(), T, [8, 8, 8, 8], ids=ids, seed=7)
+    layer = wl.draw_layer(spec, slots=[0, 1, 2, 3])
+    pool = make_pool(spec)
+    load_adapters(pool, spec, [0, 1, 2, 3], cache=layer.adapters)
+    pool.unload_adapter(3)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    assert pool.device_error() == 1
+    vid, _ = oplan.validate(ids, pool.loaded)
+    layer.ids = vid
+    refs = bdlora.layer_forward(layer)
+    for p in range(len(spec.projs)):
+        _check(ys[p], refs[p], what="invalid ids")
+    pool.close()
+
+
+def test_empty_batch_and_errors(torch_cuda):
+    torch = torch_cuda
+    import paper_2510_23346_amd as bd
+    spec = wl.custom_workload("err", wl.tiny_projs(), 8, [8], seed=1)
+    layer = wl.draw_layer(spec, slots=[0])
+    pool = make_pool(spec)
+    load_adapters(pool, spec, [0], cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    e = torch.empty((0, spec.projs[0].d_out), dtype=torch.bfloat16, device="cuda")
+    pool.forward_shard(0, dl.X[0][:0], dl.W[0], dl.ids[:0], e, T=0)
+    xp, wp, op = dl.X[0].data_ptr(), dl.W[0].data_ptr(), dl.out[0].data_ptr()
+    with pytest.raises(bd.BDLoRAError) as e:
+        pool.forward_shard(0, xp, wp, dl.ids, op, T=9)                          # T > max_tokens
+    assert e.value.code == -4
+    with pytest.raises(bd.BDLoRAError) as e:
+        pool.forward_shard(5, xp, wp, dl.ids, op, T=8)                          # no such projection
+    assert e.value.code == -1
+    with pytest.raises(bd.BDLoRAError) as e:
+        pool.forward_shard(0, xp + 2, wp, dl.ids, op, T=8)                      # misaligned X
+    assert e.value.code == -1
+    with pytest.raises(ValueError):
+        pool.forward_shard(0, dl.X[0], dl.W[0], dl.ids, dl.out[0], T=9)         # binding shape check
+    A9 = [[np.zeros((ps.d_in, 9), np.uint16) for _ in ps.slices] for ps in spec.projs]
+    B9 = [[np.zeros((9, n), np.uint16) for n in ps.slices] for ps in spec.projs]
+    with pytest.raises(bd.BDLoRAError) as e:
+        pool.load_adapter(0, 9, 1.0, A9, B9)                                    # rank > max_rank
+    assert e.value.code == -1
+    bad = [[a.copy() for a in row] for row in layer.adapters[0].A_bits]
+    bad[0][0][0, 0] = 0x7FC0                                                    # NaN
+    with pytest.raises(bd.BDLoRAError):
+        pool.load_adapter(0, 8, 1.0, bad, layer.adapters[0].B_bits)
+    pool.close()
+
+
+# ---------------------------------------------------------------------------
+# the N shards of one layer, run one after another on one GPU (Sec. 3)
+# ---------------------------------------------------------------------------
+
+def test_all_shards_reassemble_the_unsharded_layer(torch_cuda):
+    torch = torch_cuda
+    import paper_2510_23346_amd as bd
+    from workloads import bf16_round
+    rng = np.random.default_rng(42)
+    N, S, d, di, r_tot = 4, 24, 128, 256, 32
+    bf = lambda shape, sc: bf16_round(rng.standard_normal(shape).astype(np.float32) * sc)
+    Xb, X = bf((S, d), 1.0)
+    W1b, W1 = bf((d, di), d ** -0.5)            # column layer d -> di
+    A1b, A1 = bf((d, r_tot), d ** -0.5)
+    B1b, B1 = bf((r_tot // N, di), (r_tot // N) ** -0.5)     # compact block-diagonal B
+    W2b, W2 = bf((di, d), di ** -0.5)           # row layer di -> d
+    A2b, A2 = bf((di, r_tot // N), di ** -0.5)               # compact block-diagonal A
+    B2b, B2 = bf((r_tot, d), (r_tot // N) ** -0.5)
+    gamma = 2.0
+    ids = torch.zeros(S, dtype=torch.int32, device="cuda")
+    col_parts, row_sum = [], np.zeros((S, d))
+    Y1 = np.zeros((S, di), np.float32)
+    for i, ((a1, b1), (a1b, b1b)) in enumerate(zip(bdlora.column_shards(A1, B1, N),
+                                                 bdlora.column_shards(A1b, B1b, N))):
+        n_s = di // N
+        pool = bd.Pool([("column", d, (n_s,))], 1, r_tot // N, S)
+        pool.load_adapter(0, r_tot // N, gamma, [[np.ascontiguousarray(a1b)]], [[np.ascontiguousarray(b1b)]])
+        Xd = torch.from_numpy(Xb.view(np.int16)).cuda().view(torch.bfloat16)
+        Wd = torch.from_numpy(np.ascontiguousarray(W1b[:, i * n_s:(i + 1) * n_s].T).view(np.int16)).cuda().view(torch.bfloat16)
+        out = torch.empty((S, n_s), dtype=torch.bfloat16, device="cuda")
+        pool.forward_shard(0, Xd, Wd, ids, out)
+        torch.cuda.synchronize()
+        col_parts.append(device_to_float(out))
+        pool.close()
+    y_col = np.concatenate(col_parts, axis=1)
+    _check(y_col, bdlora.column_full(X, W1, A1, B1, N, gamma), what="column shards")
+    for i, ((a2, b2), (a2b, b2b)) in enumerate(zip(bdlora.row_shards(A2, B2, N), bdlora.row_shards(A2b, B2b, N))):
+        k_s = di // N
+        pool = bd.Pool([("row", k_s, (d,))], 1, r_tot // N, S)
+        pool.load_adapter(0, r_tot // N, gamma, [[np.ascontiguousarray(a2b)]], [[np.ascontiguousarray(b2b)]])
+        Xs = np.ascontiguousarray(bf16_round(y_col[:, i * k_s:(i + 1) * k_s])[0])
+        Xd = torch.from_numpy(Xs.view(np.int16)).cuda().view(torch.bfloat16)
+        Wd = torch.from_numpy(np.ascontiguousarray(W2b[i * k_s:(i + 1) * k_s, :].T).view(np.int16)).cuda().view(torch.bfloat16)
+        out = torch.empty((S, d), dtype=torch.bfloat16, device="cuda")
+        pool.forward_shard(0, Xd, Wd, ids, out)
+        torch.cuda.synchronize()
+        row_sum += device_to_float(out)
+        pool.close()
+    Y1r = bf16_round(y_col)[1]
+    _check(row_sum, bdlora.row_full(Y1r, W2, A2, B2, N, gamma), what="row partial sum")
+
+
+# ---------------------------------------------------------------------------
+# the five benchmark workloads at full size
+# ---------------------------------------------------------------------------
+
+def _sample_rows(ids, k, seed):
+    T = ids.size
+    rng = np.random.default_rng(seed)
+    rows = set(rng.choice(T, size=min(k, T), replace=False).tolist())
+    rows |= {0, T - 1}
+    change = np.nonzero(np.diff(ids) != 0)[0]
+    rows |= set(change.tolist()) | set((change + 1).tolist())
+    return np.array(sorted(rows))
+
+
+@pytest.mark.parametrize("index", [0, 1, 2, 3, 4])
+def test_workload_parity(torch_cuda, index):
+    torch = torch_cuda
+    spec = wl.workload(index)
+    ids = wl.draw_ids(spec)
+    active = sorted(int(s) for s in np.unique(ids) if s >= 0)
+    layer = wl.draw_layer(spec, slots=active)
+    pool = make_pool(spec)
+    load_adapters(pool, spec, active, cache=layer.adapters)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    yb = _base_only(torch, spec, dl, pool)
+    if spec.T <= 512:
+        rows = np.arange(spec.T)
+        refs = bdlora.layer_forward(layer)
+    else:
+        rows = _sample_rows(ids, 96, index)
+        refs = bdlora.layer_forward_rows(layer, rows)
+    rbase = _oracle_base(layer, rows)
+    for p in range(len(spec.projs)):
+        _check(ys[p][rows], refs[p], yb[p][rows], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
+        # every output is finite and the unsampled rows were written
+        assert np.all(np.isfinite(ys[p]))
+    assert pool.device_error() == 0
+    pool.close()

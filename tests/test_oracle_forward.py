@@ -233,3 +233,16 @@ def test_planted_mistakes_fail_the_brute_force_pin(kind):
     yb = bdlora.brute_force(X, W, ids, ad, sl)
     ym = _mutant(kind)(X, W, ids, ad, sl)
     assert not np.allclose(ym, yb, rtol=1e-9, atol=1e-9)
+
+
+def test_delta_error_rule_allows_only_output_rounding():
+    from workloads import bf16_round
+    rng = np.random.default_rng(3)
+    ref_base = rng.standard_normal(500) * 2
+    ref = ref_base + rng.standard_normal(500)
+    y = bf16_round(ref)[1].astype(np.float64)
+    yb = bf16_round(ref_base)[1].astype(np.float64)
+    assert bdlora.delta_errors(y, yb, ref, ref_base) == 0.0      # rounding alone passes
+    y_bad = y.copy()
+    y_bad[7] += 0.1                                              # a real 0.1 error does not
+    assert bdlora.delta_errors(y_bad, yb, ref, ref_base) > 0.01
