@@ -22,10 +22,12 @@
  *  - Element type of X, W_s, out and of adapter factors: bfloat16, passed as
  *    16-bit patterns (uint16_t on the host, any 2-byte type on the device).
  *    Products accumulate in fp32; out is rounded once to bf16 (nearest-even).
- *  - Layouts are row-major.  X: [T x d_in].  W_s: [d_out_s x d_in] (the
- *    nn.Linear weight layout, d_in contiguous).  out: [T x d_out_s], slices
- *    side by side.  Adapter factors are given in the paper's layout:
- *    A: [d_in x rank], B: [rank x slice_out] per slice.
+ *  - Layouts.  X: [T x d_in] row-major.  out: [T x d_out_s] row-major,
+ *    slices side by side.  Base weights are packed once, before serving, by
+ *    bdlora_pack_weight from the nn.Linear layout [d_out_s x d_in] into the
+ *    matrix-core fragment layout the kernels stream (same size); forward
+ *    calls take the packed weight.  Adapter factors are given in the paper's
+ *    layout: A: [d_in x rank], B: [rank x slice_out] per slice.
  *  - Adapter ids: int32, one per token; -1 = no adapter (base only).  An id
  *    that is out of range or names an empty slot is treated as -1 and raises
  *    the pool's sticky device error flag (see bdlora_get_device_error).
@@ -111,10 +113,19 @@ int bdlora_load_adapter(bdlora_pool_t pool, int32_t slot, int32_t rank, float sc
 /* Mark `slot` empty; later ids naming it are invalid.  Errors: INVALID_ARG. */
 int bdlora_unload_adapter(bdlora_pool_t pool, int32_t slot);
 
+/* Pack a base weight W [N x K] (nn.Linear layout, row-major, bf16, device)
+ * into W_packed (device, N*K elements, not overlapping W): 16-row blocks of
+ * 32-wide k-steps, each stored as the 1 KB operand of one gfx950 bf16 MFMA
+ * (element [(rb*(K/32) + ks)*512 + lane*8 + i] = W[16 rb + lane%16]
+ * [32 ks + 8 (lane/16) + i]).  N: multiple of 16; K: multiple of 32.
+ * Enqueued on `stream`.  Errors: INVALID_ARG, SHAPE, HIP. */
+int bdlora_pack_weight(const void* W, void* W_packed, int32_t N, int32_t K, void* stream);
+
 /* One projection call (Alg. 2 on one device; Alg. 1 first or second
  * projection): out = X W_s^T + scale_a (X A_a) B_a per token.
  * proj: index into the pool's projection list.  X: device [T x d_in];
- * W: device [d_out_s x d_in]; ids: device int32 [T]; out: device [T x d_out_s].
+ * W: device, the base weight [d_out_s x d_in] packed by bdlora_pack_weight;
+ * ids: device int32 [T]; out: device [T x d_out_s].
  * T: 0..max_tokens (T = 0 enqueues nothing).  Errors: INVALID_ARG, SHAPE, HIP. */
 int bdlora_forward_shard(bdlora_pool_t pool, int32_t proj, const void* X, const void* W,
                          const int32_t* ids, int32_t T, void* out, void* stream);

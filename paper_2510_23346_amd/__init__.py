@@ -17,7 +17,7 @@ import numpy as np
 
 __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
-    "adapter_elems", "pool_size", "HEADER_FUNCTIONS",
+    "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS",
 ]
 
 COLUMN, ROW = 0, 1
@@ -52,6 +52,7 @@ _SIGS = {
     "bdlora_build_plan": (_I, [_IP, _I, _IP, _I, _IP, _IP, _IP, _IP, _IP, _IP]),
     "bdlora_plan_device": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P]),
     "bdlora_get_device_error": (_I, [_P, _P, _IP]),
+    "bdlora_pack_weight": (_I, [_P, _P, _I, _I, _P]),
     "bdlora_adapter_elems": (_I, [_c.POINTER(ProjDesc), _I, _I, _LP]),
     "bdlora_pool_size": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _I, _LP, _LP]),
     "bdlora_pool_bytes": (_I, [_P, _LP]),
@@ -128,6 +129,18 @@ def pool_size(projs, max_slots: int, max_rank: int, max_tokens: int) -> Tuple[in
     _check(lib().bdlora_pool_size(arr, len(norm), int(max_slots), int(max_rank), int(max_tokens),
                                   _c.byref(a), _c.byref(b)))
     return a.value, b.value
+
+
+def pack_weight(W, W_packed=None, stream=None):
+    """Pack a base weight ``W [N, K]`` (nn.Linear layout, bf16 device tensor)
+    into the fragment layout forward calls take; returns the packed tensor."""
+    N, K = int(W.shape[0]), int(W.shape[1])
+    if W_packed is None:
+        W_packed = W.new_empty((N, K))
+    if tuple(W_packed.shape) != (N, K) or not W.is_contiguous() or not W_packed.is_contiguous():
+        raise ValueError("W and W_packed must be contiguous [N, K] tensors")
+    _check(lib().bdlora_pack_weight(_ptr(W), _ptr(W_packed), N, K, _stream_handle(stream)))
+    return W_packed
 
 
 def _i32p(a: np.ndarray):

@@ -46,6 +46,7 @@ struct Layout {
     long long slot_stride = 0;         // elements
     long long slab_bytes = 0, ws_bytes = 0;
     long long z_elems[bdl::kMaxProjs];
+    long long xp_elems[bdl::kMaxProjs];
 };
 
 // Validates the pool arguments and computes the memory layout.
@@ -92,18 +93,22 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
         for (int s = d.n_slices; s <= bdl::kMaxSlices; ++s) P.slice_col[s] = col;
         P.N = col;
         P.zs = P.S * L->r8max;
-        P.a_off = off;
-        off = round_up(off + (long long)P.S * L->r8max * P.K, kAlign);
+        P.a_off = off;                                   // packed A^T_cat, rows padded to 16
+        off = round_up(off + round_up((long long)P.S * L->r8max, 16) * P.K, kAlign);
         P.b_off = off;
         off = round_up(off + (long long)P.N * L->r8max, kAlign);
         L->z_elems[p] = 2LL * max_tokens * P.zs;      // hi and lo planes
+        L->xp_elems[p] = round_up(max_tokens, 16) * P.K;
     }
     L->slot_stride = off;
     L->slab_bytes = (long long)max_slots * off * 2;
     long long ws = 0;
     ws += 8LL * max_tokens * 4;                                   // vid, perm (+ slack)
     ws += 4LL * (max_slots + 2) * 4 + 2 * 4;                      // group tables, meta, err
-    for (int p = 0; p < n_projs; ++p) ws += L->z_elems[p] * 2;
+    ws += ((long long)max_slots + max_tokens / 16 + 2) * 16;      // shrink items
+    ws += std::max(((long long)max_tokens / 16 + 1) * (2LL * L->r8max + 64),
+                   ((long long)max_tokens / 64 + 1) * (8LL * L->r8max + 64)) * 4;   // tile octets
+    for (int p = 0; p < n_projs; ++p) ws += (L->z_elems[p] + L->xp_elems[p]) * 2;
     ws += max_slots * 12LL;                                       // slot tables
     L->ws_bytes = ws;
     return BDLORA_OK;
@@ -136,10 +141,13 @@ struct bdlora_pool {
     int* d_gslot = nullptr;
     int* d_gstart = nullptr;
     int* d_gcount = nullptr;
-    int* d_gitem = nullptr;
+    int4* d_items = nullptr;
+    int* d_tile_oct = nullptr;
+    long long items_cap = 0, oct_elems = 0;
     int* d_meta = nullptr;
     int* d_err = nullptr;
     uint16_t* d_Z[bdl::kMaxProjs] = {};
+    uint16_t* d_Xp[bdl::kMaxProjs] = {};
     uint16_t* d_stage = nullptr;
     long long stage_elems = 0;
     hipStream_t load_stream = nullptr;
@@ -166,10 +174,12 @@ void free_pool(bdlora_pool* P) {
     f(P->d_gslot);
     f(P->d_gstart);
     f(P->d_gcount);
-    f(P->d_gitem);
+    f(P->d_items);
+    f(P->d_tile_oct);
     f(P->d_meta);
     f(P->d_err);
     for (auto z : P->d_Z) f(z);
+    for (auto x : P->d_Xp) f(x);
     f(P->d_stage);
     for (auto e : P->prof_ev) (void)hipEventDestroy(e);
     if (P->load_stream) (void)hipStreamDestroy(P->load_stream);
@@ -298,12 +308,17 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gcount, S + 1, &tot));
-    BDL_TRY(dev_alloc(&P->d_gitem, S + 2, &tot));
+    P->items_cap = (long long)S + MT / 16 + 2;
+    BDL_TRY(dev_alloc(&P->d_items, P->items_cap, &tot));
+    P->oct_elems = ((long long)MT / 16 + 1) * (16LL * L.r8max / 8 + 64);
+    P->oct_elems = std::max(P->oct_elems, ((long long)MT / 64 + 1) * (64LL * L.r8max / 8 + 64));
+    BDL_TRY(dev_alloc(&P->d_tile_oct, P->oct_elems, &tot));
     BDL_TRY(dev_alloc(&P->d_meta, 4, &tot));
     BDL_TRY(dev_alloc(&P->d_err, 1, &tot));
     long long stage = 0;
     for (int p = 0; p < n_projs; ++p) {
         BDL_TRY(dev_alloc(&P->d_Z[p], L.z_elems[p], &tot));
+        BDL_TRY(dev_alloc(&P->d_Xp[p], L.xp_elems[p], &tot));
         const ProjInfo& pi = L.proj[p];
         stage = std::max(stage, (long long)pi.S * pi.K * std::max(1, max_rank) + (long long)std::max(1, max_rank) * pi.N);
     }
@@ -414,8 +429,8 @@ int bdlora_load_adapter(bdlora_pool_t P, int32_t slot, int32_t rank, float scale
                 BDL_HIP(hipMemcpyAsync(P->d_stage + off, B_host[k + s], n * 2, hipMemcpyHostToDevice, P->load_stream));
                 off += n;
             }
-            BDL_HIP(bdl::launch_pack(slab + pi.a_off, slab + pi.b_off, P->d_stage, pi.K, pi.S, pi.slice_out, rank,
-                                     r8, P->load_stream));
+            BDL_HIP(bdl::launch_pack_adapter(slab + pi.a_off, slab + pi.b_off, P->d_stage, pi.K, pi.S,
+                                             pi.slice_out, rank, r8, P->load_stream));
             BDL_HIP(hipStreamSynchronize(P->load_stream));   // stage is reused by the next projection
         }
         k += pi.S;
@@ -438,27 +453,49 @@ int bdlora_unload_adapter(bdlora_pool_t P, int32_t slot) {
     return upload_slot_tables(P, slot);
 }
 
-static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::PlanArgs* a, int mts) {
+// Kernel shapes by batch size: decode batches use short row tiles and narrow
+// shrink items (more workgroups), prefill batches the largest tiles.
+struct Shapes {
+    int smb, snb;   // shrink row / column blocks of 16
+    int gmb, gnb;   // base GEMM row / column blocks of 16
+};
+
+// Column blocks per base-GEMM tile: the widest tile (least re-reading of the
+// activations) that still leaves enough workgroups to occupy the chip.
+static Shapes pick_shapes(int T, long long col_blocks = 0) {
+    Shapes k;
+    k.smb = T <= 512 ? 1 : 4;
+    k.snb = T <= 512 ? 1 : 4;
+    k.gmb = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
+    const long long row_tiles = (T + 16 * k.gmb - 1) / (16 * k.gmb);
+    const long long blocks = col_blocks * row_tiles;
+    k.gnb = blocks >= 4 * 192 ? 4 : (blocks >= 2 * 192 ? 2 : 1);
+    return k;
+}
+
+static int oct_cap(const Layout& L, int gemm_mt) { return gemm_mt * L.r8max / 8 + 64; }
+
+static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::PrepArgs* a, const Shapes& k) {
     a->ids = ids;
     a->T = T;
     a->loaded = P->d_loaded;
+    a->r8 = P->d_r8;
     a->max_slots = P->L.max_slots;
-    a->mts = mts;
+    a->mts = 16 * k.smb;
+    a->gemm_mt = 16 * k.gmb;
+    a->oct_cap = oct_cap(P->L, 16 * k.gmb);
     a->vid = P->d_vid;
     a->perm = P->d_perm;
     a->gslot = P->d_gslot;
     a->gstart = P->d_gstart;
     a->gcount = P->d_gcount;
-    a->gitem = P->d_gitem;
+    a->items = P->d_items;
+    a->tile_oct = P->d_tile_oct;
     a->meta = P->d_meta;
     a->err = P->d_err;
+    a->n_jobs = 0;
+    a->total_frags = 0;
 }
-
-static int shrink_mb(int T) { return T <= 512 ? 1 : 4; }
-
-static int gemm_mb(int T) { return T <= 16 ? 1 : (T <= 32 ? 2 : 4); }
-
-static int gemm_nb(int /*T*/) { return 2; }
 
 int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
                          const void* const* W, void* const* out, const int32_t* ids, int32_t T, void* stream) {
@@ -482,9 +519,11 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
 
-    const int mbs = shrink_mb(T), mts = 16 * mbs;
-    const int mb = gemm_mb(T), nb = gemm_nb(T);
-    const int MT = bdl::gemm_tile_rows(mb), NT = bdl::gemm_tile_cols(nb);
+    long long col_blocks = 0;
+    for (int i = 0; i < n; ++i) col_blocks += L.proj[projs[i]].N / 16;
+    const Shapes k = pick_shapes(T, col_blocks);
+    const int mts = 16 * k.smb, nts = 16 * k.snb;
+    const int MT = 16 * k.gmb, NT = 16 * k.gnb;
 
     bdl::FwdArgs fa;
     std::memset(&fa, 0, sizeof(fa));
@@ -503,6 +542,7 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
         const ProjInfo& pi = L.proj[projs[i]];
         bdl::ProjLaunch& pl = fa.p[q];
         pl.X = (const uint16_t*)X[i];
+        pl.Xp = P->d_Xp[projs[i]];
         pl.W = (const uint16_t*)W[i];
         pl.out = (uint16_t*)out[i];
         pl.Z = P->d_Z[projs[i]];
@@ -517,31 +557,41 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
         pl.tiles_n = (pi.N + NT - 1) / NT;
         pl.tile_base = tile;
         tile += tiles_m * pl.tiles_n;
-        cch = std::max(cch, (pi.S * L.r8max + bdl::shrink_tile_cols() - 1) / bdl::shrink_tile_cols());
+        cch = std::max(cch, (pi.S * L.r8max + nts - 1) / nts);
     }
     fa.n_proj = n;
     fa.T = T;
     fa.pool = P->d_slabs;
     fa.slot_stride = L.slot_stride;
-    fa.max_slots = L.max_slots;
     fa.r8max = L.r8max;
-    fa.r8 = P->d_r8;
     fa.scale = P->d_scale;
     fa.vid = P->d_vid;
     fa.perm = P->d_perm;
-    fa.gslot = P->d_gslot;
-    fa.gstart = P->d_gstart;
-    fa.gcount = P->d_gcount;
-    fa.gitem = P->d_gitem;
+    fa.items = P->d_items;
     fa.meta = P->d_meta;
     fa.items_bound = std::min(T, std::max(n_loaded, 1)) + (T + mts - 1) / mts;
     fa.cchunks = cch;
-    fa.mts = mts;
+    fa.tile_oct = P->d_tile_oct;
+    fa.oct_cap = oct_cap(L, MT);
     fa.tiles_m = tiles_m;
     fa.total_tiles = tile;
+    if (fa.items_bound > P->items_cap || (long long)tiles_m * fa.oct_cap > P->oct_elems)
+        return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
 
-    bdl::PlanArgs pa;
-    fill_plan_args(P, ids, T, &pa, mts);
+    bdl::PrepArgs pa;
+    fill_plan_args(P, ids, T, &pa, k);
+    int frags = 0;
+    for (int q = 0; q < n; ++q) {
+        bdl::PackJob& J = pa.jobs[q];
+        J.src = fa.p[q].X;
+        J.dst = P->d_Xp[projs[order[q]]];
+        J.rows = T;
+        J.K = fa.p[q].K;
+        J.frag_base = frags;
+        frags += ((T + 15) / 16) * (J.K / 32);
+    }
+    pa.n_jobs = n;
+    pa.total_frags = frags;
 
     hipEvent_t* ev = nullptr;
     if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * 6 <= P->prof_ev.size()) {
@@ -550,13 +600,13 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
         --P->prof_left;
     }
     if (ev) BDL_HIP(hipEventRecord(ev[0], s));
-    BDL_HIP(bdl::launch_plan(pa, s));
+    BDL_HIP(bdl::launch_prep(pa, s));
     if (ev) BDL_HIP(hipEventRecord(ev[1], s));
     if (ev) BDL_HIP(hipEventRecord(ev[2], s));
-    BDL_HIP(bdl::launch_shrink(fa, mbs, s));
+    BDL_HIP(bdl::launch_shrink(fa, k.smb, k.snb, s));
     if (ev) BDL_HIP(hipEventRecord(ev[3], s));
     if (ev) BDL_HIP(hipEventRecord(ev[4], s));
-    BDL_HIP(bdl::launch_gemm(fa, mb, nb, s));
+    BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
     if (ev) BDL_HIP(hipEventRecord(ev[5], s));
     return BDLORA_OK;
 }
@@ -579,9 +629,9 @@ int bdlora_plan_device(bdlora_pool_t P, const int32_t* ids, int32_t T, int32_t* 
     DeviceGuard guard(P->device);
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
-    bdl::PlanArgs pa;
-    fill_plan_args(P, ids, T, &pa, 16 * shrink_mb(T));
-    BDL_HIP(bdl::launch_plan(pa, s));
+    bdl::PrepArgs pa;
+    fill_plan_args(P, ids, T, &pa, pick_shapes(T));
+    BDL_HIP(bdl::launch_prep(pa, s));
     const int G = std::min(T, P->L.max_slots);
     if (T > 0) {
         BDL_HIP(hipMemcpyAsync(vid, P->d_vid, (size_t)T * 4, hipMemcpyDeviceToDevice, s));
@@ -593,6 +643,15 @@ int bdlora_plan_device(bdlora_pool_t P, const int32_t* ids, int32_t T, int32_t* 
         BDL_HIP(hipMemcpyAsync(gcount, P->d_gcount, (size_t)G * 4, hipMemcpyDeviceToDevice, s));
     }
     BDL_HIP(hipMemcpyAsync(n_groups, P->d_meta, 4, hipMemcpyDeviceToDevice, s));
+    return BDLORA_OK;
+}
+
+int bdlora_pack_weight(const void* W, void* W_packed, int32_t N, int32_t K, void* stream) {
+    if (!W || !W_packed) return fail(BDLORA_ERR_INVALID_ARG, "null pointer");
+    if (W == W_packed) return fail(BDLORA_ERR_INVALID_ARG, "packing cannot run in place");
+    if (N < 16 || N % 16 || K < 32 || K % 32) return fail(BDLORA_ERR_SHAPE, "N must be a multiple of 16, K of 32");
+    if (!aligned16(W) || !aligned16(W_packed)) return fail(BDLORA_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
+    BDL_HIP(bdl::launch_pack_rows((const uint16_t*)W, (uint16_t*)W_packed, N, K, (hipStream_t)stream));
     return BDLORA_OK;
 }
 

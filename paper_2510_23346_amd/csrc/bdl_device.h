@@ -40,36 +40,71 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
     return (uint16_t)(u >> 16);
 }
 
+// wave index as a scalar (uniform) value
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// One wave accumulates acc[MB][NB] (MB row blocks x NB col blocks of 16) over
-// the k-steps (32 wide) ks = ks0 + j*stride + u, u < U, while ks < ks_end.
-// ap[rb] / bp[cb] already point at this lane's row / col and k offset.
-template <int MB, int NB, int U>
-__device__ __forceinline__ void mma_ksteps(f32x4 (&acc)[MB][NB], const uint16_t* const (&ap)[MB],
-                                           const uint16_t* const (&bp)[NB], int ks0, int ks_end,
-                                           int stride) {
-    for (int ks = ks0; ks < ks_end; ks += stride) {
-        u32x4 a[U][MB], b[U][NB];
+// MFMA fragment layout.  A K-contiguous matrix with rows padded to a
+// multiple of 16 is stored as 1 KB fragments, fragment (rb, ks) holding the
+// operand of one 16-row block for one 32-wide k-step exactly as the 64 lanes
+// load it: element [(rb * KS + ks) * 512 + lane * 8 + i] is
+// M[16 rb + lane % 16][32 ks + 8 (lane / 16) + i].  Weights, packed
+// activations and the pool's A^T factors use it, so every operand load of a
+// wave reads 1 KB of contiguous memory.
+constexpr int kFrag = 512;                  // elements per fragment
+
+__device__ __forceinline__ size_t frag_index(int rb, int ks, int KS) {
+    return ((size_t)rb * KS + ks) * kFrag;
+}
+
+// Wave-level K loop over the contiguous k-step range [k0, k0 + n), n >= 1.
+// ap[rb] / bp[cb] point at this lane's element of k-step 0; consecutive
+// k-steps are sa / sb elements apart.  D stages of loads stay in flight: the
+// loads of k-step i + D are issued right after the MFMAs of k-step i.  Load
+// addresses are clamped to the last k-step, so the steady-state loop issues
+// the same loads every iteration and each load's only consumer is the next
+// iteration (the compiler cannot sink it next to its use); the last n % D
+// k-steps are consumed after the loop.
+template <int MB, int NB, int D>
+__device__ __forceinline__ void mma_range(f32x4 (&acc)[MB][NB], const uint16_t* const (&ap)[MB],
+                                          const uint16_t* const (&bp)[NB], int k0, int n, int sa,
+                                          int sb) {
+    u32x4 a[D][MB], b[D][NB];
+    const int last = k0 + n - 1;
+    auto load = [&](int d, int ks) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (ks + u < ks_end) {
+        for (int cb = 0; cb < NB; ++cb) b[d][cb] = ld16(bp[cb] + (size_t)ks * sb);
 #pragma unroll
-                for (int cb = 0; cb < NB; ++cb) b[u][cb] = ld16(bp[cb] + (size_t)(ks + u) * 32);
+        for (int rb = 0; rb < MB; ++rb) a[d][rb] = ld16(ap[rb] + (size_t)ks * sa);
+    };
+    auto comp = [&](int d) {
 #pragma unroll
-                for (int rb = 0; rb < MB; ++rb) a[u][rb] = ld16(ap[rb] + (size_t)(ks + u) * 32);
-            }
-        }
+        for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (ks + u < ks_end) {
+            for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = mfma(a[d][rb], b[d][cb], acc[rb][cb]);
+    };
 #pragma unroll
-                for (int rb = 0; rb < MB; ++rb)
+    for (int d = 0; d < D; ++d) load(d, min(k0 + d, last));
+    int i = 0;
+    for (; i + D <= n; i += D) {
 #pragma unroll
-                    for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = mfma(a[u][rb], b[u][cb], acc[rb][cb]);
-            }
+        for (int d = 0; d < D; ++d) {
+            comp(d);
+            load(d, min(k0 + i + d + D, last));
         }
     }
+    const int rem = n - i;
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+        if (d < rem) comp(d);
+}
+
+// Contiguous k-step range of wave w when KS k-steps are split over kWaves.
+__device__ __forceinline__ void wave_krange(int KS, int w, int* k0, int* n) {
+    const int q = KS / kWaves, r = KS - q * kWaves;
+    *k0 = w * q + min(w, r);
+    *n = q + (w < r ? 1 : 0);
 }
 
 // Deterministic reduction of the 8 waves' accumulators of one MT x NT tile
@@ -79,7 +114,7 @@ __device__ __forceinline__ void mma_ksteps(f32x4 (&acc)[MB][NB], const uint16_t*
 template <int MB, int NB>
 __device__ __forceinline__ void reduce_waves(f32x4 (&acc)[MB][NB], float* red) {
     constexpr int NT = NB * 16, MT = MB * 16, LD = NT + 4, REG = MT * LD;
-    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    const int w = wave_id(), l = threadIdx.x & 63;
     auto put = [&](float* dst) {
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb)

@@ -3,50 +3,112 @@
 // A forward launch of one token batch over P projections (all sharing the
 // tokens' adapter ids) runs three kernels on the caller's stream:
 //
-//  1. plan_kernel   -- validates ids and groups tokens by adapter (counting
-//                      sort over slots, one workgroup).  Integer work only.
+//  1. prep_kernel   -- workgroup 0 plans the batch: validates ids and groups
+//                      tokens by adapter (counting sort over slots), and
+//                      writes ready-to-use work descriptors for the other two
+//                      kernels (shrink items; per row tile, the adapter
+//                      octets to expand).  The other workgroups copy the
+//                      activations X into the MFMA fragment layout.
 //  2. shrink_kernel -- Z = scale * X A for every adapter group (the LoRA
 //                      "shrink", matmul_3 / matmul_5 of the paper's Fig. 2/3,
-//                      line "Z <- X A" of Alg. 1 and Alg. 2).  Each group's
+//                      step "Z <- X A" of Alg. 1 and Alg. 2).  Each group's
 //                      factor A^T is streamed once; the group's token rows are
 //                      gathered.
 //  3. gemm_kernel   -- out = X W_s^T + Z B for each output tile: the base
 //                      product (matmul_1 / matmul_2) with the LoRA "expand"
 //                      (matmul_4 / matmul_6) and the add (add_1 / add_2)
 //                      fused, one bf16 store per output (Alg. 1 / Alg. 2,
-//                      lines "Y_adapter <- Z B" and "Y <- Y + Y_adapter").
+//                      steps "Y_adapter <- Z B" and "Y <- Y + Y_adapter").
 //
 // Both GEMM-shaped kernels use 8 waves per workgroup that split the K loop
-// and reduce through LDS in a fixed order, so results are bitwise
-// reproducible.  The expand runs as extra MFMA k-steps: for the adapters
-// present in the tile, 8-rank pieces ("octets") of B^T are the B operand
-// and the matching Z entries (zero for tokens of other adapters) the A
-// operand.  Z is kept as a pair of bf16 numbers (hi + lo, about 16
-// significant bits) and multiplied in two MFMAs, so the intermediate adds
-// no bf16-sized error to the LoRA term.
+// into contiguous ranges and reduce through LDS in a fixed order, so results
+// are bitwise reproducible.  Their operands are read in the 1 KB fragment
+// layout (see bdl_device.h).  The expand runs as extra MFMA k-steps: for the
+// adapters present in the tile, 8-rank pieces ("octets") of B^T are the B
+// operand and the matching Z entries (zero for tokens of other adapters) the
+// A operand.  Z is kept as a pair of bf16 numbers (hi + lo, about 16
+// significant bits) and multiplied in two MFMAs, so the intermediate adds no
+// bf16-sized error to the LoRA term.
 #include "bdl_device.h"
 
 namespace bdl {
 
+constexpr int kStages = 3;                    // k-steps of loads kept in flight per wave
+
 // --------------------------------------------------------------------------
 // 1. plan
+//    vid[t]      validated id (-1: none or invalid, invalid ones raise *err)
+//    groups      (slot, start, count) per adapter in use, slots ascending
+//    perm        tokens group after group, ascending inside a group
+//    items       shrink work items {slot, first perm index, rows <= mts, r8}
+//    tile_oct    per base-GEMM row tile: the 8-rank octets of every adapter
+//                present in the tile (slots ascending), code = slot<<12 |
+//                r8<<4 | octet, padded with -1 to oct_cap entries
 // --------------------------------------------------------------------------
 
-__global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
-    extern __shared__ int cnt[];              // [max_slots]: counts, then cursors
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ int wave_excl_scan(int v, int lane) {
+    int inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int u = __shfl_up(inc, d);
+        if (lane >= d) inc += u;
+    }
+    return inc - v;
+}
+
+// activations -> fragment layout (all the prep launch's workgroups but 0)
+__device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
+    const int l = threadIdx.x & 63;
+    for (int f = blk * 16 + (threadIdx.x >> 6); f < a.total_frags; f += nblk * 16) {
+        int j = 0;
+        while (j + 1 < a.n_jobs && f >= a.jobs[j + 1].frag_base) ++j;
+        const PackJob& J = a.jobs[j];
+        const int KS = J.K >> 5;
+        const int local = f - J.frag_base;
+        const int rb = local / KS, ks = local - rb * KS;
+        const int row = rb * 16 + (l & 15);
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if (row < J.rows) v = ld16(J.src + (size_t)row * J.K + ks * 32 + (l >> 4) * 8);
+        *reinterpret_cast<u32x4*>(J.dst + (size_t)local * kFrag + l * 8) = v;
+    }
+}
+
+__global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
+    if (blockIdx.x > 0) {
+        pack_activations(a, blockIdx.x - 1, gridDim.x - 1);
+        return;
+    }
+    extern __shared__ int tabs[];             // cnt | r8 | loaded, max_slots each
+    int* cnt = tabs;                          // counts, then cursors
+    int* r8l = tabs + a.max_slots;
+    int* ldl = tabs + 2 * a.max_slots;
+    __shared__ int vid_l[kPlanLdsTokens];
     __shared__ int s_err;
     __shared__ int wsum[16][3];
     __shared__ int wpre[16][3];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const bool in_lds = a.T <= kPlanLdsTokens;
 
-    for (int s = tid; s < a.max_slots; s += 1024) cnt[s] = 0;
+    for (int s = tid; s < a.max_slots; s += 1024) {
+        cnt[s] = 0;
+        r8l[s] = a.r8[s];
+        ldl[s] = a.loaded[s];
+    }
     if (tid == 0) s_err = 0;
     __syncthreads();
     for (int t = tid; t < a.T; t += 1024) {
         const int id = a.ids[t];
-        const bool ok = id >= 0 && id < a.max_slots && a.loaded[id] != 0;
+        const bool ok = id >= 0 && id < a.max_slots && ldl[id] != 0;
         if (!ok && id != -1) s_err = 1;
-        a.vid[t] = ok ? id : -1;
+        const int v = ok ? id : -1;
+        a.vid[t] = v;
+        if (in_lds) vid_l[t] = v;
         if (ok) atomicAdd(&cnt[id], 1);
     }
     __syncthreads();
@@ -61,19 +123,11 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
         grp += c > 0;
         itm += (c + a.mts - 1) / a.mts;
     }
-    int it = tok, ig = grp, ii = itm;
-    for (int d = 1; d < 64; d <<= 1) {
-        const int t2 = __shfl_up(it, d), g2 = __shfl_up(ig, d), i2 = __shfl_up(ii, d);
-        if (lane >= d) {
-            it += t2;
-            ig += g2;
-            ii += i2;
-        }
-    }
+    const int et = wave_excl_scan(tok, lane), eg = wave_excl_scan(grp, lane), ei = wave_excl_scan(itm, lane);
     if (lane == 63) {
-        wsum[wv][0] = it;
-        wsum[wv][1] = ig;
-        wsum[wv][2] = ii;
+        wsum[wv][0] = et + tok;
+        wsum[wv][1] = eg + grp;
+        wsum[wv][2] = ei + itm;
     }
     __syncthreads();
     if (tid < 3) {
@@ -84,18 +138,18 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
         }
     }
     __syncthreads();
-    int tok_off = wpre[wv][0] + it - tok;
-    int g_off = wpre[wv][1] + ig - grp;
-    int i_off = wpre[wv][2] + ii - itm;
+    int tok_off = wpre[wv][0] + et;
+    int g_off = wpre[wv][1] + eg;
+    int i_off = wpre[wv][2] + ei;
     for (int s = s0; s < s1; ++s) {
         const int c = cnt[s];
         if (c > 0) {
             a.gslot[g_off] = s;
             a.gstart[g_off] = tok_off;
             a.gcount[g_off] = c;
-            a.gitem[g_off] = i_off;
+            for (int r = 0; r < c; r += a.mts)
+                a.items[i_off++] = make_int4(s, tok_off + r, min(a.mts, c - r), r8l[s]);
             ++g_off;
-            i_off += (c + a.mts - 1) / a.mts;
         }
         cnt[s] = tok_off;                     // cursor for the placement below
         tok_off += c;
@@ -103,21 +157,20 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
     if (tid == 1023) {
         a.meta[0] = g_off;
         a.meta[1] = i_off;
-        a.gitem[g_off] = i_off;
     }
     __syncthreads();
 
-    // stable placement, tokens in order, by one wave (64 tokens per step)
     if (wv == 0) {
+        // stable placement, tokens in order, 64 per step
         for (int base = 0; base < a.T; base += 64) {
             const int t = base + lane;
-            const int id = t < a.T ? a.ids[t] : -1;
-            bool ok = t < a.T && id >= 0 && id < a.max_slots && a.loaded[id] != 0;
+            const int v = t < a.T ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
+            bool ok = v >= 0;
             unsigned long long act = __ballot(ok);
             while (act) {
                 const int leader = __ffsll((long long)act) - 1;
-                const int s = __shfl(id, leader);
-                const bool mine = ok && id == s;
+                const int s = __shfl(v, leader);
+                const bool mine = ok && v == s;
                 const unsigned long long m = __ballot(mine);
                 const int b = cnt[s];
                 if (lane == leader) cnt[s] = b + __popcll(m);
@@ -128,51 +181,68 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
                 act &= ~m;
             }
         }
+    } else {
+        // expand octet lists of the base-GEMM row tiles, one tile per wave
+        const int mt = a.gemm_mt;
+        const int tiles = (a.T + mt - 1) / mt;
+        for (int m = wv - 1; m < tiles; m += 15) {
+            const int t = m * mt + lane;
+            int v = (lane < mt && t < a.T) ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
+            bool active = v >= 0;
+            int my_slot = -1, nd = 0;
+            while (__ballot(active)) {
+                const int sm = wave_min(active ? v : 0x7fffffff);
+                if (lane == nd) my_slot = sm;
+                if (v == sm) active = false;
+                ++nd;
+            }
+            const int r8s = my_slot >= 0 ? r8l[my_slot] : 0;
+            const int c = r8s >> 3;
+            const int pos = wave_excl_scan(c, lane);
+            int* dst = a.tile_oct + (size_t)m * a.oct_cap;
+            for (int j = 0; j < c; ++j) dst[pos + j] = (my_slot << 12) | (r8s << 4) | j;
+            const int total = __shfl(pos + c, 63);
+            for (int i = total + lane; i < a.oct_cap; i += 64) dst[i] = -1;
+        }
     }
     if (tid == 0 && s_err) atomicOr(a.err, 1);
 }
 
-hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), a.max_slots * sizeof(int), s, a);
+hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
+    int pack_blocks = (a.total_frags + 15) / 16;
+    if (pack_blocks > 1024) pack_blocks = 1024;
+    hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), 3 * a.max_slots * sizeof(int), s, a);
     return hipGetLastError();
 }
 
 // --------------------------------------------------------------------------
 // 2. shrink: Z[t, sigma * r8max + j] = scale_a * sum_k X[t, k] A_a,sigma[k, j]
+//    work item = (projection, shrink item, 16*NB-column chunk of A^T_cat)
 // --------------------------------------------------------------------------
 
-constexpr int kShrinkNB = 4;                  // 64 columns (rank entries) per item
-constexpr int kUnroll = 2;
-
-template <int MB>
+template <int MB, int NB>
 __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
-    constexpr int NB = kShrinkNB, MT = MB * 16, NT = NB * 16, LD = NT + 4;
+    constexpr int MT = MB * 16, NT = NB * 16, LD = NT + 4;
     __shared__ float red[4 * MT * LD];
-    const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lr = l & 15, lk = (l >> 4) * 8;
-    const int n_groups = a.meta[0], n_items = a.meta[1];
+    const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15;
+    const int n_items = a.meta[1];
     const int per_proj = a.items_bound * a.cchunks;
     const int total = a.n_proj * per_proj;
 
     for (int flat = blockIdx.x; flat < total; flat += gridDim.x) {
         const int p = flat / per_proj, rem = flat - p * per_proj;
         const int item = rem / a.cchunks, cc = rem - item * a.cchunks;
+        const int4 it = a.items[item];       // in bounds for every item < items_bound
         if (item >= n_items) continue;
-        int lo = 0, hi = n_groups - 1;          // last group whose first item <= item
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (a.gitem[mid] <= item) lo = mid;
-            else hi = mid - 1;
-        }
-        const int g = lo;
-        const int slot = a.gslot[g];
-        const int r8s = a.r8[slot];
+        const int slot = it.x, nrows = it.z, r8s = it.w;
         const ProjLaunch& P = a.p[p];
         const int ncols = P.n_slices * r8s;
         const int c0 = cc * NT;
         if (c0 >= ncols) continue;
-        const int row0 = (item - a.gitem[g]) * MT;
-        const int nrows = min(MT, a.gcount[g] - row0);
-        const int* prow = a.perm + a.gstart[g] + row0;
+        const float sc = a.scale[slot];
+        const int* prow = a.perm + it.y;
+        const int KS = P.K >> 5;
+        const int nblk = (ncols + 15) >> 4;
         const uint16_t* abase = a.pool + (size_t)slot * a.slot_stride + P.a_off;
 
         const uint16_t* ap[MB];
@@ -180,22 +250,20 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb) {
             const int t = prow[min(rb * 16 + lr, nrows - 1)];
-            ap[rb] = P.X + (size_t)t * P.K + lk;
+            ap[rb] = P.Xp + frag_index(t >> 4, 0, KS) + ((t & 15) + 16 * (l >> 4)) * 8;
         }
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) {
-            const int c = min(c0 + cb * 16 + lr, ncols - 1);
-            bp[cb] = abase + (size_t)c * P.K + lk;
-        }
+        for (int cb = 0; cb < NB; ++cb) bp[cb] = abase + frag_index(min((c0 >> 4) + cb, nblk - 1), 0, KS) + l * 8;
         f32x4 acc[MB][NB];
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
             for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        mma_ksteps<MB, NB, kUnroll>(acc, ap, bp, w * kUnroll, P.K / 32, kWaves * kUnroll);
+        int k0, nk;
+        wave_krange(KS, w, &k0, &nk);
+        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
         reduce_waves<MB, NB>(acc, red);
 
-        const float sc = a.scale[slot];
         for (int idx = threadIdx.x; idx < MT * NT; idx += kThreads) {
             const int r = idx / NT, c = idx - (idx / NT) * NT;
             const int cg = c0 + c;
@@ -213,16 +281,20 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
     }
 }
 
-hipError_t launch_shrink(const FwdArgs& a, int mb, hipStream_t s) {
+hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
     const int total = a.n_proj * a.items_bound * a.cchunks;
     const int grid = total < 4096 ? total : 4096;
     if (grid <= 0) return hipSuccess;
-    if (mb == 1) hipLaunchKernelGGL(shrink_kernel<1>, dim3(grid), dim3(kThreads), 0, s, a);
-    else hipLaunchKernelGGL(shrink_kernel<4>, dim3(grid), dim3(kThreads), 0, s, a);
-    return hipGetLastError();
+#define BDL_SHRINK_CASE(M, NN)                                                   \
+    if (mb == M && nb == NN) {                                                   \
+        hipLaunchKernelGGL((shrink_kernel<M, NN>), dim3(grid), dim3(kThreads), 0, s, a); \
+        return hipGetLastError();                                                \
+    }
+    BDL_SHRINK_CASE(1, 1) BDL_SHRINK_CASE(1, 2) BDL_SHRINK_CASE(1, 4)
+    BDL_SHRINK_CASE(4, 1) BDL_SHRINK_CASE(4, 2) BDL_SHRINK_CASE(4, 4)
+#undef BDL_SHRINK_CASE
+    return hipErrorInvalidValue;
 }
-
-int shrink_tile_cols() { return kShrinkNB * 16; }
 
 // --------------------------------------------------------------------------
 // 3. base GEMM with fused expand
@@ -231,13 +303,8 @@ int shrink_tile_cols() { return kShrinkNB * 16; }
 template <int MB, int NB>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
     constexpr int MT = MB * 16, NT = NB * 16, LD = NT + 4;
-    constexpr int kMaxOct = MT * (kMaxRank8 / 8);
     __shared__ float red[4 * MT * LD];
-    __shared__ int tvid[MT];
-    __shared__ unsigned bitmap[kMaxSlots / 32];
-    __shared__ int oct[kMaxOct];
-    __shared__ int s_noct;
-    const int w = threadIdx.x >> 6, l = threadIdx.x & 63, lr = l & 15, lk = (l >> 4) * 8;
+    const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15;
 
     const int bid = blockIdx.x;
     int p = 0;
@@ -248,63 +315,35 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
     const int m0 = mt * MT, n0 = nt * NT;
     const int T = a.T, N = P.N, K = P.K;
 
-    int my_vid = -1;
-    if (threadIdx.x < MT && m0 + (int)threadIdx.x < T) my_vid = a.vid[m0 + threadIdx.x];
+    // expand inputs that do not depend on the base product: fetched first
+    const int* codes = a.tile_oct + (size_t)mt * a.oct_cap;
+    int code = codes[4 * w + (l >> 4)];
+    int rvid[MB];
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) {
+        const int row = m0 + rb * 16 + lr;
+        rvid[rb] = row < T ? a.vid[row] : -1;
+    }
 
     // ---- base product X W_s^T over this wave's k-steps
+    const int KS = K >> 5;
+    const int nrb = (T + 15) >> 4, ncb = N >> 4;
     const uint16_t* ap[MB];
     const uint16_t* bp[NB];
 #pragma unroll
-    for (int rb = 0; rb < MB; ++rb) {
-        const int row = min(m0 + rb * 16 + lr, T - 1);
-        ap[rb] = P.X + (size_t)row * K + lk;
-    }
+    for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(min(mt * MB + rb, nrb - 1), 0, KS) + l * 8;
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-        const int col = min(n0 + cb * 16 + lr, N - 1);
-        bp[cb] = P.W + (size_t)col * K + lk;
-    }
+    for (int cb = 0; cb < NB; ++cb) bp[cb] = P.W + frag_index(min(nt * NB + cb, ncb - 1), 0, KS) + l * 8;
     f32x4 acc[MB][NB];
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
         for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    mma_ksteps<MB, NB, kUnroll>(acc, ap, bp, w * kUnroll, K / 32, kWaves * kUnroll);
+    int k0, nk;
+    wave_krange(KS, w, &k0, &nk);
+    if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
 
-    // ---- adapters present in this row tile, as a list of 8-rank octets
-    const int nwords = (a.max_slots + 31) >> 5;
-    for (int i = threadIdx.x; i < nwords; i += kThreads) bitmap[i] = 0u;
-    if (threadIdx.x < MT) tvid[threadIdx.x] = my_vid;
-    __syncthreads();
-    if (threadIdx.x < MT && my_vid >= 0) atomicOr(&bitmap[my_vid >> 5], 1u << (my_vid & 31));
-    __syncthreads();
-    if (w == 0) {
-        int base = 0;
-        for (int wb = 0; wb < nwords; wb += 64) {
-            const int wi = wb + l;
-            const unsigned bits = wi < nwords ? bitmap[wi] : 0u;
-            int cnt = 0;
-            for (unsigned bb = bits; bb; bb &= bb - 1u) cnt += a.r8[wi * 32 + __ffs(bb) - 1] >> 3;
-            int inc = cnt;
-            for (int d = 1; d < 64; d <<= 1) {
-                const int v = __shfl_up(inc, d);
-                if (l >= d) inc += v;
-            }
-            int o = base + inc - cnt;
-            for (unsigned bb = bits; bb; bb &= bb - 1u) {
-                const int slot = wi * 32 + __ffs(bb) - 1;
-                const int r8s = a.r8[slot];
-                for (int j = 0; j < (r8s >> 3); ++j) oct[o++] = (slot << 12) | (r8s << 4) | j;
-            }
-            base += __shfl(inc, 63);
-        }
-        if (l == 0) s_noct = base;
-    }
-    __syncthreads();
-
-    // ---- expand: acc += Zhat B over the octets (masked per token)
-    const int noct = s_noct;
-    const int esteps = (noct + 3) >> 2;
+    // ---- expand: acc += Zhat B over the tile's octets (masked per token)
     int sig[NB];
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) {
@@ -314,9 +353,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
         sig[cb] = sgm;
     }
     const u32x4 zero4 = u32x4{0u, 0u, 0u, 0u};
-    for (int e = w; e < esteps; e += kWaves) {
-        const int o = e * 4 + (l >> 4);
-        const int code = o < noct ? oct[o] : -1;
+    for (int e = w;;) {
+        if (!__any(code >= 0)) break;
         const int slot = code >> 12, r8s = (code >> 4) & 0xff, j0 = (code & 15) * 8;
         u32x4 bv[NB];
 #pragma unroll
@@ -332,9 +370,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
             if (cb == 0 || sig[cb] != sig[cb - 1]) {
 #pragma unroll
                 for (int rb = 0; rb < MB; ++rb) {
-                    const int r = rb * 16 + lr;
-                    const bool match = code >= 0 && m0 + r < T && tvid[r] == slot;
-                    const uint16_t* zp = P.Z + (size_t)(m0 + r) * P.zs + sig[cb] * a.r8max + j0;
+                    const bool match = code >= 0 && rvid[rb] == slot;
+                    const uint16_t* zp = P.Z + (size_t)(m0 + rb * 16 + lr) * P.zs + sig[cb] * a.r8max + j0;
                     zh[rb] = match ? ld16(zp) : zero4;
                     zl[rb] = match ? ld16(zp + P.zplane) : zero4;
                 }
@@ -345,6 +382,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
                 acc[rb][cb] = mfma(zl[rb], bv[cb], acc[rb][cb]);
             }
         }
+        e += kWaves;
+        if (4 * e + 4 > a.oct_cap) break;
+        code = codes[4 * e + (l >> 4)];
     }
 
     // ---- reduce the 8 waves and store bf16 (two columns per thread)
@@ -358,9 +398,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
         }
     }
 }
-
-int gemm_tile_rows(int mb) { return mb * 16; }
-int gemm_tile_cols(int nb) { return nb * 16; }
 
 hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s) {
     const dim3 grid(a.total_tiles), block(kThreads);
@@ -378,12 +415,37 @@ hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s) {
 }
 
 // --------------------------------------------------------------------------
-// adapter pack: paper layout -> kernel layout (off the per-batch path)
-//   stage = [A_0 .. A_{S-1} | B_0 .. B_{S-1}],  A_s [K x r], B_s [r x n_s]
-//   dst_a = A^T_cat [S * r8 x K]   (row s*r8 + j = column j of A_s, zero if j >= r)
-//   dst_b = B^T_cat [N x r8]       (row n = column n of its slice's B, zero pad)
+// packing (off the per-batch path)
 // --------------------------------------------------------------------------
 
+// rows-major [rows x K] -> fragment layout with rows padded to 16 (zeros)
+__global__ void pack_rows_kernel(const uint16_t* src, uint16_t* dst, int rows, int K, long long frags) {
+    const int l = threadIdx.x & 63;
+    const int KS = K >> 5;
+    for (long long f = (blockIdx.x * (long long)blockDim.x + threadIdx.x) >> 6; f < frags;
+         f += ((long long)gridDim.x * blockDim.x) >> 6) {
+        const int rb = (int)(f / KS), ks = (int)(f - (long long)rb * KS);
+        const int row = rb * 16 + (l & 15);
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if (row < rows) v = ld16(src + (size_t)row * K + ks * 32 + (l >> 4) * 8);
+        *reinterpret_cast<u32x4*>(dst + (size_t)f * kFrag + l * 8) = v;
+    }
+}
+
+hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s) {
+    const long long frags = (long long)((rows + 15) / 16) * (K / 32);
+    if (frags == 0) return hipSuccess;
+    long long blocks = (frags + 3) / 4;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, rows, K, frags);
+    return hipGetLastError();
+}
+
+// adapter: paper layout -> pool layout
+//   stage = [A_0 .. A_{S-1} | B_0 .. B_{S-1}],  A_s [K x r], B_s [r x n_s]
+//   dst_a = A^T_cat in fragment layout: row s*r8 + j of A^T_cat is column j
+//           of A_s (zero for j >= r), rows padded to a multiple of 16
+//   dst_b = B^T_cat [N x r8] row-major: row n is column n of its slice's B
 struct PackArgs {
     uint16_t* dst_a;
     uint16_t* dst_b;
@@ -393,18 +455,24 @@ struct PackArgs {
     int slice_col[kMaxSlices + 1];
 };
 
-__global__ void pack_kernel(PackArgs a) {
-    const long long na = (long long)a.S * a.r8 * a.K;
+__global__ void pack_adapter_kernel(PackArgs a) {
+    const int KS = a.K >> 5;
+    const int arows = a.S * a.r8;
+    const long long na = (long long)((arows + 15) / 16) * KS * kFrag;
     const long long nb = (long long)a.N * a.r8;
     const long long a_elems = (long long)a.S * a.K * a.rank;
     for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < na + nb;
          i += (long long)gridDim.x * blockDim.x) {
         if (i < na) {
-            const long long row = i / a.K;
-            const int k = (int)(i - row * a.K);
-            const int s = (int)(row / a.r8), j = (int)(row - (long long)s * a.r8);
+            const long long f = i / kFrag;
+            const int e = (int)(i - f * kFrag), l = e >> 3, q = e & 7;
+            const int rb = (int)(f / KS), ks = (int)(f - (long long)rb * KS);
+            const int row = rb * 16 + (l & 15), k = ks * 32 + (l >> 4) * 8 + q;
             uint16_t v = 0;
-            if (j < a.rank) v = a.stage[(long long)s * a.K * a.rank + (long long)k * a.rank + j];
+            if (row < arows) {
+                const int s = row / a.r8, j = row - s * a.r8;
+                if (j < a.rank) v = a.stage[(long long)s * a.K * a.rank + (long long)k * a.rank + j];
+            }
             a.dst_a[i] = v;
         } else {
             const long long q = i - na;
@@ -420,8 +488,8 @@ __global__ void pack_kernel(PackArgs a) {
     }
 }
 
-hipError_t launch_pack(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K, int n_slices,
-                       const int* slice_out, int rank, int r8, hipStream_t s) {
+hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K, int n_slices,
+                               const int* slice_out, int rank, int r8, hipStream_t s) {
     PackArgs a;
     a.dst_a = dst_a;
     a.dst_b = dst_b;
@@ -437,11 +505,11 @@ hipError_t launch_pack(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, 
         if (i < n_slices) col += slice_out[i];
     }
     a.N = col;
-    const long long total = (long long)n_slices * r8 * K + (long long)col * r8;
+    const long long total = (long long)((n_slices * r8 + 15) / 16) * (K / 32) * kFrag + (long long)col * r8;
     if (total == 0) return hipSuccess;
     long long blocks = (total + 255) / 256;
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(pack_adapter_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

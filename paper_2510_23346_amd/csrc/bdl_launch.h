@@ -9,19 +9,21 @@ namespace bdl {
 constexpr int kMaxProjs = 8;
 constexpr int kMaxSlices = 4;
 constexpr int kMaxSlots = 8192;
-constexpr int kMaxRank8 = 128;      // largest supported rank, rounded up to 8
+constexpr int kMaxRank8 = 128;       // largest supported rank, rounded up to 8
+constexpr int kPlanLdsTokens = 4096; // plan keeps validated ids in LDS up to this batch size
 
 // One projection of a forward launch.
 struct ProjLaunch {
-    const uint16_t* X;        // [T x K]   bf16
-    const uint16_t* W;        // [N x K]   bf16 (nn.Linear layout)
-    uint16_t* out;            // [T x N]   bf16
+    const uint16_t* X;        // [T x K] bf16 activations (row-major)
+    const uint16_t* Xp;       // packed activations, fragment layout, rows padded to 16
+    const uint16_t* W;        // packed base weight, fragment layout ([N x K] nn.Linear rows)
+    uint16_t* out;            // [T x N] bf16
     uint16_t* Z;              // [2 x max_tokens x zs] workspace: scale * X A per slice as a
                               // bf16 pair (hi plane, then lo plane at Z + zplane)
     long long zplane;         // elements between the hi and the lo plane
     int K, N, n_slices, zs;
     int slice_col[kMaxSlices + 1];   // first column of each slice; [n_slices] = N
-    long long a_off, b_off;   // element offsets of A^T_cat and B^T_cat in a slot
+    long long a_off, b_off;   // element offsets of packed A^T_cat and of B^T_cat in a slot
     int tiles_n;              // base GEMM: column tiles of this projection
     int tile_base;            // base GEMM: first flattened tile of this projection
 };
@@ -33,49 +35,58 @@ struct FwdArgs {
     int T;
     const uint16_t* pool;     // adapter slabs
     long long slot_stride;    // elements per slot
-    int max_slots;
     int r8max;                // per-slice Z stride (elements)
-    const int* r8;            // [max_slots] rank rounded up to 8 (0: none)
     const float* scale;       // [max_slots]
     const int* vid;           // [T] validated ids
     const int* perm;          // [T] tokens grouped by adapter
-    const int* gslot;         // [groups]
-    const int* gstart;        // [groups] start in perm
-    const int* gcount;        // [groups]
-    const int* gitem;         // [groups + 1] first shrink item of each group
-    const int* meta;          // [0] groups, [1] shrink items
-    int items_bound;          // shrink: upper bound on items per projection
+    const int4* items;        // shrink items {slot, first perm index, rows, r8}
+    const int* meta;          // [1] number of shrink items
+    int items_bound;          // shrink: upper bound on items
     int cchunks;              // shrink: column chunks per item (upper bound)
-    int mts;                  // shrink: rows per item
+    const int* tile_oct;      // expand octet codes per row tile (-1 padded)
+    int oct_cap;              // entries per row tile in tile_oct
     int tiles_m;              // base GEMM: row tiles
     int total_tiles;          // base GEMM: flattened tiles over all projections
 };
 
-// Plan launch (one workgroup).
-struct PlanArgs {
+// Activation packing job of the prep launch.
+struct PackJob {
+    const uint16_t* src;      // [rows x K] row-major
+    uint16_t* dst;            // fragment layout, rows padded to a multiple of 16
+    int rows, K;
+    int frag_base;            // first fragment of this job in the launch's numbering
+};
+
+// Prep launch: workgroup 0 plans the batch, the others pack activations.
+struct PrepArgs {
     const int* ids;
     int T;
     const int* loaded;
+    const int* r8;            // [max_slots]
     int max_slots;
-    int mts;
+    int mts;                  // shrink rows per item
+    int gemm_mt;              // base GEMM row tile (<= 64)
+    int oct_cap;
     int* vid;
     int* perm;
     int* gslot;
     int* gstart;
     int* gcount;
-    int* gitem;
-    int* meta;
+    int4* items;
+    int* tile_oct;
+    int* meta;                // [0] groups, [1] shrink items
     int* err;
+    PackJob jobs[kMaxProjs];
+    int n_jobs;
+    int total_frags;
 };
 
 // Host-side launchers (bdl_kernels.hip).
-hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
-hipError_t launch_shrink(const FwdArgs& a, int mb, hipStream_t s);
+hipError_t launch_prep(const PrepArgs& a, hipStream_t s);
+hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);
-hipError_t launch_pack(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K, int n_slices,
-                       const int* slice_out, int rank, int r8, hipStream_t s);
-int gemm_tile_rows(int mb);
-int gemm_tile_cols(int nb);
-int shrink_tile_cols();
+hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K,
+                               int n_slices, const int* slice_out, int rank, int r8, hipStream_t s);
+hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s);
 
 }  // namespace bdl

@@ -188,6 +188,35 @@ def test_invalid_ids_are_base_only_and_flagged(torch_cuda):
     pool.close()
 
 
+def _fragment_layout(W):
+    """Reference of the packed weight layout: 16-row blocks x 32-wide k-steps,
+    element [(rb*KS + ks)*512 + lane*8 + i] = W[16 rb + lane%16][32 ks + 8 (lane//16) + i]."""
+    N, K = W.shape
+    KS = K // 32
+    out = np.empty(N * K, W.dtype)
+    for rb in range(N // 16):
+        for ks in range(KS):
+            for lane in range(64):
+                base = (rb * KS + ks) * 512 + lane * 8
+                out[base:base + 8] = W[16 * rb + lane % 16, 32 * ks + 8 * (lane // 16): 32 * ks + 8 * (lane // 16) + 8]
+    return out
+
+
+@pytest.mark.parametrize("N,K", [(16, 32), (48, 96), (80, 256)])
+def test_pack_weight_layout_bit_exact(torch_cuda, N, K):
+    torch = torch_cuda
+    import paper_2510_23346_amd as bd
+    rng = np.random.default_rng(N + K)
+    W = rng.integers(0, 1 << 16, size=(N, K), dtype=np.uint16)
+    Wd = torch.from_numpy(W.view(np.int16)).cuda()
+    P = bd.pack_weight(Wd)
+    torch.cuda.synchronize()
+    got = P.cpu().numpy().view(np.uint16).reshape(-1)
+    assert np.array_equal(got, _fragment_layout(W))
+    with pytest.raises(bd.BDLoRAError):
+        bd.pack_weight(Wd[:, :K - 8].contiguous())                               # K not a multiple of 32
+
+
 def test_empty_batch_and_errors(torch_cuda):
     torch = torch_cuda
     import paper_2510_23346_amd as bd
@@ -250,7 +279,7 @@ def test_all_shards_reassemble_the_unsharded_layer(torch_cuda):
         pool = bd.Pool([("column", d, (n_s,))], 1, r_tot // N, S)
         pool.load_adapter(0, r_tot // N, gamma, [[np.ascontiguousarray(a1b)]], [[np.ascontiguousarray(b1b)]])
         Xd = torch.from_numpy(Xb.view(np.int16)).cuda().view(torch.bfloat16)
-        Wd = torch.from_numpy(np.ascontiguousarray(W1b[:, i * n_s:(i + 1) * n_s].T).view(np.int16)).cuda().view(torch.bfloat16)
+        Wd = bd.pack_weight(torch.from_numpy(np.ascontiguousarray(W1b[:, i * n_s:(i + 1) * n_s].T).view(np.int16)).cuda().view(torch.bfloat16))
         out = torch.empty((S, n_s), dtype=torch.bfloat16, device="cuda")
         pool.forward_shard(0, Xd, Wd, ids, out)
         torch.cuda.synchronize()
@@ -264,7 +293,7 @@ def test_all_shards_reassemble_the_unsharded_layer(torch_cuda):
         pool.load_adapter(0, r_tot // N, gamma, [[np.ascontiguousarray(a2b)]], [[np.ascontiguousarray(b2b)]])
         Xs = np.ascontiguousarray(bf16_round(y_col[:, i * k_s:(i + 1) * k_s])[0])
         Xd = torch.from_numpy(Xs.view(np.int16)).cuda().view(torch.bfloat16)
-        Wd = torch.from_numpy(np.ascontiguousarray(W2b[i * k_s:(i + 1) * k_s, :].T).view(np.int16)).cuda().view(torch.bfloat16)
+        Wd = bd.pack_weight(torch.from_numpy(np.ascontiguousarray(W2b[i * k_s:(i + 1) * k_s, :].T).view(np.int16)).cuda().view(torch.bfloat16))
         out = torch.empty((S, d), dtype=torch.bfloat16, device="cuda")
         pool.forward_shard(0, Xd, Wd, ids, out)
         torch.cuda.synchronize()

@@ -32,8 +32,16 @@ def device_to_float(t) -> np.ndarray:
     return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
+def pack_weight(w):
+    """nn.Linear-layout device weight -> the library's packed layout."""
+    from paper_2510_23346_amd import pack_weight as _pack
+    out = _pack(w)
+    return out
+
+
 class DeviceLayer:
-    """Device copies of one drawn layer: ids, per-projection X, W and out."""
+    """Device copies of one drawn layer: ids, per-projection X, packed W and
+    out."""
 
     def __init__(self, layer: LayerInputs, device="cuda", T: Optional[int] = None):
         torch = _torch()
@@ -43,7 +51,7 @@ class DeviceLayer:
         self.X, self.W, self.out = [], [], []
         for pi in layer.projs:
             self.X.append(bits_to_device(pi.X_bits[:T], device))
-            self.W.append(bits_to_device(np.ascontiguousarray(pi.W_bits.T), device))
+            self.W.append(pack_weight(bits_to_device(np.ascontiguousarray(pi.W_bits.T), device)))
             self.out.append(torch.empty((T, pi.spec.d_out), dtype=torch.bfloat16, device=device))
 
     def outputs(self) -> List[np.ndarray]:
