@@ -67,6 +67,34 @@ def algorithmic_flops(spec, ids, ranks):
     return g, s
 
 
+KERNEL_SOURCES = ("bdl_kernels.hip", "bdl_device.h", "bdl_launch.h", "bdl_api.cpp")
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2510_23346_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload_name):
+    """HBM bytes per base-GEMM launch from the committed rocprofv3 counter
+    summary of this workload, if it was taken on the current kernel sources
+    (else None: the counters are stale or absent)."""
+    import re
+    path = os.path.join(ROOT, "profiles", f"gemm_kernel_{workload_name}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    mh = re.search(r"first 16 hex\): `([0-9a-f]{16})`", text)
+    mt = re.search(r"gemm_traffic_bytes_per_launch: (\d+)", text)
+    if not mh or not mt or mh.group(1) != kernel_source_hash():
+        return None
+    return int(mt.group(1))
+
+
 def cpu_baseline(spec, layer, seconds):
     """Time the oracle (fp64 numpy) on this host: whole steps until
     ``seconds`` have passed."""
@@ -105,6 +133,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of graphs")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="before the benchmark, run 3 plain device copies of MIB MiB (untimed), "
+                         "a known-size reference for hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs one GPU's shard only; --gpus {args.gpus} is not supported "
@@ -120,6 +151,14 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     bd.lib()
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     spec = wl.workload(args.workload)
     ids_np = wl.draw_ids(spec)
     resident = list(range(spec.n_slots)) if spec.n_slots <= 128 else sorted(
@@ -209,6 +248,7 @@ def main():
         achieved = g_flops / gemm_s / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFS,
                 "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4), "traffic": None}
+    roof["traffic"] = committed_traffic(spec.name)
     roof["kernel"] = "bdl::gemm_kernel (base product + fused expand)"
     roof["kernel_ms"] = round(k_ms[2], 5)
 
