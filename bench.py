@@ -2,8 +2,8 @@
 """Benchmark of the BD-LoRA layer-shard forward on one MI355X.
 
 A step is one forward of a whole decoder-layer shard (all its projections:
-plan, shrink, base product with fused expand) over one batch of synthetic
-tokens, through the library's C ABI.  Default workload: Llama-3.1-8B layer
+plan, shrink, base product, expand) over one batch of synthetic tokens,
+through the library's C ABI.  Default workload: Llama-3.1-8B layer
 shard at 1/8 tensor parallelism, 64 decode tokens, 32 resident adapters of
 rank 16, adapter ids Zipf(1.0).
 
@@ -34,23 +34,25 @@ MALL_BYTES = 256 << 20
 
 
 def algorithmic_bytes(spec, ids, ranks):
-    """Per-step bytes the method must move, split by kernel.
+    """Per-step bytes the method must move (bf16 = 2 bytes), split by launch.
 
-    gemm: every base weight once, X and out once per projection, the B
-    factor of every adapter some token uses.  shrink: the A factor of every
-    adapter some token uses.  bf16 = 2 bytes.
+    Returns (main, expand, active): ``main`` is what the shrink and base
+    product must read, i.e. every base weight once, X once per projection and
+    the A factor of every adapter some token uses; ``expand`` is the B factor
+    of every such adapter plus the output written once.
     """
     active = sorted({int(a) for a in ids if a >= 0})
     T = len(ids)
-    g = s = 0
+    m = e = 0
     for p in spec.projs:
         n = sum(p.slices)
-        g += p.d_in * n + T * p.d_in + T * n
+        m += p.d_in * n + T * p.d_in
+        e += T * n
         for a in active:
             r = ranks[a]
-            g += r * n
-            s += len(p.slices) * p.d_in * r
-    return 2 * g, 2 * s, len(active)
+            m += len(p.slices) * p.d_in * r
+            e += r * n
+    return 2 * m, 2 * e, len(active)
 
 
 def algorithmic_flops(spec, ids, ranks):
@@ -67,7 +69,8 @@ def algorithmic_flops(spec, ids, ranks):
     return g, s
 
 
-KERNEL_SOURCES = ("bdl_kernels.hip", "bdl_device.h", "bdl_launch.h", "bdl_api.cpp")
+KERNEL_SOURCES = ("bdl_prep.hip", "bdl_decode.hip", "bdl_kernels.hip", "bdl_device.h", "bdl_launch.h",
+                  "bdl_api.cpp")
 
 
 def kernel_source_hash():
@@ -79,17 +82,17 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def committed_traffic(workload_name):
-    """HBM bytes per base-GEMM launch from the committed rocprofv3 counter
-    summary of this workload, if it was taken on the current kernel sources
-    (else None: the counters are stale or absent)."""
+def committed_traffic(kernel, workload_name):
+    """HBM bytes per launch of ``kernel`` from the committed rocprofv3
+    counter summary of this workload, if it was taken on the current kernel
+    sources (else None: the counters are stale or absent)."""
     import re
-    path = os.path.join(ROOT, "profiles", f"gemm_kernel_{workload_name}.md")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_name}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     mh = re.search(r"first 16 hex\): `([0-9a-f]{16})`", text)
-    mt = re.search(r"gemm_traffic_bytes_per_launch: (\d+)", text)
+    mt = re.search(r"traffic_bytes_per_launch: (\d+)", text)
     if not mh or not mt or mh.group(1) != kernel_source_hash():
         return None
     return int(mt.group(1))
@@ -164,10 +167,10 @@ def main():
     resident = list(range(spec.n_slots)) if spec.n_slots <= 128 else sorted(
         int(s) for s in np.unique(ids_np) if s >= 0)
     layer = wl.draw_layer(spec, slots=resident)
-    g_bytes, s_bytes, n_active = algorithmic_bytes(spec, ids_np, spec.ranks)
+    m_bytes, e_bytes, n_active = algorithmic_bytes(spec, ids_np, spec.ranks)
     g_flops, s_flops = algorithmic_flops(spec, ids_np, spec.ranks)
-    step_bytes = g_bytes + s_bytes
-    decode = spec.T <= 256
+    step_bytes = m_bytes + e_bytes
+    decode = spec.T <= bd.DECODE_MAX_T
 
     # rotated copies: each is a pool with the same adapters plus its own tensors
     pool0 = make_pool(spec)
@@ -239,18 +242,25 @@ def main():
             sums[k] += ms[k] * n
         cnt += n
     k_ms = [s / max(1, cnt) for s in sums]
-    gemm_s = k_ms[2] * 1e-3
     if decode:
-        achieved = g_bytes / gemm_s / 1e9
+        # decode launches: prep (plan + packing), main (K-split shrink and
+        # base partials), epilogue (partial sums + expand); main moves the
+        # weights and dominates
+        names = ("prep", "main", "epilogue")
+        dom, dom_name = 1, "bdl::dec_main_kernel"
+        achieved = m_bytes / (k_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None}
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
     else:
-        achieved = g_flops / gemm_s / 1e12
+        names = ("prep", "shrink", "gemm")
+        dom, dom_name = 2, "bdl::gemm_kernel"
+        achieved = g_flops / (k_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFS,
-                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4), "traffic": None}
-    roof["traffic"] = committed_traffic(spec.name)
-    roof["kernel"] = "bdl::gemm_kernel (base product + fused expand)"
-    roof["kernel_ms"] = round(k_ms[2], 5)
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4)}
+    roof["traffic"] = committed_traffic(dom_name.split("::")[1], spec.name)
+    roof["kernel"] = dom_name
+    roof["kernel_ms"] = round(k_ms[dom], 5)
+    roof["algorithmic"] = m_bytes if decode else g_flops
 
     out = {
         "metric": "tokens/s per layer-shard",
@@ -282,7 +292,7 @@ def main():
             "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         },
         "step_flops": g_flops + s_flops,
-        "kernel_ms": {"plan": round(k_ms[0], 5), "shrink": round(k_ms[1], 5), "gemm": round(k_ms[2], 5)},
+        "kernel_ms": {nm: round(v, 5) for nm, v in zip(names, k_ms)},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

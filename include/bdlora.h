@@ -65,6 +65,11 @@ extern "C" {
 #define BDLORA_MAX_PROJS  8
 #define BDLORA_MAX_SLOTS  8192
 #define BDLORA_MAX_RANK   128
+/* Batches of at most this many tokens take the decode launch sequence (plan
+ * and packing, K-split shrink and base partials, epilogue); larger ones take
+ * the prefill sequence (plan and packing, shrink, base product with the
+ * expand fused in). */
+#define BDLORA_DECODE_MAX_T 64
 
 typedef struct bdlora_pool* bdlora_pool_t;
 
@@ -189,10 +194,13 @@ int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max
 int bdlora_pool_bytes(bdlora_pool_t pool, int64_t* bytes);
 
 /* Timing hooks.  bdlora_profile_begin(pool, n) makes the next n forward
- * calls record HIP events around each of their three launches (plan, shrink,
- * base-plus-expand) on the caller's stream.  bdlora_profile_end waits for
- * them and writes the mean duration in milliseconds of each launch kind to
- * ms[0..2] and the number of recorded calls to *n. */
+ * calls record HIP events around each of their three launches on the
+ * caller's stream: for a decode batch (T <= BDLORA_DECODE_MAX_T) plan and
+ * packing, K-split shrink and base partials, epilogue; for a larger batch
+ * plan and packing, shrink, base product with fused expand.
+ * bdlora_profile_end waits for them and writes the mean duration in
+ * milliseconds of each launch to ms[0..2] and the number of recorded calls
+ * to *n.  The calls averaged should all take the same sequence. */
 int bdlora_profile_begin(bdlora_pool_t pool, int32_t n);
 int bdlora_profile_end(bdlora_pool_t pool, float* ms, int32_t* n);
 

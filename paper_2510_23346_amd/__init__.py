@@ -17,11 +17,12 @@ import numpy as np
 
 __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
-    "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS",
+    "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T",
 ]
 
 COLUMN, ROW = 0, 1
 MAX_SLICES = 4
+DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libbdlora.so")
 _LIB = None

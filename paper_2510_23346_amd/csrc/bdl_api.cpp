@@ -108,7 +108,10 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
     ws += ((long long)max_slots + max_tokens / 16 + 2) * 16;      // shrink items
     ws += std::max(((long long)max_tokens / 16 + 1) * (2LL * L->r8max + 64),
                    ((long long)max_tokens / 64 + 1) * (8LL * L->r8max + 64)) * 4;   // tile octets
-    for (int p = 0; p < n_projs; ++p) ws += (L->z_elems[p] + L->xp_elems[p]) * 2;
+    for (int p = 0; p < n_projs; ++p) {
+        ws += (L->z_elems[p] + L->xp_elems[p]) * 2;
+        ws += (long long)bdl::kMaxKSplit * bdl::kDecodeMaxT * (L->proj[p].N + L->proj[p].zs) * 4;
+    }
     ws += max_slots * 12LL;                                       // slot tables
     L->ws_bytes = ws;
     return BDLORA_OK;
@@ -137,6 +140,7 @@ struct bdlora_pool {
     std::vector<int> h_rank, h_r8, h_loaded;
     std::vector<float> h_scale;
     int* d_vid = nullptr;
+    int* d_tr8 = nullptr;
     int* d_perm = nullptr;
     int* d_gslot = nullptr;
     int* d_gstart = nullptr;
@@ -147,6 +151,8 @@ struct bdlora_pool {
     int* d_meta = nullptr;
     int* d_err = nullptr;
     uint16_t* d_Z[bdl::kMaxProjs] = {};
+    float* d_Yp[bdl::kMaxProjs] = {};
+    float* d_Zp[bdl::kMaxProjs] = {};
     uint16_t* d_Xp[bdl::kMaxProjs] = {};
     uint16_t* d_stage = nullptr;
     long long stage_elems = 0;
@@ -170,6 +176,7 @@ void free_pool(bdlora_pool* P) {
     f(P->d_scale);
     f(P->d_loaded);
     f(P->d_vid);
+    f(P->d_tr8);
     f(P->d_perm);
     f(P->d_gslot);
     f(P->d_gstart);
@@ -179,6 +186,8 @@ void free_pool(bdlora_pool* P) {
     f(P->d_meta);
     f(P->d_err);
     for (auto z : P->d_Z) f(z);
+    for (auto y : P->d_Yp) f(y);
+    for (auto z : P->d_Zp) f(z);
     for (auto x : P->d_Xp) f(x);
     f(P->d_stage);
     for (auto e : P->prof_ev) (void)hipEventDestroy(e);
@@ -304,6 +313,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_scale, S, &tot));
     BDL_TRY(dev_alloc(&P->d_loaded, S, &tot));
     BDL_TRY(dev_alloc(&P->d_vid, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_tr8, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
@@ -319,6 +329,8 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     for (int p = 0; p < n_projs; ++p) {
         BDL_TRY(dev_alloc(&P->d_Z[p], L.z_elems[p], &tot));
         BDL_TRY(dev_alloc(&P->d_Xp[p], L.xp_elems[p], &tot));
+        BDL_TRY(dev_alloc(&P->d_Yp[p], (long long)bdl::kMaxKSplit * bdl::kDecodeMaxT * L.proj[p].N, &tot));
+        BDL_TRY(dev_alloc(&P->d_Zp[p], (long long)bdl::kMaxKSplit * bdl::kDecodeMaxT * L.proj[p].zs, &tot));
         const ProjInfo& pi = L.proj[p];
         stage = std::max(stage, (long long)pi.S * pi.K * std::max(1, max_rank) + (long long)std::max(1, max_rank) * pi.N);
     }
@@ -485,6 +497,7 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->gemm_mt = 16 * k.gmb;
     a->oct_cap = oct_cap(P->L, 16 * k.gmb);
     a->vid = P->d_vid;
+    a->tr8 = P->d_tr8;
     a->perm = P->d_perm;
     a->gslot = P->d_gslot;
     a->gstart = P->d_gstart;
@@ -495,6 +508,114 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->err = P->d_err;
     a->n_jobs = 0;
     a->total_frags = 0;
+}
+
+// Decode batches: prep (plan + activation packing), one launch of K-split
+// shrink and base items writing fp32 partials, one epilogue launch.
+static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
+                          const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s) {
+    const Layout& L = P->L;
+    std::vector<int> order(n);
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+        return (long long)L.proj[projs[x]].K * L.proj[projs[x]].N > (long long)L.proj[projs[y]].K * L.proj[projs[y]].N;
+    });
+    int n_loaded = 0;
+    for (int v : P->h_loaded) n_loaded += v != 0;
+    // K chunk so that about 512 base items cover the batch (two per CU: the
+    // kernel holds two workgroups per CU), a multiple of the 8 waves
+    long long work = 0;
+    for (int i = 0; i < n; ++i) work += (long long)((L.proj[projs[i]].N + 63) / 64) * (L.proj[projs[i]].K / 32);
+    int kc = (int)((work + 511) / 512);
+    kc = std::max(8, (kc + 7) / 8 * 8);
+
+    bdl::DecArgs da;
+    std::memset(&da, 0, sizeof(da));
+    const int items_bound = std::min(T, std::max(n_loaded, 1)) + (T + 15) / 16;
+    int shrink = 0, gemm = 0, epi = 0;
+    for (int q = 0; q < n; ++q) {
+        const int i = order[q];
+        const ProjInfo& pi = L.proj[projs[i]];
+        bdl::DecProj& d = da.p[q];
+        d.Xp = P->d_Xp[projs[i]];
+        d.W = (const uint16_t*)W[i];
+        d.out = (uint16_t*)out[i];
+        d.Yp = P->d_Yp[projs[i]];
+        d.Zp = P->d_Zp[projs[i]];
+        d.K = pi.K;
+        d.N = pi.N;
+        d.n_slices = pi.S;
+        d.zs = pi.zs;
+        for (int t = 0; t <= bdl::kMaxSlices; ++t) d.slice_col[t] = pi.slice_col[t];
+        d.a_off = pi.a_off;
+        d.b_off = pi.b_off;
+        const int KS = pi.K / 32;
+        d.ks = std::min(bdl::kMaxKSplit, std::max(1, (KS + kc - 1) / kc));
+        d.kchunk = (KS + d.ks - 1) / d.ks;
+        d.cchunks = (pi.S * L.r8max + 63) / 64;
+        d.tiles_n = (pi.N + 63) / 64;
+        d.shrink_base = shrink;
+        shrink += items_bound * d.cchunks * d.ks;
+        d.gemm_base = gemm;
+        gemm += d.tiles_n * d.ks;
+        d.epi_base = epi;
+        epi += T * (pi.N / 8);
+    }
+    da.n_proj = n;
+    da.T = T;
+    da.pool = P->d_slabs;
+    da.slot_stride = L.slot_stride;
+    da.r8max = L.r8max;
+    da.scale = P->d_scale;
+    da.r8 = P->d_r8;
+    da.vid = P->d_vid;
+    da.tr8 = P->d_tr8;
+    da.perm = P->d_perm;
+    da.items = P->d_items;
+    da.meta = P->d_meta;
+    da.items_bound = items_bound;
+    da.shrink_slots = shrink;
+    da.gemm_items = gemm;
+    da.epi_units = epi;
+    if (items_bound > P->items_cap) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
+
+    Shapes k;
+    k.smb = 1;
+    k.snb = 4;
+    k.gmb = (T + 15) / 16;
+    k.gnb = 4;
+    bdl::PrepArgs pa;
+    fill_plan_args(P, ids, T, &pa, k);
+    pa.tile_oct = nullptr;                        // the epilogue needs no octet lists
+    int frags = 0;
+    for (int q = 0; q < n; ++q) {
+        bdl::PackJob& J = pa.jobs[q];
+        J.src = (const uint16_t*)X[order[q]];
+        J.dst = P->d_Xp[projs[order[q]]];
+        J.rows = T;
+        J.K = da.p[q].K;
+        J.frag_base = frags;
+        frags += ((T + 15) / 16) * (J.K / 32);
+    }
+    pa.n_jobs = n;
+    pa.total_frags = frags;
+
+    hipEvent_t* ev = nullptr;
+    if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * 6 <= P->prof_ev.size()) {
+        ev = &P->prof_ev[(size_t)P->prof_used * 6];
+        ++P->prof_used;
+        --P->prof_left;
+    }
+    if (ev) BDL_HIP(hipEventRecord(ev[0], s));
+    BDL_HIP(bdl::launch_prep(pa, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[1], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[2], s));
+    BDL_HIP(bdl::launch_dec_main(da, k.gmb, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[3], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[4], s));
+    BDL_HIP(bdl::launch_dec_epi(da, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[5], s));
+    return BDLORA_OK;
 }
 
 int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
@@ -518,6 +639,8 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
     DeviceGuard guard(P->device);
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
+
+    if (T <= bdl::kDecodeMaxT) return forward_decode(P, n, projs, X, W, out, ids, T, s);
 
     long long col_blocks = 0;
     for (int i = 0; i < n; ++i) col_blocks += L.proj[projs[i]].N / 16;

@@ -36,186 +36,6 @@ namespace bdl {
 constexpr int kStages = 3;                    // k-steps of loads kept in flight per wave
 
 // --------------------------------------------------------------------------
-// 1. plan
-//    vid[t]      validated id (-1: none or invalid, invalid ones raise *err)
-//    groups      (slot, start, count) per adapter in use, slots ascending
-//    perm        tokens group after group, ascending inside a group
-//    items       shrink work items {slot, first perm index, rows <= mts, r8}
-//    tile_oct    per base-GEMM row tile: the 8-rank octets of every adapter
-//                present in the tile (slots ascending), code = slot<<12 |
-//                r8<<4 | octet, padded with -1 to oct_cap entries
-// --------------------------------------------------------------------------
-
-__device__ __forceinline__ int wave_min(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
-    return v;
-}
-
-__device__ __forceinline__ int wave_excl_scan(int v, int lane) {
-    int inc = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int u = __shfl_up(inc, d);
-        if (lane >= d) inc += u;
-    }
-    return inc - v;
-}
-
-// activations -> fragment layout (all the prep launch's workgroups but 0)
-__device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
-    const int l = threadIdx.x & 63;
-    for (int f = blk * 16 + (threadIdx.x >> 6); f < a.total_frags; f += nblk * 16) {
-        int j = 0;
-        while (j + 1 < a.n_jobs && f >= a.jobs[j + 1].frag_base) ++j;
-        const PackJob& J = a.jobs[j];
-        const int KS = J.K >> 5;
-        const int local = f - J.frag_base;
-        const int rb = local / KS, ks = local - rb * KS;
-        const int row = rb * 16 + (l & 15);
-        u32x4 v = u32x4{0u, 0u, 0u, 0u};
-        if (row < J.rows) v = ld16(J.src + (size_t)row * J.K + ks * 32 + (l >> 4) * 8);
-        *reinterpret_cast<u32x4*>(J.dst + (size_t)local * kFrag + l * 8) = v;
-    }
-}
-
-__global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
-    if (blockIdx.x > 0) {
-        pack_activations(a, blockIdx.x - 1, gridDim.x - 1);
-        return;
-    }
-    extern __shared__ int tabs[];             // cnt | r8 | loaded, max_slots each
-    int* cnt = tabs;                          // counts, then cursors
-    int* r8l = tabs + a.max_slots;
-    int* ldl = tabs + 2 * a.max_slots;
-    __shared__ int vid_l[kPlanLdsTokens];
-    __shared__ int s_err;
-    __shared__ int wsum[16][3];
-    __shared__ int wpre[16][3];
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const bool in_lds = a.T <= kPlanLdsTokens;
-
-    for (int s = tid; s < a.max_slots; s += 1024) {
-        cnt[s] = 0;
-        r8l[s] = a.r8[s];
-        ldl[s] = a.loaded[s];
-    }
-    if (tid == 0) s_err = 0;
-    __syncthreads();
-    for (int t = tid; t < a.T; t += 1024) {
-        const int id = a.ids[t];
-        const bool ok = id >= 0 && id < a.max_slots && ldl[id] != 0;
-        if (!ok && id != -1) s_err = 1;
-        const int v = ok ? id : -1;
-        a.vid[t] = v;
-        if (in_lds) vid_l[t] = v;
-        if (ok) atomicAdd(&cnt[id], 1);
-    }
-    __syncthreads();
-
-    // exclusive scan over slots of (tokens, groups, shrink items)
-    const int per = (a.max_slots + 1023) / 1024;
-    const int s0 = min(tid * per, a.max_slots), s1 = min(s0 + per, a.max_slots);
-    int tok = 0, grp = 0, itm = 0;
-    for (int s = s0; s < s1; ++s) {
-        const int c = cnt[s];
-        tok += c;
-        grp += c > 0;
-        itm += (c + a.mts - 1) / a.mts;
-    }
-    const int et = wave_excl_scan(tok, lane), eg = wave_excl_scan(grp, lane), ei = wave_excl_scan(itm, lane);
-    if (lane == 63) {
-        wsum[wv][0] = et + tok;
-        wsum[wv][1] = eg + grp;
-        wsum[wv][2] = ei + itm;
-    }
-    __syncthreads();
-    if (tid < 3) {
-        int acc = 0;
-        for (int w = 0; w < 16; ++w) {
-            wpre[w][tid] = acc;
-            acc += wsum[w][tid];
-        }
-    }
-    __syncthreads();
-    int tok_off = wpre[wv][0] + et;
-    int g_off = wpre[wv][1] + eg;
-    int i_off = wpre[wv][2] + ei;
-    for (int s = s0; s < s1; ++s) {
-        const int c = cnt[s];
-        if (c > 0) {
-            a.gslot[g_off] = s;
-            a.gstart[g_off] = tok_off;
-            a.gcount[g_off] = c;
-            for (int r = 0; r < c; r += a.mts)
-                a.items[i_off++] = make_int4(s, tok_off + r, min(a.mts, c - r), r8l[s]);
-            ++g_off;
-        }
-        cnt[s] = tok_off;                     // cursor for the placement below
-        tok_off += c;
-    }
-    if (tid == 1023) {
-        a.meta[0] = g_off;
-        a.meta[1] = i_off;
-    }
-    __syncthreads();
-
-    if (wv == 0) {
-        // stable placement, tokens in order, 64 per step
-        for (int base = 0; base < a.T; base += 64) {
-            const int t = base + lane;
-            const int v = t < a.T ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
-            bool ok = v >= 0;
-            unsigned long long act = __ballot(ok);
-            while (act) {
-                const int leader = __ffsll((long long)act) - 1;
-                const int s = __shfl(v, leader);
-                const bool mine = ok && v == s;
-                const unsigned long long m = __ballot(mine);
-                const int b = cnt[s];
-                if (lane == leader) cnt[s] = b + __popcll(m);
-                if (mine) {
-                    a.perm[b + __popcll(m & ((1ull << lane) - 1ull))] = t;
-                    ok = false;
-                }
-                act &= ~m;
-            }
-        }
-    } else {
-        // expand octet lists of the base-GEMM row tiles, one tile per wave
-        const int mt = a.gemm_mt;
-        const int tiles = (a.T + mt - 1) / mt;
-        for (int m = wv - 1; m < tiles; m += 15) {
-            const int t = m * mt + lane;
-            int v = (lane < mt && t < a.T) ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
-            bool active = v >= 0;
-            int my_slot = -1, nd = 0;
-            while (__ballot(active)) {
-                const int sm = wave_min(active ? v : 0x7fffffff);
-                if (lane == nd) my_slot = sm;
-                if (v == sm) active = false;
-                ++nd;
-            }
-            const int r8s = my_slot >= 0 ? r8l[my_slot] : 0;
-            const int c = r8s >> 3;
-            const int pos = wave_excl_scan(c, lane);
-            int* dst = a.tile_oct + (size_t)m * a.oct_cap;
-            for (int j = 0; j < c; ++j) dst[pos + j] = (my_slot << 12) | (r8s << 4) | j;
-            const int total = __shfl(pos + c, 63);
-            for (int i = total + lane; i < a.oct_cap; i += 64) dst[i] = -1;
-        }
-    }
-    if (tid == 0 && s_err) atomicOr(a.err, 1);
-}
-
-hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
-    int pack_blocks = (a.total_frags + 15) / 16;
-    if (pack_blocks > 1024) pack_blocks = 1024;
-    hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), 3 * a.max_slots * sizeof(int), s, a);
-    return hipGetLastError();
-}
-
-// --------------------------------------------------------------------------
 // 2. shrink: Z[t, sigma * r8max + j] = scale_a * sum_k X[t, k] A_a,sigma[k, j]
 //    work item = (projection, shrink item, 16*NB-column chunk of A^T_cat)
 // --------------------------------------------------------------------------

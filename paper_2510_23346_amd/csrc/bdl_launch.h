@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "bdlora.h"
+
 namespace bdl {
 
 constexpr int kMaxProjs = 8;
@@ -68,6 +70,7 @@ struct PrepArgs {
     int gemm_mt;              // base GEMM row tile (<= 64)
     int oct_cap;
     int* vid;
+    int* tr8;                 // [T] rank (padded to 8) of each token's adapter, 0 if none
     int* perm;
     int* gslot;
     int* gstart;
@@ -81,7 +84,51 @@ struct PrepArgs {
     int total_frags;
 };
 
-// Host-side launchers (bdl_kernels.hip).
+// ---- decode path (T <= kDecodeMaxT): split-K partials + epilogue -------------
+constexpr int kDecodeMaxT = BDLORA_DECODE_MAX_T;
+constexpr int kMaxKSplit = 8;
+
+struct DecProj {
+    const uint16_t* Xp;       // packed activations (fragment layout)
+    const uint16_t* W;        // packed base weight
+    uint16_t* out;            // [T x N] bf16
+    float* Yp;                // [ks x kDecodeMaxT x N] fp32 partial base products
+    float* Zp;                // [ks x kDecodeMaxT x zs] fp32 partial scale * X A
+    int K, N, n_slices, zs;
+    int slice_col[kMaxSlices + 1];
+    long long a_off, b_off;
+    int ks;                   // K splits of this projection
+    int kchunk;               // k-steps per split
+    int cchunks;              // shrink: 64-column chunks of A^T_cat (upper bound)
+    int tiles_n;              // 64-column tiles
+    int gemm_base;            // first base-GEMM item of this projection
+    int shrink_base;          // first shrink slot of this projection
+    int epi_base;             // first epilogue unit (8 outputs) of this projection
+};
+
+struct DecArgs {
+    DecProj p[kMaxProjs];
+    int n_proj;
+    int T;
+    const uint16_t* pool;
+    long long slot_stride;
+    int r8max;
+    const float* scale;       // [max_slots]
+    const int* r8;            // [max_slots]
+    const int* vid;
+    const int* tr8;           // [T] padded rank of each token's adapter (0: none)
+    const int* perm;
+    const int4* items;
+    const int* meta;          // [1] number of shrink items
+    int items_bound;
+    int shrink_slots;         // shrink slots over all projections
+    int gemm_items;
+    int epi_units;
+};
+
+// Host-side launchers (bdl_kernels.hip, bdl_prep.hip, bdl_decode.hip).
+hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s);
+hipError_t launch_dec_epi(const DecArgs& a, hipStream_t s);
 hipError_t launch_prep(const PrepArgs& a, hipStream_t s);
 hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);

@@ -1,0 +1,209 @@
+// Prep launch of a forward call: workgroup 0 plans the batch, the others pack
+// the activations into the MFMA fragment layout.
+//
+// Plan outputs (integer work, compared bit-exactly with the host plan):
+//   vid[t]      validated id (-1: none or invalid; invalid ones raise *err)
+//   tr8[t]      rank (padded to 8) of token t's adapter, 0 if none
+//   groups      (slot, start, count) per adapter in use, slots ascending
+//   perm        tokens group after group, ascending inside a group
+//   items       shrink work items {slot, first perm index, rows <= mts, r8}
+//   tile_oct    (when asked for) per base-GEMM row tile: the 8-rank octets of
+//               every adapter present in the tile, slots ascending, code =
+//               slot<<12 | r8<<4 | octet, padded with -1 to oct_cap entries
+// Tokens are grouped by adapter (a counting sort over slots) so that every
+// adapter's factors are streamed once per batch (heterogeneous batching of
+// unmerged adapters, paper Sec. 1 and Sec. 2).
+#include "bdl_device.h"
+
+namespace bdl {
+
+// inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row
+// broadcasts of lanes 15 and 31)
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return v;
+}
+
+__device__ __forceinline__ int wave_total(int incl) { return __builtin_amdgcn_readlane(incl, 63); }
+
+// activations -> fragment layout (all workgroups but 0)
+__device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
+    const int l = threadIdx.x & 63;
+    for (int f = blk * 16 + (threadIdx.x >> 6); f < a.total_frags; f += nblk * 16) {
+        int j = 0;
+        while (j + 1 < a.n_jobs && f >= a.jobs[j + 1].frag_base) ++j;
+        const PackJob& J = a.jobs[j];
+        const int KS = J.K >> 5;
+        const int local = f - J.frag_base;
+        const int rb = local / KS, ks = local - rb * KS;
+        const int row = rb * 16 + (l & 15);
+        u32x4 v = u32x4{0u, 0u, 0u, 0u};
+        if (row < J.rows) v = ld16(J.src + (size_t)row * J.K + ks * 32 + (l >> 4) * 8);
+        *reinterpret_cast<u32x4*>(J.dst + (size_t)local * kFrag + l * 8) = v;
+    }
+}
+
+__global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
+    if (blockIdx.x > 0) {
+        pack_activations(a, blockIdx.x - 1, gridDim.x - 1);
+        return;
+    }
+    extern __shared__ int tabs[];             // cnt | r8 | loaded | 15 tile bitmaps
+    const int nwords = (a.max_slots + 31) >> 5;
+    int* cnt = tabs;                          // counts, then group starts
+    int* r8l = tabs + a.max_slots;
+    int* ldl = tabs + 2 * a.max_slots;
+    unsigned* bits = reinterpret_cast<unsigned*>(tabs + 3 * a.max_slots);
+    __shared__ int vid_l[kPlanLdsTokens];
+    __shared__ int s_err;
+    __shared__ int wsum[16][3];
+    __shared__ int wpre[16][3];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const bool in_lds = a.T <= kPlanLdsTokens;
+
+    for (int s = tid; s < a.max_slots; s += 1024) {
+        cnt[s] = 0;
+        r8l[s] = a.r8[s];
+        ldl[s] = a.loaded[s];
+    }
+    if (tid == 0) s_err = 0;
+    __syncthreads();
+    for (int t = tid; t < a.T; t += 1024) {
+        const int id = a.ids[t];
+        const bool ok = id >= 0 && id < a.max_slots && ldl[id] != 0;
+        if (!ok && id != -1) s_err = 1;
+        const int v = ok ? id : -1;
+        a.vid[t] = v;
+        a.tr8[t] = ok ? r8l[id] : 0;
+        if (in_lds) vid_l[t] = v;
+        if (ok) atomicAdd(&cnt[id], 1);
+    }
+    __syncthreads();
+
+    // exclusive scan over slots of (tokens, groups, shrink items)
+    const int per = (a.max_slots + 1023) / 1024;
+    const int s0 = min(tid * per, a.max_slots), s1 = min(s0 + per, a.max_slots);
+    int tok = 0, grp = 0, itm = 0;
+    for (int s = s0; s < s1; ++s) {
+        const int c = cnt[s];
+        tok += c;
+        grp += c > 0;
+        itm += (c + a.mts - 1) / a.mts;
+    }
+    const int it = wave_incl_scan(tok), ig = wave_incl_scan(grp), ii = wave_incl_scan(itm);
+    if (lane == 63) {
+        wsum[wv][0] = it;
+        wsum[wv][1] = ig;
+        wsum[wv][2] = ii;
+    }
+    __syncthreads();
+    if (tid < 3) {
+        int acc = 0;
+        for (int w = 0; w < 16; ++w) {
+            wpre[w][tid] = acc;
+            acc += wsum[w][tid];
+        }
+    }
+    __syncthreads();
+    int tok_off = wpre[wv][0] + it - tok;
+    int g_off = wpre[wv][1] + ig - grp;
+    int i_off = wpre[wv][2] + ii - itm;
+    for (int s = s0; s < s1; ++s) {
+        const int c = cnt[s];
+        if (c > 0) {
+            a.gslot[g_off] = s;
+            a.gstart[g_off] = tok_off;
+            a.gcount[g_off] = c;
+            for (int r = 0; r < c; r += a.mts)
+                a.items[i_off++] = make_int4(s, tok_off + r, min(a.mts, c - r), r8l[s]);
+            ++g_off;
+        }
+        cnt[s] = tok_off;                     // group start for the placement below
+        tok_off += c;
+    }
+    if (tid == 1023) {
+        a.meta[0] = g_off;
+        a.meta[1] = i_off;
+    }
+    __syncthreads();
+
+    // stable placement: perm[start(v) + #{t' < t : vid[t'] == v}] = t
+    if (a.T <= 1024) {
+        const int t = tid;
+        const int v = t < a.T ? vid_l[t] : -1;
+        if (v >= 0) {
+            int rank = 0;
+            for (int u = 0; u < t; ++u) rank += vid_l[u] == v;
+            a.perm[cnt[v] + rank] = t;
+        }
+    } else if (wv == 0) {
+        for (int base = 0; base < a.T; base += 64) {
+            const int t = base + lane;
+            const int v = t < a.T ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
+            bool ok = v >= 0;
+            unsigned long long act = __ballot(ok);
+            while (act) {
+                const int leader = __ffsll((long long)act) - 1;
+                const int s = __shfl(v, leader);
+                const bool mine = ok && v == s;
+                const unsigned long long m = __ballot(mine);
+                const int b = cnt[s];
+                if (lane == leader) cnt[s] = b + __popcll(m);
+                if (mine) {
+                    a.perm[b + __popcll(m & ((1ull << lane) - 1ull))] = t;
+                    ok = false;
+                }
+                act &= ~m;
+            }
+        }
+    }
+
+    // expand octet lists of the base-GEMM row tiles, one tile per wave
+    if (a.tile_oct && wv > 0) {
+        const int mt = a.gemm_mt;
+        const int tiles = (a.T + mt - 1) / mt;
+        unsigned* bm = bits + (size_t)(wv - 1) * nwords;
+        for (int m = wv - 1; m < tiles; m += 15) {
+            for (int i = lane; i < nwords; i += 64) bm[i] = 0u;
+            __builtin_amdgcn_wave_barrier();
+            const int t = m * mt + lane;
+            const int v = (lane < mt && t < a.T) ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
+            if (v >= 0) atomicOr(&bm[v >> 5], 1u << (v & 31));
+            __builtin_amdgcn_wave_barrier();
+            int* dst = a.tile_oct + (size_t)m * a.oct_cap;
+            int base = 0;
+            for (int wb = 0; wb < nwords; wb += 64) {
+                const int wi = wb + lane;
+                const unsigned word = wi < nwords ? bm[wi] : 0u;
+                int c = 0;
+                for (unsigned b = word; b; b &= b - 1u) c += r8l[wi * 32 + __ffs(b) - 1] >> 3;
+                const int inc = wave_incl_scan(c);
+                int o = base + inc - c;
+                for (unsigned b = word; b; b &= b - 1u) {
+                    const int slot = wi * 32 + __ffs(b) - 1;
+                    const int r8s = r8l[slot];
+                    for (int j = 0; j < (r8s >> 3); ++j) dst[o++] = (slot << 12) | (r8s << 4) | j;
+                }
+                base += wave_total(inc);
+            }
+            for (int i = base + lane; i < a.oct_cap; i += 64) dst[i] = -1;
+        }
+    }
+    if (tid == 0 && s_err) atomicOr(a.err, 1);
+}
+
+hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
+    int pack_blocks = (a.total_frags + 15) / 16;
+    if (pack_blocks > 1024) pack_blocks = 1024;
+    const int nwords = (a.max_slots + 31) >> 5;
+    const size_t lds = 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
+    hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), lds, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace bdl

@@ -36,6 +36,16 @@ def test_exports_every_declared_function(L):
     assert sorted(bd.HEADER_FUNCTIONS) == names
 
 
+def test_binding_constants_match_header():
+    text = open(os.path.join(ROOT, "include", "bdlora.h")).read()
+    macros = dict(re.findall(r"^#define (BDLORA_\w+)\s+\(?(-?\d+)\)?", text, re.M))
+    assert int(macros["BDLORA_DECODE_MAX_T"]) == bd.DECODE_MAX_T
+    assert int(macros["BDLORA_MAX_SLICES"]) == bd.MAX_SLICES
+    assert (int(macros["BDLORA_COLUMN"]), int(macros["BDLORA_ROW"])) == (bd.COLUMN, bd.ROW)
+    for code, name in bd.STATUS.items():
+        assert int(macros["BDLORA_" + ("OK" if code == 0 else "ERR_" + name)]) == code
+
+
 def test_adapter_elems_reproduce_paper_counts(L):
     # per-shard elements x N shards x layers = the paper's BD-LoRA counts
     for model, tp, r_total, mill in [("llama-3.1-8b", 8, 32, 36.2), ("llama-3.1-8b", 8, 512, 578.8),

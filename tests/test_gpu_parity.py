@@ -103,6 +103,20 @@ def test_base_only_rows_equal_no_adapter_rows(torch_cuda):
     pool.close()
 
 
+def test_decode_path_is_deterministic(torch_cuda):
+    torch = torch_cuda
+    T = 40
+    spec = wl.custom_workload("det-dec", wl.tiny_projs(), T, [8, 16, 4], seed=6)
+    layer = wl.draw_layer(spec, slots=[0, 1, 2])
+    pool = make_pool(spec)
+    load_adapters(pool, spec, [0, 1, 2], cache=layer.adapters)
+    _, y1 = _run_layer(torch, spec, layer, pool)
+    _, y2 = _run_layer(torch, spec, layer, pool)
+    for a, b in zip(y1, y2):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    pool.close()
+
+
 def test_deterministic_and_shard_equals_layer(torch_cuda):
     torch = torch_cuda
     T = 70
