@@ -47,6 +47,7 @@ struct Layout {
     long long slab_bytes = 0, ws_bytes = 0;
     long long z_elems[bdl::kMaxProjs];
     long long xp_elems[bdl::kMaxProjs];
+    long long part_slots = 0;          // decode partial tiles
 };
 
 // Validates the pool arguments and computes the memory layout.
@@ -108,10 +109,16 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
     ws += ((long long)max_slots + max_tokens / 16 + 2) * 16;      // shrink items
     ws += std::max(((long long)max_tokens / 16 + 1) * (2LL * L->r8max + 64),
                    ((long long)max_tokens / 64 + 1) * (8LL * L->r8max + 64)) * 4;   // tile octets
+    for (int p = 0; p < n_projs; ++p) ws += (L->z_elems[p] + L->xp_elems[p]) * 2;
+    // decode partial tiles: one per (group, workgroup) pair of the main launch
+    long long groups = 0;
+    const int act_max = std::min({bdl::kDecodeMaxT, max_slots, max_tokens});
     for (int p = 0; p < n_projs; ++p) {
-        ws += (L->z_elems[p] + L->xp_elems[p]) * 2;
-        ws += (long long)bdl::kMaxKSplit * bdl::kDecodeMaxT * (L->proj[p].N + L->proj[p].zs) * 4;
+        const ProjInfo& P = L->proj[p];
+        groups += (P.N / 16 + (long long)act_max * ((P.S * L->r8max + 15) / 16) + 3) / 4;
     }
+    L->part_slots = groups + bdl::kDecMaxGrid;
+    ws += L->part_slots * bdl::kPartElems * 4 + (long long)max_tokens * 4;
     ws += max_slots * 12LL;                                       // slot tables
     L->ws_bytes = ws;
     return BDLORA_OK;
@@ -151,8 +158,9 @@ struct bdlora_pool {
     int* d_meta = nullptr;
     int* d_err = nullptr;
     uint16_t* d_Z[bdl::kMaxProjs] = {};
-    float* d_Yp[bdl::kMaxProjs] = {};
-    float* d_Zp[bdl::kMaxProjs] = {};
+    int* d_tgrp = nullptr;
+    float* d_part = nullptr;
+    int n_cu = 0;
     uint16_t* d_Xp[bdl::kMaxProjs] = {};
     uint16_t* d_stage = nullptr;
     long long stage_elems = 0;
@@ -186,8 +194,8 @@ void free_pool(bdlora_pool* P) {
     f(P->d_meta);
     f(P->d_err);
     for (auto z : P->d_Z) f(z);
-    for (auto y : P->d_Yp) f(y);
-    for (auto z : P->d_Zp) f(z);
+    f(P->d_tgrp);
+    f(P->d_part);
     for (auto x : P->d_Xp) f(x);
     f(P->d_stage);
     for (auto e : P->prof_ev) (void)hipEventDestroy(e);
@@ -298,6 +306,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     bdlora_pool* P = new bdlora_pool();
     P->device = device;
     P->L = L;
+    P->n_cu = std::max(1, prop.multiProcessorCount);
     long long tot = 0;
     const int S = max_slots, MT = max_tokens;
 #define BDL_TRY(x)         \
@@ -314,6 +323,8 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_loaded, S, &tot));
     BDL_TRY(dev_alloc(&P->d_vid, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_tr8, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_tgrp, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_part, L.part_slots * bdl::kPartElems, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
@@ -329,8 +340,6 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     for (int p = 0; p < n_projs; ++p) {
         BDL_TRY(dev_alloc(&P->d_Z[p], L.z_elems[p], &tot));
         BDL_TRY(dev_alloc(&P->d_Xp[p], L.xp_elems[p], &tot));
-        BDL_TRY(dev_alloc(&P->d_Yp[p], (long long)bdl::kMaxKSplit * bdl::kDecodeMaxT * L.proj[p].N, &tot));
-        BDL_TRY(dev_alloc(&P->d_Zp[p], (long long)bdl::kMaxKSplit * bdl::kDecodeMaxT * L.proj[p].zs, &tot));
         const ProjInfo& pi = L.proj[p];
         stage = std::max(stage, (long long)pi.S * pi.K * std::max(1, max_rank) + (long long)std::max(1, max_rank) * pi.N);
     }
@@ -498,6 +507,7 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->oct_cap = oct_cap(P->L, 16 * k.gmb);
     a->vid = P->d_vid;
     a->tr8 = P->d_tr8;
+    a->tgrp = nullptr;
     a->perm = P->d_perm;
     a->gslot = P->d_gslot;
     a->gstart = P->d_gstart;
@@ -510,74 +520,61 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->total_frags = 0;
 }
 
-// Decode batches: prep (plan + activation packing), one launch of K-split
-// shrink and base items writing fp32 partials, one epilogue launch.
+// Decode batches: prep (plan + activation packing), the split-K main launch
+// over W_s and the used adapters' A^T, the epilogue.
 static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
                           const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s) {
     const Layout& L = P->L;
-    std::vector<int> order(n);
-    for (int i = 0; i < n; ++i) order[i] = i;
-    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-        return (long long)L.proj[projs[x]].K * L.proj[projs[x]].N > (long long)L.proj[projs[y]].K * L.proj[projs[y]].N;
-    });
     int n_loaded = 0;
     for (int v : P->h_loaded) n_loaded += v != 0;
-    // K chunk so that about 512 base items cover the batch (two per CU: the
-    // kernel holds two workgroups per CU), a multiple of the 8 waves
-    long long work = 0;
-    for (int i = 0; i < n; ++i) work += (long long)((L.proj[projs[i]].N + 63) / 64) * (L.proj[projs[i]].K / 32);
-    int kc = (int)((work + 511) / 512);
-    kc = std::max(8, (kc + 7) / 8 * 8);
+    const int act_max = std::min(T, n_loaded);
 
     bdl::DecArgs da;
     std::memset(&da, 0, sizeof(da));
-    const int items_bound = std::min(T, std::max(n_loaded, 1)) + (T + 15) / 16;
-    int shrink = 0, gemm = 0, epi = 0;
-    for (int q = 0; q < n; ++q) {
-        const int i = order[q];
+    long long units_min = 0, units_max = 0, groups_max = 0;
+    int tiles = 0;
+    for (int i = 0; i < n; ++i) {
         const ProjInfo& pi = L.proj[projs[i]];
-        bdl::DecProj& d = da.p[q];
+        bdl::DecProj& d = da.p[i];
         d.Xp = P->d_Xp[projs[i]];
         d.W = (const uint16_t*)W[i];
         d.out = (uint16_t*)out[i];
-        d.Yp = P->d_Yp[projs[i]];
-        d.Zp = P->d_Zp[projs[i]];
         d.K = pi.K;
         d.N = pi.N;
         d.n_slices = pi.S;
-        d.zs = pi.zs;
         for (int t = 0; t <= bdl::kMaxSlices; ++t) d.slice_col[t] = pi.slice_col[t];
         d.a_off = pi.a_off;
         d.b_off = pi.b_off;
-        const int KS = pi.K / 32;
-        d.ks = std::min(bdl::kMaxKSplit, std::max(1, (KS + kc - 1) / kc));
-        d.kchunk = (KS + d.ks - 1) / d.ks;
-        d.cchunks = (pi.S * L.r8max + 63) / 64;
-        d.tiles_n = (pi.N + 63) / 64;
-        d.shrink_base = shrink;
-        shrink += items_bound * d.cchunks * d.ks;
-        d.gemm_base = gemm;
-        gemm += d.tiles_n * d.ks;
-        d.epi_base = epi;
-        epi += T * (pi.N / 8);
+        d.nWb = pi.N / 16;
+        d.nbA = (pi.S * L.r8max + 15) / 16;
+        d.tile_base = tiles;
+        tiles += (pi.N + 63) / 64;
+        units_min += (long long)d.nWb * (pi.K / 32);
+        units_max += (d.nWb + (long long)act_max * d.nbA) * (pi.K / 32);
+        groups_max += (d.nWb + (long long)act_max * d.nbA + 3) / 4;
     }
+    // two workgroups per CU, each with at least 4 units (one k-step of a
+    // full group) whatever the number of adapters in use; the kernels' 32-bit
+    // schedule arithmetic needs units * workgroups < 2^32
+    const int grid = (int)std::min<long long>(
+        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, units_min / 4, 0xffffffffLL / std::max(1LL, units_max)});
+    if (grid < 1) return fail(BDLORA_ERR_SHAPE, "projection too small for the decode launch");
+    if (groups_max + grid > L.part_slots) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
     da.n_proj = n;
     da.T = T;
     da.pool = P->d_slabs;
     da.slot_stride = L.slot_stride;
-    da.r8max = L.r8max;
     da.scale = P->d_scale;
-    da.r8 = P->d_r8;
     da.vid = P->d_vid;
     da.tr8 = P->d_tr8;
-    da.perm = P->d_perm;
-    da.items = P->d_items;
+    da.tgrp = P->d_tgrp;
+    da.gslot = P->d_gslot;
     da.meta = P->d_meta;
-    da.items_bound = items_bound;
-    da.shrink_slots = shrink;
-    da.gemm_items = gemm;
-    da.epi_units = epi;
-    if (items_bound > P->items_cap) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
+    da.part = P->d_part;
+    da.part_slots = (int)L.part_slots;
+    da.main_grid = grid;
+    da.tiles = tiles;
+    da.err = P->d_err;
 
     Shapes k;
     k.smb = 1;
@@ -587,11 +584,12 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     bdl::PrepArgs pa;
     fill_plan_args(P, ids, T, &pa, k);
     pa.tile_oct = nullptr;                        // the epilogue needs no octet lists
+    pa.tgrp = P->d_tgrp;
     int frags = 0;
     for (int q = 0; q < n; ++q) {
         bdl::PackJob& J = pa.jobs[q];
-        J.src = (const uint16_t*)X[order[q]];
-        J.dst = P->d_Xp[projs[order[q]]];
+        J.src = (const uint16_t*)X[q];
+        J.dst = P->d_Xp[projs[q]];
         J.rows = T;
         J.K = da.p[q].K;
         J.frag_base = frags;

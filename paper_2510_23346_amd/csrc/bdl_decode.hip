@@ -1,20 +1,28 @@
 // Decode path (batches of at most kDecodeMaxT tokens): two launches after
-// the prep launch.
+// the prep launch (plan + activation packing).
 //
-//  dec_main_kernel -- one grid holding two kinds of work items, all of about
-//                     the same size so the 256 CUs stay evenly loaded:
-//                     * shrink items: Zp[s] = scale * X_rows A over the s-th K
-//                       chunk, for one adapter group and up to 64 rank
-//                       columns (Alg. 1 / Alg. 2 step "Z <- X A");
-//                     * base items: Yp[s] = X W_s^T over the s-th K chunk of a
-//                       64-column tile (step "Y <- X W").
-//                     Items with no work (past the batch's shrink items) exit
-//                     at once.  The 8 waves of an item split its columns in
-//                     two halves and its k-steps in four quarters, and reduce
-//                     the quarters through LDS in a fixed order.
-//  dec_epi_kernel  -- out[t, n] = sum_s Yp[s][t][n]
-//                                 + sum_j (sum_s Zp[s][t][j]) B^T[n][j]
-//                     (steps "Y_adapter <- Z B" and "Y <- Y + Y_adapter"),
+//  dec_main_kernel -- one split-K GEMM of the packed activations X [T x K]
+//                     against a virtual column list per projection: the
+//                     16-column blocks of W_s, then the blocks of A^T_cat of
+//                     every adapter the batch uses.  So one pass streams the
+//                     base weight once (step "Y <- X W" of Alg. 1 / Alg. 2)
+//                     and every used adapter's A once (step "Z <- X A"),
+//                     computing Z for all tokens against all used adapters;
+//                     the epilogue keeps each token's own.  Work is counted in
+//                     units of one block times one 32-wide k-step; consecutive
+//                     blocks form groups of 4, and workgroup b takes the
+//                     k-steps whose first unit lies in [b U / G, (b+1) U / G),
+//                     so all G workgroups stream the same number of bytes.
+//                     Workgroups are 8 waves: 2 column halves x 4 quarters of
+//                     the k-range.
+//                     Each (group, workgroup) pair writes one fp32 partial
+//                     tile to slot g + b (injective: along the unit order both
+//                     indices only grow).
+//  dec_epi_kernel  -- per 64-column output tile, all tokens:
+//                     out[t, n] = sum of the tile's partials
+//                                 + scale * sum_j Z[t, j] B^T[n, j]
+//                     with Z[t, :] summed from the partials of the token's own
+//                     adapter (steps "Y_adapter <- Z B", "Y <- Y + Y_adapter"),
 //                     in fp32, one bf16 store per output.
 #include "bdl_device.h"
 
@@ -22,143 +30,150 @@ namespace bdl {
 
 constexpr int kDecStages = 2;
 
-// Eight waves as 2 column halves x 4 K-quarters: wave w owns column blocks
-// 2 (w & 1) and 2 (w & 1) + 1 of the item's four, over the (w >> 1)-th
-// quarter of its k-steps.  The three upper quarters hand their accumulators
-// to the first through LDS (one barrier); the first-quarter waves then hold
-// the item's result in the MFMA output layout.
+// Position of projection p in the unit and group orders for n_act adapters
+// in use.  Everything here derives from kernel arguments and one uniform
+// load, so it stays in scalar registers.
+struct ProjPos {
+    unsigned ub;    // first unit (the host keeps U * G below 2^32)
+    int gb;         // first group
+    int nb;         // virtual blocks
+    int KS;         // k-steps
+};
+
+__device__ __forceinline__ int dec_nblk(const DecArgs& a, int n_act, int p) {
+    return a.p[p].nWb + n_act * a.p[p].nbA;
+}
+
+__device__ __forceinline__ ProjPos dec_pos(const DecArgs& a, int n_act, int p) {
+    unsigned u = 0;
+    int g = 0;
+    for (int q = 0; q < p; ++q) {
+        const int nb = dec_nblk(a, n_act, q);
+        u += (unsigned)nb * (unsigned)(a.p[q].K >> 5);
+        g += (nb + 3) >> 2;
+    }
+    return ProjPos{u, g, dec_nblk(a, n_act, p), a.p[p].K >> 5};
+}
+
+__device__ __forceinline__ unsigned dec_units(const DecArgs& a, int n_act) {
+    unsigned u = 0;
+    for (int q = 0; q < a.n_proj; ++q) u += (unsigned)dec_nblk(a, n_act, q) * (unsigned)(a.p[q].K >> 5);
+    return u;
+}
+
+// workgroup whose unit range holds unit u: largest b with floor(b U / G) <= u
+__device__ __forceinline__ int dec_wg_of(unsigned u, unsigned U, int G) {
+    return (int)(((u + 1) * (unsigned)G - 1) / U);
+}
+
+// Eight waves as 2 column halves x 4 K-quarters: wave w owns blocks
+// 2 (w & 1) and 2 (w & 1) + 1 of the group (nbw of them exist), over the
+// (w >> 1)-th quarter of the k-range.  The four quarters meet in LDS; all 512
+// threads then add them in a fixed order and store the group's fp32 partial
+// (rows < T, the group's wdt blocks) as 16-byte chunks.
+constexpr int kRedLd = 68;    // LDS row stride (floats): 4 rows apart land 16 banks apart
+
 template <int MB>
-__device__ __forceinline__ void item_tile(f32x4 (&acc)[MB][2], const uint16_t* const (&ap)[MB],
-                                          const uint16_t* const (&bp)[2], int kb, int ke, float* red) {
-    constexpr int MT = MB * 16, LD = 36, REG = MT * LD;
+__device__ __forceinline__ void seg_tile(const uint16_t* const (&ap)[MB], const uint16_t* const (&bp)[2],
+                                         int kb, int ke, int nbw, int wdt, float* red, float* dst, int T) {
+    constexpr int REG = MB * 16 * kRedLd;
     const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1, kq = w >> 1;
+    f32x4 acc[MB][2];
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int n = ke - kb, q = n >> 2, r = n & 3;
     const int k0 = kb + kq * q + min(kq, r), nk = q + (kq < r ? 1 : 0);
-    if (nk > 0) mma_range<MB, 2, kDecStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
-    if (kq > 0) {
-        float* dst = red + ((kq - 1) * 2 + cg) * REG;
+    // a wave with one block loads it twice (second copy discarded): narrow
+    // groups only end a projection's column list
+    if (nk > 0 && nbw > 0) mma_range<MB, 2, kDecStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
+    __syncthreads();                          // the previous segment's readers are done
+    if (nbw > 0) {
+        float* reg = red + kq * REG + cg * 32 + (l & 15);
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) dst[(rb * 16 + 4 * (l >> 4) + i) * LD + cb * 16 + (l & 15)] = acc[rb][cb][i];
+                for (int i = 0; i < 4; ++i) reg[(rb * 16 + 4 * (l >> 4) + i) * kRedLd + cb * 16] = acc[rb][cb][i];
     }
     __syncthreads();
-    if (kq == 0) {
+    const int nc4 = wdt * 4;
 #pragma unroll
-        for (int j = 0; j < 3; ++j) {
-            const float* src = red + (j * 2 + cg) * REG;
+    for (int j = 0; j < (MB * 16 * 16 + kThreads - 1) / kThreads; ++j) {
+        const int c = threadIdx.x + j * kThreads;
+        const int row = c >> 4, c4 = c & 15;
+        if (c < MB * 16 * 16 && row < T && c4 < nc4) {
+            const float* src = red + row * kRedLd + c4 * 4;
+            float4 v = *reinterpret_cast<const float4*>(src);
 #pragma unroll
-            for (int rb = 0; rb < MB; ++rb)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[rb][cb][i] += src[(rb * 16 + 4 * (l >> 4) + i) * LD + cb * 16 + (l & 15)];
+            for (int k = 1; k < 4; ++k) {
+                const float4 u = *reinterpret_cast<const float4*>(src + k * REG);
+                v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+            }
+            *reinterpret_cast<float4*>(dst + row * 64 + c4 * 4) = v;
         }
     }
+}
+
+// element pointer of k-step 0 of virtual block vb of projection P
+__device__ __forceinline__ const uint16_t* dec_block(const DecArgs& a, const DecProj& P, int vb, int KS) {
+    if (vb < P.nWb) return P.W + frag_index(vb, 0, KS);
+    const int ai = (vb - P.nWb) / P.nbA, c = vb - P.nWb - ai * P.nbA;
+    const int slot = a.gslot[ai];
+    return a.pool + (size_t)slot * a.slot_stride + P.a_off + frag_index(c, 0, KS);
 }
 
 template <int MB>
 __global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
-    constexpr int MT = MB * 16, NT = 64, LDR = 36;
-    __shared__ float red[6 * (MT > 16 ? MT : 16) * LDR];
-    const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15, cg = w & 1, kq = w >> 1;
-    int b = blockIdx.x;
+    __shared__ float red[4 * MB * 16 * kRedLd];
+    const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1;
+    const int n_act = a.meta[0];
+    const int G = gridDim.x, b = blockIdx.x;
+    const unsigned U = dec_units(a, n_act);
+    if (U == 0) return;
+    const unsigned sb = (unsigned)b * U / (unsigned)G, se = (unsigned)(b + 1) * U / (unsigned)G;
 
-    if (b < a.shrink_slots) {
-        // ---- shrink item: 16 token rows of one adapter group x 64 A^T rows
-        int p = 0;
-        while (p + 1 < a.n_proj && b >= a.p[p + 1].shrink_base) ++p;
-        const DecProj& P = a.p[p];
-        const int local = b - P.shrink_base;
-        const int item = local / (P.cchunks * P.ks);
-        const int rem = local - item * (P.cchunks * P.ks);
-        const int cc = rem / P.ks, s = rem - cc * P.ks;
-        const int n_items = a.meta[1];
-        if (item >= n_items) return;
-        const int4 it = a.items[item];
-        const int slot = it.x, nrows = it.z, r8s = it.w;
-        const int ncols = P.n_slices * r8s;
-        const int c0 = cc * NT;
-        if (c0 >= ncols) return;
-        const float sc = a.scale[slot];
-        const int* prow = a.perm + it.y;
-        const int KS = P.K >> 5;
-        const int nblk = (ncols + 15) >> 4;
-        const uint16_t* abase = a.pool + (size_t)slot * a.slot_stride + P.a_off;
-        const uint16_t* ap[1];
-        const uint16_t* bp[2];
-        {
-            const int t = prow[min(lr, nrows - 1)];
-            ap[0] = P.Xp + frag_index(t >> 4, 0, KS) + ((t & 15) + 16 * (l >> 4)) * 8;
+    // group holding unit sb, and its first k-step starting at or after sb
+    int p = 0;
+    ProjPos pp = dec_pos(a, n_act, 0);
+    while (p + 1 < a.n_proj && sb >= pp.ub + (unsigned)pp.nb * pp.KS) pp = dec_pos(a, n_act, ++p);
+    int gl = min((int)((sb - pp.ub) / (4u * pp.KS)), ((pp.nb + 3) >> 2) - 1);
+    unsigned goff = pp.ub + 4u * gl * pp.KS;
+    int wdt = min(4, pp.nb - 4 * gl);
+    int k0 = (int)((sb - goff + wdt - 1) / (unsigned)wdt);
+    for (;;) {
+        if (k0 >= pp.KS) {                    // next group (next projection after the last)
+            if (++gl >= ((pp.nb + 3) >> 2)) {
+                if (++p >= a.n_proj) break;
+                pp = dec_pos(a, n_act, p);
+                gl = 0;
+            }
+            goff = pp.ub + 4u * gl * pp.KS;
+            wdt = min(4, pp.nb - 4 * gl);
+            k0 = 0;
+            if (goff >= se) break;
         }
+        const int KS = pp.KS;
+        const int k1 = (int)min((unsigned)KS, (se - goff + wdt - 1) / (unsigned)wdt);
+        if (k1 <= k0) break;
+        const DecProj& P = a.p[p];
+        const int nbw = max(0, min(2, wdt - 2 * cg));
+        const uint16_t* ap[MB];
+        const uint16_t* bp[2];
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(rb, 0, KS) + l * 8;
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
-            bp[cb] = abase + frag_index(min((c0 >> 4) + 2 * cg + cb, nblk - 1), 0, KS) + l * 8;
-        f32x4 acc[1][2];
-        const int kb = s * P.kchunk;
-        item_tile<1>(acc, ap, bp, kb, min(KS, kb + P.kchunk), red);
-        if (kq == 0) {
-            float* zdst = P.Zp + (size_t)s * kDecodeMaxT * P.zs;
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const int cgl = c0 + cg * 32 + cb * 16 + lr;
-                if (cgl < ncols) {
-                    const int sig = cgl / r8s, j = cgl - sig * r8s;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int row = 4 * (l >> 4) + i;
-                        if (row < nrows) zdst[(size_t)prow[row] * P.zs + sig * a.r8max + j] = sc * acc[0][cb][i];
-                    }
-                }
-            }
-        }
-        return;
-    }
-
-    // ---- base item: all rows x 64 columns over one K chunk
-    b -= a.shrink_slots;
-    int p = 0;
-    while (p + 1 < a.n_proj && b >= a.p[p + 1].gemm_base) ++p;
-    const DecProj& P = a.p[p];
-    const int local = b - P.gemm_base;
-    const int nt = local / P.ks, s = local - nt * P.ks;
-    const int T = a.T, N = P.N;
-    const int KS = P.K >> 5;
-    const int nrb = (T + 15) >> 4, ncb = N >> 4;
-    const uint16_t* ap[MB];
-    const uint16_t* bp[2];
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(min(rb, nrb - 1), 0, KS) + l * 8;
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb) bp[cb] = P.W + frag_index(min(nt * 4 + cg * 2 + cb, ncb - 1), 0, KS) + l * 8;
-    f32x4 acc[MB][2];
-    const int kb = s * P.kchunk;
-    item_tile<MB>(acc, ap, bp, kb, min(KS, kb + P.kchunk), red);
-    if (kq == 0) {
-        float* ydst = P.Yp + (size_t)s * kDecodeMaxT * N;
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb) {
-            const int col = nt * NT + cg * 32 + cb * 16 + lr;
-            if (col < N) {
-#pragma unroll
-                for (int rb = 0; rb < MB; ++rb)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int row = rb * 16 + 4 * (l >> 4) + i;
-                        if (row < T) ydst[(size_t)row * N + col] = acc[rb][cb][i];
-                    }
-            }
-        }
+            bp[cb] = dec_block(a, P, 4 * gl + min(2 * cg + cb, wdt - 1), KS) + l * 8;
+        const int slot = pp.gb + gl + b;
+        seg_tile<MB>(ap, bp, k0, k1, nbw, wdt, red, a.part + (size_t)min(slot, a.part_slots - 1) * kPartElems, a.T);
+        k0 = k1;
     }
 }
 
 hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s) {
-    const int grid = a.shrink_slots + a.gemm_items;
-    if (grid <= 0) return hipSuccess;
+    const int grid = a.main_grid;
+    if (grid <= 0 || grid > kDecMaxGrid) return hipErrorInvalidValue;
     switch (mb) {
         case 1: hipLaunchKernelGGL(dec_main_kernel<1>, dim3(grid), dim3(kThreads), 0, s, a); break;
         case 2: hipLaunchKernelGGL(dec_main_kernel<2>, dim3(grid), dim3(kThreads), 0, s, a); break;
@@ -169,71 +184,150 @@ hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s) {
     return hipGetLastError();
 }
 
-__device__ __forceinline__ void add8(float (&acc)[8], const float* p) {
-    const float4 a0 = *reinterpret_cast<const float4*>(p);
-    const float4 a1 = *reinterpret_cast<const float4*>(p + 4);
+// Workgroups of the main launch holding k-steps of group gl of projection pp:
+// the owners of its first and of its last k-step (every one between owns at
+// least one, since each workgroup's range spans at least one k-step).
+__device__ __forceinline__ void group_wgs(const ProjPos& pp, int gl, unsigned U, int G, int* b0, int* b1) {
+    const int wdt = min(4, pp.nb - 4 * gl);
+    const unsigned goff = pp.ub + 4u * gl * pp.KS;
+    *b0 = dec_wg_of(goff, U, G);
+    *b1 = dec_wg_of(goff + (unsigned)(pp.KS - 1) * wdt, U, G);
+}
+
+constexpr int kEpiSeg = 8;     // partial tiles of an output group loaded in the first pass
+constexpr int kEpiZSeg = 4;    // partial tiles of a Z group loaded in the first pass
+
+__device__ __forceinline__ void add8(float (&acc)[8], const float4& a0, const float4& a1) {
     acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
     acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
 }
 
-// one thread = 8 consecutive outputs of one token row.  Every load of the
-// thread is issued before the first use (split loops are unrolled to the
-// largest split count and predicated).
-__global__ __launch_bounds__(256) void dec_epi_kernel(DecArgs a) {
-    const int u = blockIdx.x * 256 + threadIdx.x;
-    if (u >= a.epi_units) return;
+__device__ __forceinline__ float4 ldf4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+
+// acc[c] += sc * sum_e z[e] * B^T[c][e] for the 8 ranks held in q[c]
+__device__ __forceinline__ void expand8(float (&acc)[8], const float (&z)[8], const u32x4 (&q)[8], float sc) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const uint32_t qq[4] = {q[c].x, q[c].y, q[c].z, q[c].w};
+        float sum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sum = fmaf(z[2 * e], __uint_as_float(qq[e] << 16), sum);
+            sum = fmaf(z[2 * e + 1], __uint_as_float(qq[e] & 0xffff0000u), sum);
+        }
+        acc[c] = fmaf(sc, sum, acc[c]);
+    }
+}
+
+// One workgroup per 64-column output tile of one projection, all tokens:
+// thread (t, g) computes the 8 outputs of token t in columns 8 g .. 8 g + 7
+// of the tile.  Tokens of one adapter share their B^T lines inside the
+// workgroup, so each tile reads each used adapter's B once.  After the
+// token's id, rank and group are known, every load of the base partials, of
+// the first 16 ranks' B^T and of their Z partials is issued before any sum,
+// so a thread waits for two round trips (more only for ranks above 16 or
+// groups split over many workgroups).  Sums run over workgroups in order.
+__global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
+    const int n_act = a.meta[0];
+    const int tile = blockIdx.x;
     int p = 0;
-    while (p + 1 < a.n_proj && u >= a.p[p + 1].epi_base) ++p;
+    while (p + 1 < a.n_proj && tile >= a.p[p + 1].tile_base) ++p;
     const DecProj& P = a.p[p];
-    const int per_row = P.N >> 3;
-    const int local = u - P.epi_base;
-    const int t = local / per_row, col = (local - t * per_row) * 8;
-    const int ks = P.ks;
+    const int n = tile - P.tile_base;
+    const int t = threadIdx.x >> 3;
+    const int col = n * 64 + (threadIdx.x & 7) * 8;
+    if (t >= a.T || col >= P.N) return;
     const int v = a.vid[t];
     const int r8s = a.tr8[t];
+    const int ai = a.tgrp[t];
+    const ProjPos pp = dec_pos(a, n_act, p);
+    const unsigned U = dec_units(a, n_act);
+    const int G = a.main_grid;
 
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const float* y = P.Yp + (size_t)t * P.N + col;
+    // base partials of this tile
+    int b0, b1;
+    group_wgs(pp, n, U, G, &b0, &b1);
+    const float* ysrc = a.part + (size_t)(pp.gb + n + b0) * kPartElems + t * 64 + (col - n * 64);
+    // loads are unconditional with the index clamped to the last slot, so the
+    // compiler issues them all before the first sum
+    float4 y[kEpiSeg][2];
 #pragma unroll
-    for (int s = 0; s < kMaxKSplit; ++s)
-        if (s < ks) add8(acc, y + (size_t)s * kDecodeMaxT * P.N);
+    for (int j = 0; j < kEpiSeg; ++j) {
+        const size_t o = (size_t)min(j, b1 - b0) * kPartElems;
+        y[j][0] = ldf4(ysrc + o);
+        y[j][1] = ldf4(ysrc + o + 4);
+    }
 
-    if (r8s > 0) {
-        int sig = 0;
-        while (sig + 1 < P.n_slices && col >= P.slice_col[sig + 1]) ++sig;
-        const float* z = P.Zp + (size_t)t * P.zs + sig * a.r8max;
-        const uint16_t* bb = a.pool + (size_t)v * a.slot_stride + P.b_off + (size_t)col * r8s;
-        // two 8-rank chunks per iteration, all their loads issued together
-        for (int j0 = 0; j0 < r8s; j0 += 16) {
-            const bool two = j0 + 8 < r8s;
-            u32x4 q[2][8];
-            float zz[2][8];
+    // LoRA operands of ranks 0..15: B^T rows and Z partials
+    const bool lora = r8s > 0 && ai >= 0;
+    int sig = 0;
+    while (sig + 1 < P.n_slices && col >= P.slice_col[sig + 1]) ++sig;
+    const uint16_t* bb = a.pool + (size_t)max(v, 0) * a.slot_stride + P.b_off + (size_t)col * r8s;
+    float sc = 0.f;
+    u32x4 q[2][8];
+    float4 zp[2][kEpiZSeg][2];
+    int z0[2] = {0, 0}, z1[2] = {-1, -1};
+    const float* zsrc[2] = {nullptr, nullptr};
+    if (lora) {
+        sc = a.scale[v];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int jj = two ? j0 + 8 * h : j0;
+        for (int h = 0; h < 2; ++h) {
+            if (8 * h < r8s) {
 #pragma unroll
-                for (int c = 0; c < 8; ++c) q[h][c] = ld16(bb + (size_t)c * r8s + jj);
+                for (int c = 0; c < 8; ++c) q[h][c] = ld16(bb + (size_t)c * r8s + 8 * h);
+                const int vc = sig * r8s + 8 * h;
+                const int vb = P.nWb + ai * P.nbA + (vc >> 4);
+                group_wgs(pp, vb >> 2, U, G, &z0[h], &z1[h]);
+                zsrc[h] = a.part + (size_t)(pp.gb + (vb >> 2) + z0[h]) * kPartElems + t * 64 + (vb & 3) * 16 + (vc & 15);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) zz[h][e] = 0.f;
-#pragma unroll
-                for (int s = 0; s < kMaxKSplit; ++s)
-                    if (s < ks) add8(zz[h], z + (size_t)s * kDecodeMaxT * P.zs + jj);
-            }
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                if (h == 1 && !two) break;
-#pragma unroll
-                for (int c = 0; c < 8; ++c) {
-                    const uint32_t qq[4] = {q[h][c].x, q[h][c].y, q[h][c].z, q[h][c].w};
-                    float sum = 0.f;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        sum = fmaf(zz[h][2 * e], __uint_as_float(qq[e] << 16), sum);
-                        sum = fmaf(zz[h][2 * e + 1], __uint_as_float(qq[e] & 0xffff0000u), sum);
-                    }
-                    acc[c] += sum;
+                for (int j = 0; j < kEpiZSeg; ++j) {
+                    const size_t o = (size_t)min(j, z1[h] - z0[h]) * kPartElems;
+                    zp[h][j][0] = ldf4(zsrc[h] + o);
+                    zp[h][j][1] = ldf4(zsrc[h] + o + 4);
                 }
             }
+        }
+    }
+
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < kEpiSeg; ++j)
+        if (b0 + j <= b1) add8(acc, y[j][0], y[j][1]);
+    for (int b = b0 + kEpiSeg; b <= b1; ++b) {
+        const float* src = ysrc + (size_t)(b - b0) * kPartElems;
+        add8(acc, ldf4(src), ldf4(src + 4));
+    }
+    if (lora) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            if (8 * h < r8s) {
+                float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < kEpiZSeg; ++j)
+                    if (z0[h] + j <= z1[h]) add8(z, zp[h][j][0], zp[h][j][1]);
+                for (int b = z0[h] + kEpiZSeg; b <= z1[h]; ++b) {
+                    const float* src = zsrc[h] + (size_t)(b - z0[h]) * kPartElems;
+                    add8(z, ldf4(src), ldf4(src + 4));
+                }
+                expand8(acc, z, q[h], sc);
+            }
+        }
+        // ranks 16 and up, 8 at a time
+        for (int j0 = 16; j0 < r8s; j0 += 8) {
+            u32x4 qr[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) qr[c] = ld16(bb + (size_t)c * r8s + j0);
+            const int vc = sig * r8s + j0;
+            const int vb = P.nWb + ai * P.nbA + (vc >> 4);
+            int c0, c1;
+            group_wgs(pp, vb >> 2, U, G, &c0, &c1);
+            const float* src = a.part + (size_t)(pp.gb + (vb >> 2)) * kPartElems + t * 64 + (vb & 3) * 16 + (vc & 15);
+            float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int b = c0; b <= c1; ++b) {
+                const float* s2 = src + (size_t)b * kPartElems;
+                add8(z, ldf4(s2), ldf4(s2 + 4));
+            }
+            expand8(acc, z, qr, sc);
         }
     }
     u32x4 o;
@@ -245,9 +339,9 @@ __global__ __launch_bounds__(256) void dec_epi_kernel(DecArgs a) {
 }
 
 hipError_t launch_dec_epi(const DecArgs& a, hipStream_t s) {
-    const int grid = (a.epi_units + 255) / 256;
-    if (grid <= 0) return hipSuccess;
-    hipLaunchKernelGGL(dec_epi_kernel, dim3(grid), dim3(256), 0, s, a);
+    if (a.tiles <= 0) return hipSuccess;
+    if (a.T > kDecodeMaxT || a.main_grid <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(dec_epi_kernel, dim3(a.tiles), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -71,6 +71,7 @@ struct PrepArgs {
     int oct_cap;
     int* vid;
     int* tr8;                 // [T] rank (padded to 8) of each token's adapter, 0 if none
+    int* tgrp;                // [T] group index of each token's adapter, -1 if none (optional)
     int* perm;
     int* gslot;
     int* gstart;
@@ -84,26 +85,27 @@ struct PrepArgs {
     int total_frags;
 };
 
-// ---- decode path (T <= kDecodeMaxT): split-K partials + epilogue -------------
+// ---- decode path (T <= kDecodeMaxT) ----------------------------------------
+// The main launch is one split-K GEMM of the packed activations against a
+// virtual column list per projection: the W_s column blocks (16 columns
+// each), then for every adapter the batch uses (in group order) the blocks of
+// its A^T_cat.  Work is counted in units of one 16-column block times one
+// 32-wide k-step; groups of 4 consecutive blocks are cut into k-ranges so
+// that every workgroup of the launch gets the same number of units.
 constexpr int kDecodeMaxT = BDLORA_DECODE_MAX_T;
-constexpr int kMaxKSplit = 8;
+constexpr int kDecMaxGrid = 1024;    // most workgroups of the main launch
+constexpr int kPartElems = 64 * 64;  // fp32 partial tile: 64 rows x 64 virtual columns
 
 struct DecProj {
     const uint16_t* Xp;       // packed activations (fragment layout)
     const uint16_t* W;        // packed base weight
     uint16_t* out;            // [T x N] bf16
-    float* Yp;                // [ks x kDecodeMaxT x N] fp32 partial base products
-    float* Zp;                // [ks x kDecodeMaxT x zs] fp32 partial scale * X A
-    int K, N, n_slices, zs;
+    int K, N, n_slices;
     int slice_col[kMaxSlices + 1];
     long long a_off, b_off;
-    int ks;                   // K splits of this projection
-    int kchunk;               // k-steps per split
-    int cchunks;              // shrink: 64-column chunks of A^T_cat (upper bound)
-    int tiles_n;              // 64-column tiles
-    int gemm_base;            // first base-GEMM item of this projection
-    int shrink_base;          // first shrink slot of this projection
-    int epi_base;             // first epilogue unit (8 outputs) of this projection
+    int nWb;                  // W column blocks (N / 16)
+    int nbA;                  // A^T_cat blocks per adapter (rows padded to 16)
+    int tile_base;            // first epilogue tile (64 output columns) of this projection
 };
 
 struct DecArgs {
@@ -112,18 +114,17 @@ struct DecArgs {
     int T;
     const uint16_t* pool;
     long long slot_stride;
-    int r8max;
     const float* scale;       // [max_slots]
-    const int* r8;            // [max_slots]
-    const int* vid;
+    const int* vid;           // [T] validated ids
     const int* tr8;           // [T] padded rank of each token's adapter (0: none)
-    const int* perm;
-    const int4* items;
-    const int* meta;          // [1] number of shrink items
-    int items_bound;
-    int shrink_slots;         // shrink slots over all projections
-    int gemm_items;
-    int epi_units;
+    const int* tgrp;          // [T] group (adapter in use) index of each token, -1: none
+    const int* gslot;         // [groups] slot of each adapter in use
+    const int* meta;          // [0] number of adapters in use
+    float* part;              // partial tiles: slot g + b for group g and workgroup b
+    int part_slots;
+    int main_grid;            // workgroups of the main launch
+    int tiles;                // epilogue tiles over all projections
+    int* err;                 // sticky error flag
 };
 
 // Host-side launchers (bdl_kernels.hip, bdl_prep.hip, bdl_decode.hip).

@@ -4,6 +4,7 @@
 // Plan outputs (integer work, compared bit-exactly with the host plan):
 //   vid[t]      validated id (-1: none or invalid; invalid ones raise *err)
 //   tr8[t]      rank (padded to 8) of token t's adapter, 0 if none
+//   tgrp[t]     (when asked for) group index of token t's adapter, -1 if none
 //   groups      (slot, start, count) per adapter in use, slots ascending
 //   perm        tokens group after group, ascending inside a group
 //   items       shrink work items {slot, first perm index, rows <= mts, r8}
@@ -116,6 +117,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     for (int s = s0; s < s1; ++s) {
         const int c = cnt[s];
         if (c > 0) {
+            ldl[s] = g_off;                   // group index of the slot (validation is done)
             a.gslot[g_off] = s;
             a.gstart[g_off] = tok_off;
             a.gcount[g_off] = c;
@@ -131,6 +133,11 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
         a.meta[1] = i_off;
     }
     __syncthreads();
+    if (a.tgrp)
+        for (int t = tid; t < a.T; t += 1024) {
+            const int v = in_lds ? vid_l[t] : a.vid[t];
+            a.tgrp[t] = v >= 0 ? ldl[v] : -1;
+        }
 
     // stable placement: perm[start(v) + #{t' < t : vid[t'] == v}] = t
     if (a.T <= 1024) {
