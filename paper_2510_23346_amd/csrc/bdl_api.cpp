@@ -518,6 +518,7 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->err = P->d_err;
     a->n_jobs = 0;
     a->total_frags = 0;
+    a->decode_plan = 0;
 }
 
 // Decode batches: prep (plan + activation packing), the split-K main launch
@@ -585,6 +586,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     fill_plan_args(P, ids, T, &pa, k);
     pa.tile_oct = nullptr;                        // the epilogue needs no octet lists
     pa.tgrp = P->d_tgrp;
+    pa.decode_plan = 1;
     int frags = 0;
     for (int q = 0; q < n; ++q) {
         bdl::PackJob& J = pa.jobs[q];

@@ -83,6 +83,7 @@ struct PrepArgs {
     PackJob jobs[kMaxProjs];
     int n_jobs;
     int total_frags;
+    int decode_plan;          // T <= 64: one wave writes vid, tr8, tgrp, gslot, meta only
 };
 
 // ---- decode path (T <= kDecodeMaxT) ----------------------------------------

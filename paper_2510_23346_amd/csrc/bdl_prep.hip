@@ -1,5 +1,6 @@
 // Prep launch of a forward call: workgroup 0 plans the batch, the others pack
-// the activations into the MFMA fragment layout.
+// the activations into the MFMA fragment layout.  Decode batches take a
+// one-wave plan that writes only what the decode launches read.
 //
 // Plan outputs (integer work, compared bit-exactly with the host plan):
 //   vid[t]      validated id (-1: none or invalid; invalid ones raise *err)
@@ -32,6 +33,86 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 
 __device__ __forceinline__ int wave_total(int incl) { return __builtin_amdgcn_readlane(incl, 63); }
 
+// minimum / bitwise or over the 64 lanes of a wave, as a uniform value
+__device__ __forceinline__ int wave_min(int v) {
+    constexpr int kMax = 0x7fffffff;
+    v = min(v, __builtin_amdgcn_update_dpp(kMax, v, 0x111, 0xf, 0xf, false));   // row_shr:1
+    v = min(v, __builtin_amdgcn_update_dpp(kMax, v, 0x112, 0xf, 0xf, false));   // row_shr:2
+    v = min(v, __builtin_amdgcn_update_dpp(kMax, v, 0x114, 0xf, 0xf, false));   // row_shr:4
+    v = min(v, __builtin_amdgcn_update_dpp(kMax, v, 0x118, 0xf, 0xf, false));   // row_shr:8
+    v = min(v, __builtin_amdgcn_update_dpp(kMax, v, 0x142, 0xa, 0xf, false));   // row_bcast:15
+    v = min(v, __builtin_amdgcn_update_dpp(kMax, v, 0x143, 0xc, 0xf, false));   // row_bcast:31
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
+__device__ __forceinline__ unsigned wave_or(unsigned v) {
+    v |= (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);
+    v |= (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);
+    v |= (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);
+    v |= (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);
+    v |= (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);
+    v |= (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);
+    return (unsigned)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Plan of a decode batch (T <= 64) by one wave: validated ids, ranks, the
+// adapters in use in ascending slot order (groups) and each token's group.
+// Lane t holds token t.  Pools of at most 64 slots keep the slot tables in
+// lanes (one load round trip) and find the groups from the bit mask of slots
+// in use; larger pools look the tables up per token and take the smallest
+// remaining slot per pass.
+__device__ void decode_plan(const PrepArgs& a) {
+    const int l = threadIdx.x & 63;
+    const bool in = l < a.T;
+    const bool small = a.max_slots <= 64;
+    const int lt = small && l < a.max_slots ? a.loaded[l] : 0;
+    const int rt = small && l < a.max_slots ? a.r8[l] : 0;
+    const int id = in ? a.ids[l] : -1;
+    const bool in_range = id >= 0 && id < a.max_slots;
+    int ld, r8v;
+    if (small) {
+        ld = __shfl(lt, in_range ? id : 0);
+        r8v = __shfl(rt, in_range ? id : 0);
+        if (!in_range) ld = r8v = 0;
+    } else {
+        ld = in_range ? a.loaded[id] : 0;
+        r8v = in_range ? a.r8[id] : 0;
+    }
+    const bool ok = in_range && ld != 0;
+    const int v = ok ? id : -1;
+    const bool bad = __ballot(in && !ok && id != -1) != 0ull;
+    int g = 0, mine = -1;
+    if (small) {
+        const unsigned long long bit = ok ? 1ull << v : 0ull;
+        const unsigned long long used =
+            (unsigned long long)wave_or((unsigned)bit) | ((unsigned long long)wave_or((unsigned)(bit >> 32)) << 32);
+        const unsigned long long below = (1ull << l) - 1ull;
+        if ((used >> l) & 1ull) a.gslot[__popcll(used & below)] = l;
+        if (ok) mine = __popcll(used & (bit - 1ull));
+        g = __popcll(used);
+    } else {
+        unsigned long long rem = __ballot(ok);
+        while (rem) {
+            const int m = wave_min(((rem >> l) & 1ull) ? v : 0x7fffffff);
+            const bool eq = ok && v == m;
+            if (eq) mine = g;
+            if (l == 0) a.gslot[g] = m;
+            ++g;
+            rem &= ~__ballot(eq);
+        }
+    }
+    if (in) {
+        a.vid[l] = v;
+        a.tr8[l] = ok ? r8v : 0;
+        if (a.tgrp) a.tgrp[l] = mine;
+    }
+    if (l == 0) {
+        a.meta[0] = g;
+        a.meta[1] = 0;
+        if (bad) atomicOr(a.err, 1);
+    }
+}
+
 // activations -> fragment layout (all workgroups but 0)
 __device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
     const int l = threadIdx.x & 63;
@@ -52,6 +133,10 @@ __device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
 __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     if (blockIdx.x > 0) {
         pack_activations(a, blockIdx.x - 1, gridDim.x - 1);
+        return;
+    }
+    if (a.decode_plan) {
+        if (threadIdx.x < 64) decode_plan(a);
         return;
     }
     extern __shared__ int tabs[];             // cnt | r8 | loaded | 15 tile bitmaps
@@ -208,7 +293,7 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
     int pack_blocks = (a.total_frags + 15) / 16;
     if (pack_blocks > 1024) pack_blocks = 1024;
     const int nwords = (a.max_slots + 31) >> 5;
-    const size_t lds = 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
+    const size_t lds = a.decode_plan ? 0 : 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
     hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), lds, s, a);
     return hipGetLastError();
 }

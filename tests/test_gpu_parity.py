@@ -202,6 +202,35 @@ def test_invalid_ids_are_base_only_and_flagged(torch_cuda):
     pool.close()
 
 
+@pytest.mark.parametrize("n_slots", [64, 150])
+def test_decode_plan_pool_sizes(torch_cuda, n_slots):
+    # decode batches plan in one wave: pools of up to 64 slots keep the slot
+    # tables in lanes (slot 63 is the mask's top bit), larger pools take the
+    # per-pass minimum; unloaded and out-of-range ids must read as -1
+    torch = torch_cuda
+    T = 60
+    rng = np.random.default_rng(n_slots)
+    loaded = sorted(set(rng.choice(n_slots, size=min(40, n_slots - 1), replace=False).tolist()) | {0, n_slots - 1})
+    ids = rng.choice(loaded, size=T)
+    ids[:4] = [n_slots - 1, 0, -1, n_slots - 1]
+    ids[7] = n_slots + 5                       # out of range
+    unloaded = [s for s in range(n_slots) if s not in loaded][0]
+    ids[9] = unloaded
+    ranks = [8 if s % 3 else 16 for s in range(n_slots)]
+    spec = wl.custom_workload(f"pool{n_slots}", wl.tiny_projs(), T, ranks, ids=ids, seed=n_slots)
+    layer = wl.draw_layer(spec, slots=loaded)
+    pool = make_pool(spec)
+    load_adapters(pool, spec, loaded, cache=layer.adapters)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    assert pool.device_error() == 1
+    vid, _ = oplan.validate(ids, pool.loaded)
+    layer.ids = vid
+    refs = bdlora.layer_forward(layer)
+    for p in range(len(spec.projs)):
+        _check(ys[p], refs[p], what=f"pool {n_slots} proj {spec.projs[p].name}")
+    pool.close()
+
+
 def _fragment_layout(W):
     """Reference of the packed weight layout: 16-row blocks x 32-wide k-steps,
     element [(rb*KS + ks)*512 + lane*8 + i] = W[16 rb + lane%16][32 ks + 8 (lane//16) + i]."""
