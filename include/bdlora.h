@@ -70,6 +70,9 @@ extern "C" {
  * the prefill sequence (plan and packing, shrink, base product with the
  * expand fused in). */
 #define BDLORA_DECODE_MAX_T 64
+/* Activation between the two projections of bdlora_forward_mlp. */
+#define BDLORA_ACT_NONE     0   /* H = first projection's output (Alg. 1)  */
+#define BDLORA_ACT_SILU_MUL 1   /* H = silu(gate) * up (gated MLP)         */
 
 typedef struct bdlora_pool* bdlora_pool_t;
 
@@ -144,6 +147,29 @@ int bdlora_forward_shard(bdlora_pool_t pool, int32_t proj, const void* X, const 
 int bdlora_forward_layer(bdlora_pool_t pool, int32_t n, const int32_t* projs,
                          const void* const* X, const void* const* W, void* const* out,
                          const int32_t* ids, int32_t T, void* stream);
+
+/* One device's share of a BD-LoRA MLP (Alg. 1, App. B): the first
+ * (column-parallel) projection(s), the intermediate H, then the
+ * row-parallel projection `down`, whose output is the device's partial that
+ * the base model's all-reduce would sum.  Alg. 1 chains the projections
+ * directly (act = BDLORA_ACT_NONE: first[0] is one column projection and
+ * H = its output); the gated MLP of the Llama models the paper serves
+ * (Sec. 4) takes act = BDLORA_ACT_SILU_MUL with first[0] = gate and
+ * first[1] = up, two column projections of equal width, and
+ * H = silu(gate) * up.  Every projection adds its own BD-LoRA term per token
+ * exactly as bdlora_forward_shard does.  H [T x d_in of down] is held in the
+ * pool in bf16 (round to nearest even) and never leaves it; the first
+ * projections' width must equal down's d_in.
+ * X: device [T x d_in] bf16, shared by the first projections; W_first:
+ * host array of 1 or 2 device pointers to packed weights; W_down: packed
+ * weight of down; out: device [T x d_out of down]; ids: device int32 [T].
+ * T: 0..max_tokens.  Enqueued on `stream`; uses the pool's workspace, so
+ * calls on one pool must share one stream.
+ * Errors: INVALID_ARG (bad act, indices, kinds or null pointers), SHAPE
+ * (widths do not chain), HIP. */
+int bdlora_forward_mlp(bdlora_pool_t pool, int32_t act, const int32_t* first, int32_t down,
+                       const void* X, const void* const* W_first, const void* W_down, void* out,
+                       const int32_t* ids, int32_t T, void* stream);
 
 /* Host-side plan of a batch (the integer bookkeeping of heterogeneous
  * batching, Sec. 2 on S-LoRA), a pure host function: validates host ids

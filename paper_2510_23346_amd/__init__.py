@@ -18,11 +18,13 @@ import numpy as np
 __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
     "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T",
+    "ACT_NONE", "ACT_SILU_MUL",
 ]
 
 COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
+ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libbdlora.so")
 _LIB = None
@@ -50,6 +52,7 @@ _SIGS = {
     "bdlora_unload_adapter": (_I, [_P, _I]),
     "bdlora_forward_shard": (_I, [_P, _I, _P, _P, _P, _I, _P, _P]),
     "bdlora_forward_layer": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _I, _P]),
+    "bdlora_forward_mlp": (_I, [_P, _I, _IP, _I, _P, _c.POINTER(_P), _P, _P, _P, _I, _P]),
     "bdlora_build_plan": (_I, [_IP, _I, _IP, _I, _IP, _IP, _IP, _IP, _IP, _IP]),
     "bdlora_plan_device": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P]),
     "bdlora_get_device_error": (_I, [_P, _P, _IP]),
@@ -290,6 +293,21 @@ class Pool:
         ws = (_c.c_void_p * n)(*[_ptr(w) for w in Ws])
         os_ = (_c.c_void_p * n)(*[_ptr(o) for o in outs])
         _check(lib().bdlora_forward_layer(self._h, n, pr, xs, ws, os_, _ptr(ids), T, _stream_handle(stream)))
+
+    def forward_mlp(self, act: int, first: Sequence[int], down: int, X, W_first, W_down, out, ids,
+                    T: Optional[int] = None, stream=None):
+        """One device's share of a BD-LoRA MLP (Alg. 1): ``first`` = [proj]
+        (act ACT_NONE) or [gate, up] (ACT_SILU_MUL), then the row projection
+        ``down``; ``out`` is down's partial output."""
+        T = int(ids.shape[0]) if T is None else int(T)
+        n = len(first)
+        for i, p in enumerate(first):
+            self._check_io(p, X, W_first[i], None, T)
+        self._check_io(down, None, W_down, out, T)
+        pr = (_c.c_int32 * max(n, 1))(*[int(p) for p in first])
+        ws = (_c.c_void_p * max(n, 1))(*[_ptr(w) for w in W_first])
+        _check(lib().bdlora_forward_mlp(self._h, int(act), pr, int(down), _ptr(X), ws, _ptr(W_down), _ptr(out),
+                                        _ptr(ids), T, _stream_handle(stream)))
 
     def plan_device(self, ids, vid, gslot, gstart, gcount, perm, n_groups, T: Optional[int] = None, stream=None):
         T = int(ids.shape[0]) if T is None else int(T)

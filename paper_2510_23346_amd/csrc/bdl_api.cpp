@@ -48,6 +48,7 @@ struct Layout {
     long long z_elems[bdl::kMaxProjs];
     long long xp_elems[bdl::kMaxProjs];
     long long part_slots = 0;          // decode partial tiles
+    long long mlp_elems = 0;           // prefill MLP: gate and up outputs, fp32
 };
 
 // Validates the pool arguments and computes the memory layout.
@@ -119,6 +120,11 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
     }
     L->part_slots = groups + bdl::kDecMaxGrid;
     ws += L->part_slots * bdl::kPartElems * 4 + (long long)max_tokens * 4;
+    int max_n = 0;                                  // widest single-slice column projection
+    for (int p = 0; p < n_projs; ++p)
+        if (L->proj[p].kind == BDLORA_COLUMN && L->proj[p].S == 1) max_n = std::max(max_n, L->proj[p].N);
+    L->mlp_elems = 2LL * max_tokens * max_n;
+    ws += L->mlp_elems * 4;
     ws += max_slots * 12LL;                                       // slot tables
     L->ws_bytes = ws;
     return BDLORA_OK;
@@ -160,6 +166,7 @@ struct bdlora_pool {
     uint16_t* d_Z[bdl::kMaxProjs] = {};
     int* d_tgrp = nullptr;
     float* d_part = nullptr;
+    float* d_mlp = nullptr;
     int n_cu = 0;
     uint16_t* d_Xp[bdl::kMaxProjs] = {};
     uint16_t* d_stage = nullptr;
@@ -196,6 +203,7 @@ void free_pool(bdlora_pool* P) {
     for (auto z : P->d_Z) f(z);
     f(P->d_tgrp);
     f(P->d_part);
+    f(P->d_mlp);
     for (auto x : P->d_Xp) f(x);
     f(P->d_stage);
     for (auto e : P->prof_ev) (void)hipEventDestroy(e);
@@ -325,6 +333,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_tr8, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_tgrp, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_part, L.part_slots * bdl::kPartElems, &tot));
+    BDL_TRY(dev_alloc(&P->d_mlp, L.mlp_elems, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
@@ -523,8 +532,19 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
 
 // Decode batches: prep (plan + activation packing), the split-K main launch
 // over W_s and the used adapters' A^T, the epilogue.
+// How a call uses the decode launches: the MLP chains two calls, the second
+// reusing the first's plan and reading the intermediate the first's epilogue
+// packed.
+struct DecMode {
+    bool prep = true;              // run the prep launch (plan + activation packing)
+    int mlp_act = -1;              // >= 0: the epilogue writes the MLP intermediate
+    uint16_t* h_dst = nullptr;     // where (fragment layout of the second projection's input)
+    int h_KS = 0;
+};
+
 static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
-                          const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s) {
+                          const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s,
+                          const DecMode& mode = DecMode()) {
     const Layout& L = P->L;
     int n_loaded = 0;
     for (int v : P->h_loaded) n_loaded += v != 0;
@@ -576,6 +596,9 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     da.main_grid = grid;
     da.tiles = tiles;
     da.err = P->d_err;
+    da.mlp_act = mode.mlp_act;
+    da.h_dst = mode.h_dst;
+    da.h_KS = mode.h_KS;
 
     Shapes k;
     k.smb = 1;
@@ -587,9 +610,17 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     pa.tile_oct = nullptr;                        // the epilogue needs no octet lists
     pa.tgrp = P->d_tgrp;
     pa.decode_plan = 1;
-    int frags = 0;
-    for (int q = 0; q < n; ++q) {
-        bdl::PackJob& J = pa.jobs[q];
+    // projections given the same X (gate and up) share one packed copy
+    int frags = 0, jobs = 0;
+    for (int q = 0; q < n && mode.prep; ++q) {
+        int same = -1;
+        for (int r = 0; r < q && same < 0; ++r)
+            if (X[r] == X[q] && da.p[r].K == da.p[q].K) same = r;
+        if (same >= 0) {
+            da.p[q].Xp = da.p[same].Xp;
+            continue;
+        }
+        bdl::PackJob& J = pa.jobs[jobs++];
         J.src = (const uint16_t*)X[q];
         J.dst = P->d_Xp[projs[q]];
         J.rows = T;
@@ -597,7 +628,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         J.frag_base = frags;
         frags += ((T + 15) / 16) * (J.K / 32);
     }
-    pa.n_jobs = n;
+    pa.n_jobs = jobs;
     pa.total_frags = frags;
 
     hipEvent_t* ev = nullptr;
@@ -607,7 +638,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         --P->prof_left;
     }
     if (ev) BDL_HIP(hipEventRecord(ev[0], s));
-    BDL_HIP(bdl::launch_prep(pa, s));
+    if (mode.prep) BDL_HIP(bdl::launch_prep(pa, s));
     if (ev) BDL_HIP(hipEventRecord(ev[1], s));
     if (ev) BDL_HIP(hipEventRecord(ev[2], s));
     BDL_HIP(bdl::launch_dec_main(da, k.gmb, s));
@@ -618,30 +649,18 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     return BDLORA_OK;
 }
 
-int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
-                         const void* const* W, void* const* out, const int32_t* ids, int32_t T, void* stream) {
-    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+static bool use_decode(const Layout& L, int T) {
+    // the decode launches address their partial tiles with 32-bit byte offsets
+    return T <= bdl::kDecodeMaxT && L.part_slots * bdl::kPartElems * 4 < (1LL << 31);
+}
+
+// Batches above the decode size: prep (plan + packing; with pack = false the
+// packed activations are already in place), shrink, base product with the
+// expand fused in.
+static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
+                           const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s,
+                           bool pack = true, float* const* out_f32 = nullptr) {
     const Layout& L = P->L;
-    if (n < 1 || n > BDLORA_MAX_PROJS) return fail(BDLORA_ERR_INVALID_ARG, "n must be 1..8");
-    if (!projs || !X || !W || !out) return fail(BDLORA_ERR_INVALID_ARG, "null pointer array");
-    if (T < 0 || T > L.max_tokens) return fail(BDLORA_ERR_SHAPE, "T outside 0..max_tokens");
-    bool seen[bdl::kMaxProjs] = {};
-    for (int i = 0; i < n; ++i) {
-        if (projs[i] < 0 || projs[i] >= L.n_projs) return fail(BDLORA_ERR_INVALID_ARG, "projection index out of range");
-        if (seen[projs[i]]) return fail(BDLORA_ERR_INVALID_ARG, "projection listed twice");
-        seen[projs[i]] = true;
-        if (T > 0 && (!X[i] || !W[i] || !out[i])) return fail(BDLORA_ERR_INVALID_ARG, "null tensor pointer");
-        if (T > 0 && (!aligned16(X[i]) || !aligned16(W[i]) || !aligned16(out[i])))
-            return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
-    }
-    if (T == 0) return BDLORA_OK;
-    if (!ids) return fail(BDLORA_ERR_INVALID_ARG, "null ids");
-    DeviceGuard guard(P->device);
-    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
-    hipStream_t s = (hipStream_t)stream;
-
-    if (T <= bdl::kDecodeMaxT) return forward_decode(P, n, projs, X, W, out, ids, T, s);
-
     long long col_blocks = 0;
     for (int i = 0; i < n; ++i) col_blocks += L.proj[projs[i]].N / 16;
     const Shapes k = pick_shapes(T, col_blocks);
@@ -668,6 +687,7 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
         pl.Xp = P->d_Xp[projs[i]];
         pl.W = (const uint16_t*)W[i];
         pl.out = (uint16_t*)out[i];
+        pl.out_f32 = out_f32 ? out_f32[i] : nullptr;
         pl.Z = P->d_Z[projs[i]];
         pl.zplane = (long long)L.max_tokens * pi.zs;
         pl.K = pi.K;
@@ -703,9 +723,9 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
 
     bdl::PrepArgs pa;
     fill_plan_args(P, ids, T, &pa, k);
-    int frags = 0;
-    for (int q = 0; q < n; ++q) {
-        bdl::PackJob& J = pa.jobs[q];
+    int frags = 0, jobs = 0;
+    for (int q = 0; q < n && pack; ++q) {
+        bdl::PackJob& J = pa.jobs[jobs++];
         J.src = fa.p[q].X;
         J.dst = P->d_Xp[projs[order[q]]];
         J.rows = T;
@@ -713,7 +733,7 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
         J.frag_base = frags;
         frags += ((T + 15) / 16) * (J.K / 32);
     }
-    pa.n_jobs = n;
+    pa.n_jobs = jobs;
     pa.total_frags = frags;
 
     hipEvent_t* ev = nullptr;
@@ -734,6 +754,32 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
     return BDLORA_OK;
 }
 
+int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
+                         const void* const* W, void* const* out, const int32_t* ids, int32_t T, void* stream) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    const Layout& L = P->L;
+    if (n < 1 || n > BDLORA_MAX_PROJS) return fail(BDLORA_ERR_INVALID_ARG, "n must be 1..8");
+    if (!projs || !X || !W || !out) return fail(BDLORA_ERR_INVALID_ARG, "null pointer array");
+    if (T < 0 || T > L.max_tokens) return fail(BDLORA_ERR_SHAPE, "T outside 0..max_tokens");
+    bool seen[bdl::kMaxProjs] = {};
+    for (int i = 0; i < n; ++i) {
+        if (projs[i] < 0 || projs[i] >= L.n_projs) return fail(BDLORA_ERR_INVALID_ARG, "projection index out of range");
+        if (seen[projs[i]]) return fail(BDLORA_ERR_INVALID_ARG, "projection listed twice");
+        seen[projs[i]] = true;
+        if (T > 0 && (!X[i] || !W[i] || !out[i])) return fail(BDLORA_ERR_INVALID_ARG, "null tensor pointer");
+        if (T > 0 && (!aligned16(X[i]) || !aligned16(W[i]) || !aligned16(out[i])))
+            return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
+    }
+    if (T == 0) return BDLORA_OK;
+    if (!ids) return fail(BDLORA_ERR_INVALID_ARG, "null ids");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+
+    if (use_decode(L, T)) return forward_decode(P, n, projs, X, W, out, ids, T, s);
+    return forward_prefill(P, n, projs, X, W, out, ids, T, s);
+}
+
 int bdlora_forward_shard(bdlora_pool_t P, int32_t proj, const void* X, const void* W, const int32_t* ids, int32_t T,
                          void* out, void* stream) {
     const void* xs[1] = {X};
@@ -741,6 +787,64 @@ int bdlora_forward_shard(bdlora_pool_t P, int32_t proj, const void* X, const voi
     void* os[1] = {out};
     int32_t pr[1] = {proj};
     return bdlora_forward_layer(P, 1, pr, xs, ws, os, ids, T, stream);
+}
+
+int bdlora_forward_mlp(bdlora_pool_t P, int32_t act, const int32_t* first, int32_t down, const void* X,
+                       const void* const* W_first, const void* W_down, void* out, const int32_t* ids, int32_t T,
+                       void* stream) {
+    if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
+    const Layout& L = P->L;
+    if (act != BDLORA_ACT_NONE && act != BDLORA_ACT_SILU_MUL) return fail(BDLORA_ERR_INVALID_ARG, "unknown act");
+    const int nf = act == BDLORA_ACT_SILU_MUL ? 2 : 1;
+    if (!first || !W_first) return fail(BDLORA_ERR_INVALID_ARG, "null pointer array");
+    if (T < 0 || T > L.max_tokens) return fail(BDLORA_ERR_SHAPE, "T outside 0..max_tokens");
+    if (down < 0 || down >= L.n_projs) return fail(BDLORA_ERR_INVALID_ARG, "projection index out of range");
+    for (int j = 0; j < nf; ++j) {
+        if (first[j] < 0 || first[j] >= L.n_projs) return fail(BDLORA_ERR_INVALID_ARG, "projection index out of range");
+        if (first[j] == down || (j == 1 && first[1] == first[0]))
+            return fail(BDLORA_ERR_INVALID_ARG, "projection listed twice");
+        if (L.proj[first[j]].kind != BDLORA_COLUMN || L.proj[first[j]].S != 1)
+            return fail(BDLORA_ERR_INVALID_ARG, "first projections must be single-slice column projections");
+        if (L.proj[first[j]].N != L.proj[down].K || L.proj[first[j]].K != L.proj[first[0]].K)
+            return fail(BDLORA_ERR_SHAPE, "first projections' width must equal down's d_in");
+    }
+    if (L.proj[down].kind != BDLORA_ROW) return fail(BDLORA_ERR_INVALID_ARG, "down must be a row projection");
+    if (T == 0) return BDLORA_OK;
+    if (!ids || !X || !W_down || !out) return fail(BDLORA_ERR_INVALID_ARG, "null tensor pointer");
+    for (int j = 0; j < nf; ++j)
+        if (!W_first[j] || !aligned16(W_first[j])) return fail(BDLORA_ERR_INVALID_ARG, "W must be 16-byte aligned");
+    if (!aligned16(X) || !aligned16(W_down) || !aligned16(out))
+        return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+    const int Ni = L.proj[down].K;                 // intermediate width d_I / N
+    uint16_t* h = P->d_Xp[down];                   // H, packed as down's input
+    const void* xs[2] = {X, X};
+    const int32_t dn[1] = {down};
+    const void* wd[1] = {W_down};
+    void* od[1] = {out};
+    if (use_decode(L, T)) {
+        // first projections: their epilogue writes H packed; down reuses the plan
+        DecMode m1;
+        m1.mlp_act = act;
+        m1.h_dst = h;
+        m1.h_KS = Ni / 32;
+        void* none[2] = {nullptr, nullptr};
+        int rc = forward_decode(P, nf, first, xs, W_first, none, ids, T, s, m1);
+        if (rc) return rc;
+        DecMode m2;
+        m2.prep = false;
+        return forward_decode(P, 1, dn, xs, wd, od, ids, T, s, m2);
+    }
+    // prefill: gate/up outputs in fp32 to the pool's workspace, H packed,
+    // then down
+    float* g_u[2] = {P->d_mlp, P->d_mlp + (size_t)T * Ni};
+    void* none[2] = {nullptr, nullptr};
+    int rc = forward_prefill(P, nf, first, xs, W_first, none, ids, T, s, true, g_u);
+    if (rc) return rc;
+    BDL_HIP(bdl::launch_mlp_pack(g_u[0], act == BDLORA_ACT_SILU_MUL ? g_u[1] : nullptr, h, T, Ni, s));
+    return forward_prefill(P, 1, dn, xs, wd, od, ids, T, s, false);
 }
 
 int bdlora_plan_device(bdlora_pool_t P, const int32_t* ids, int32_t T, int32_t* vid, int32_t* gslot, int32_t* gstart,

@@ -219,24 +219,18 @@ __device__ __forceinline__ void expand8(float (&acc)[8], const float (&z)[8], co
     }
 }
 
-// One workgroup per 64-column output tile of one projection, all tokens:
-// thread (t, g) computes the 8 outputs of token t in columns 8 g .. 8 g + 7
-// of the tile.  Tokens of one adapter share their B^T lines inside the
+// The 8 outputs of token t in columns col .. col + 7 of output tile n of
+// projection p: the tile's partials added in workgroup order, plus scale *
+// sum_j Z[t, j] B^T[col + c, j] with Z from the partials of the token's own
+// adapter, all in fp32.  Tokens of one adapter share their B^T lines inside a
 // workgroup, so each tile reads each used adapter's B once.  After the
 // token's id, rank and group are known, every load of the base partials, of
 // the first 16 ranks' B^T and of their Z partials is issued before any sum,
 // so a thread waits for two round trips (more only for ranks above 16 or
-// groups split over many workgroups).  Sums run over workgroups in order.
-__global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
-    const int n_act = a.meta[0];
-    const int tile = blockIdx.x;
-    int p = 0;
-    while (p + 1 < a.n_proj && tile >= a.p[p + 1].tile_base) ++p;
+// groups split over many workgroups).
+__device__ __forceinline__ void epi_acc(const DecArgs& a, int n_act, int p, int n, int t, int col,
+                                        float (&acc)[8]) {
     const DecProj& P = a.p[p];
-    const int n = tile - P.tile_base;
-    const int t = threadIdx.x >> 3;
-    const int col = n * 64 + (threadIdx.x & 7) * 8;
-    if (t >= a.T || col >= P.N) return;
     const int v = a.vid[t];
     const int r8s = a.tr8[t];
     const int ai = a.tgrp[t];
@@ -289,7 +283,8 @@ __global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
         }
     }
 
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = 0.f;
 #pragma unroll
     for (int j = 0; j < kEpiSeg; ++j)
         if (b0 + j <= b1) add8(acc, y[j][0], y[j][1]);
@@ -330,18 +325,57 @@ __global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
             expand8(acc, z, qr, sc);
         }
     }
+}
+
+__device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
     u32x4 o;
-    o.x = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
-    o.y = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
-    o.z = (uint32_t)f2bf(acc[4]) | ((uint32_t)f2bf(acc[5]) << 16);
-    o.w = (uint32_t)f2bf(acc[6]) | ((uint32_t)f2bf(acc[7]) << 16);
-    *reinterpret_cast<u32x4*>(P.out + (size_t)t * P.N + col) = o;
+    o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+    o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    o.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+    o.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+    return o;
+}
+
+// One workgroup per 64-column output tile, all tokens: thread (t, g) computes
+// the 8 outputs of token t in columns 8 g .. 8 g + 7 of the tile.  In MLP mode
+// the tiles are those of projection 0 only, and the outputs become the MLP
+// intermediate H = out_0 (act none) or silu(out_0) * out_1 (act silu_mul,
+// projection 1 being up), stored in bf16 in the fragment layout the second
+// projection reads (rows = tokens, k = these columns).
+__global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
+    const int n_act = a.meta[0];
+    const int tile = blockIdx.x;
+    int p = 0;
+    while (p + 1 < a.n_proj && tile >= a.p[p + 1].tile_base) ++p;
+    const DecProj& P = a.p[p];
+    const int n = tile - P.tile_base;
+    const int t = threadIdx.x >> 3;
+    const int col = n * 64 + (threadIdx.x & 7) * 8;
+    if (t >= a.T || col >= P.N) return;
+    float acc[8];
+    epi_acc(a, n_act, p, n, t, col, acc);
+    if (a.mlp_act < 0) {
+        *reinterpret_cast<u32x4*>(P.out + (size_t)t * P.N + col) = pack_bf16x8(acc);
+        return;
+    }
+    if (a.mlp_act == BDLORA_ACT_SILU_MUL) {
+        float up[8];
+        epi_acc(a, n_act, 1, n, t, col, up);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[c] = acc[c] / (1.f + __expf(-acc[c])) * up[c];
+    }
+    // H[t][col .. col + 7] -> fragment (t / 16, col / 32), lane (t % 16) + 16 ((col % 32) / 8)
+    const size_t f = ((size_t)(t >> 4) * a.h_KS + (col >> 5)) * kFrag + ((t & 15) + 16 * ((col & 31) >> 3)) * 8;
+    *reinterpret_cast<u32x4*>(a.h_dst + f) = pack_bf16x8(acc);
 }
 
 hipError_t launch_dec_epi(const DecArgs& a, hipStream_t s) {
-    if (a.tiles <= 0) return hipSuccess;
+    const int grid = a.mlp_act < 0 ? a.tiles : (a.p[0].N + 63) / 64;
+    if (grid <= 0) return hipSuccess;
     if (a.T > kDecodeMaxT || a.main_grid <= 0) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(dec_epi_kernel, dim3(a.tiles), dim3(kThreads), 0, s, a);
+    if (a.mlp_act >= 0 && (!a.h_dst || (a.mlp_act == BDLORA_ACT_SILU_MUL && (a.n_proj != 2 || a.p[1].N != a.p[0].N))))
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(dec_epi_kernel, dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -207,14 +207,19 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
         code = codes[4 * e + (l >> 4)];
     }
 
-    // ---- reduce the 8 waves and store bf16 (two columns per thread)
+    // ---- reduce the 8 waves and store bf16 (or fp32), two columns per thread
     reduce_waves<MB, NB>(acc, red);
     for (int idx = threadIdx.x; idx < MT * NT / 2; idx += kThreads) {
         const int r = idx / (NT / 2), c = (idx - r * (NT / 2)) * 2;
         const int row = m0 + r, col = n0 + c;
         if (row < T && col < N) {
-            const uint32_t v = (uint32_t)f2bf(red[r * LD + c]) | ((uint32_t)f2bf(red[r * LD + c + 1]) << 16);
-            *reinterpret_cast<uint32_t*>(P.out + (size_t)row * N + col) = v;
+            if (P.out_f32) {
+                *reinterpret_cast<float2*>(P.out_f32 + (size_t)row * N + col) =
+                    float2{red[r * LD + c], red[r * LD + c + 1]};
+            } else {
+                const uint32_t v = (uint32_t)f2bf(red[r * LD + c]) | ((uint32_t)f2bf(red[r * LD + c + 1]) << 16);
+                *reinterpret_cast<uint32_t*>(P.out + (size_t)row * N + col) = v;
+            }
         }
     }
 }

@@ -20,6 +20,7 @@ struct ProjLaunch {
     const uint16_t* Xp;       // packed activations, fragment layout, rows padded to 16
     const uint16_t* W;        // packed base weight, fragment layout ([N x K] nn.Linear rows)
     uint16_t* out;            // [T x N] bf16
+    float* out_f32;           // when set: the output in fp32 [T x N] instead of out
     uint16_t* Z;              // [2 x max_tokens x zs] workspace: scale * X A per slice as a
                               // bf16 pair (hi plane, then lo plane at Z + zplane)
     long long zplane;         // elements between the hi and the lo plane
@@ -126,6 +127,9 @@ struct DecArgs {
     int main_grid;            // workgroups of the main launch
     int tiles;                // epilogue tiles over all projections
     int* err;                 // sticky error flag
+    int mlp_act;              // -1: write out; else write the MLP intermediate H (BDLORA_ACT_*)
+    uint16_t* h_dst;          // H in the fragment layout of the second projection's input
+    int h_KS;                 // k-steps of that layout (second projection's d_in / 32)
 };
 
 // Host-side launchers (bdl_kernels.hip, bdl_prep.hip, bdl_decode.hip).
@@ -137,5 +141,6 @@ hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K,
                                int n_slices, const int* slice_out, int rank, int r8, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s);
+hipError_t launch_mlp_pack(const float* G, const float* U, uint16_t* dst, int T, int N, hipStream_t s);
 
 }  // namespace bdl

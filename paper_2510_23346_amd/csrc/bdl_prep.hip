@@ -298,4 +298,43 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// MLP intermediate of a batch above the decode size: H = G (U null) or
+// silu(G) * U from the first projections' fp32 outputs [T x N], rounded to
+// bf16 and stored in the fragment layout of the second projection's input
+// (rows padded to 16 with zeros).  Thread = 8 columns of one row.
+__global__ __launch_bounds__(256) void mlp_pack_kernel(const float* G, const float* U, uint16_t* dst, int T, int N) {
+    const int per_row = N >> 3;
+    const long long u = (long long)blockIdx.x * 256 + threadIdx.x;
+    const int rows = (T + 15) & ~15;
+    if (u >= (long long)rows * per_row) return;
+    const int row = (int)(u / per_row), col = (int)(u - (long long)row * per_row) * 8;
+    u32x4 o = u32x4{0u, 0u, 0u, 0u};
+    if (row < T) {
+        const float4 g0 = *reinterpret_cast<const float4*>(G + (size_t)row * N + col);
+        const float4 g1 = *reinterpret_cast<const float4*>(G + (size_t)row * N + col + 4);
+        float h[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+        if (U) {
+            const float4 u0 = *reinterpret_cast<const float4*>(U + (size_t)row * N + col);
+            const float4 u1 = *reinterpret_cast<const float4*>(U + (size_t)row * N + col + 4);
+            const float uv[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) h[e] = h[e] / (1.f + __expf(-h[e])) * uv[e];
+        }
+        o.x = (uint32_t)f2bf(h[0]) | ((uint32_t)f2bf(h[1]) << 16);
+        o.y = (uint32_t)f2bf(h[2]) | ((uint32_t)f2bf(h[3]) << 16);
+        o.z = (uint32_t)f2bf(h[4]) | ((uint32_t)f2bf(h[5]) << 16);
+        o.w = (uint32_t)f2bf(h[6]) | ((uint32_t)f2bf(h[7]) << 16);
+    }
+    const size_t f = ((size_t)(row >> 4) * (N >> 5) + (col >> 5)) * kFrag + ((row & 15) + 16 * ((col & 31) >> 3)) * 8;
+    *reinterpret_cast<u32x4*>(dst + f) = o;
+}
+
+hipError_t launch_mlp_pack(const float* G, const float* U, uint16_t* dst, int T, int N, hipStream_t s) {
+    if (T <= 0) return hipSuccess;
+    if (N % 32) return hipErrorInvalidValue;
+    const long long units = (long long)((T + 15) & ~15) * (N >> 3);
+    hipLaunchKernelGGL(mlp_pack_kernel, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, s, G, U, dst, T, N);
+    return hipGetLastError();
+}
+
 }  // namespace bdl

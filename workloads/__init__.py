@@ -130,6 +130,16 @@ def model_projs(model: str, tp: int) -> List[ProjSpec]:
     ]
 
 
+def tiny_mlp_projs() -> List[ProjSpec]:
+    """A small MLP shard for the MLP parity tests: gate and up (column), down
+    (row), the intermediate width a multiple of 32 and of 16."""
+    return [
+        ProjSpec("gate", "column", 320, (224,)),
+        ProjSpec("up", "column", 320, (224,)),
+        ProjSpec("down", "row", 224, (160,)),
+    ]
+
+
 def tiny_projs() -> List[ProjSpec]:
     """Small projections used by parity tests: several tiles and ragged shapes."""
     return [
@@ -326,3 +336,4 @@ def custom_workload(name: str, projs: List[ProjSpec], T: int, ranks: Sequence[in
 
 
 __all__.append("custom_workload")
+__all__.append("tiny_mlp_projs")
