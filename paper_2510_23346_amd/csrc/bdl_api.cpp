@@ -583,6 +583,20 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     if (groups_max + grid > L.part_slots) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
     da.n_proj = n;
     da.T = T;
+    {
+        unsigned u = 0;
+        int g = 0;
+        for (int i = 0; i < n; ++i) {
+            const int nb = da.p[i].nWb + act_max * da.p[i].nbA;
+            da.sub[i] = u;
+            da.sgb[i] = g;
+            da.snb[i] = nb;
+            da.sks[i] = da.p[i].K / 32;
+            u += (unsigned)nb * (unsigned)da.sks[i];
+            g += (nb + 3) / 4;
+        }
+        da.units = u;
+    }
     da.pool = P->d_slabs;
     da.slot_stride = L.slot_stride;
     da.scale = P->d_scale;
@@ -591,6 +605,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     da.tgrp = P->d_tgrp;
     da.gslot = P->d_gslot;
     da.meta = P->d_meta;
+    da.act_max = act_max;
     da.part = P->d_part;
     da.part_slots = (int)L.part_slots;
     da.main_grid = grid;

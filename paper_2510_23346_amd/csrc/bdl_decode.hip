@@ -30,9 +30,13 @@ namespace bdl {
 
 constexpr int kDecStages = 2;
 
-// Position of projection p in the unit and group orders for n_act adapters
-// in use.  Everything here derives from kernel arguments and one uniform
-// load, so it stays in scalar registers.
+// word 3 of a raw buffer resource on gfx950 (32-bit untyped data)
+constexpr int kRawBufferWord3 = 0x00020000;
+
+// Position of projection p in the unit and group orders.  The column lists
+// hold act_max adapter positions (the host's bound on the number of adapters
+// a batch uses, so the schedule is known before the plan is); positions at
+// or past the batch's count n_act are skipped.
 struct ProjPos {
     unsigned ub;    // first unit (the host keeps U * G below 2^32)
     int gb;         // first group
@@ -40,25 +44,8 @@ struct ProjPos {
     int KS;         // k-steps
 };
 
-__device__ __forceinline__ int dec_nblk(const DecArgs& a, int n_act, int p) {
-    return a.p[p].nWb + n_act * a.p[p].nbA;
-}
-
-__device__ __forceinline__ ProjPos dec_pos(const DecArgs& a, int n_act, int p) {
-    unsigned u = 0;
-    int g = 0;
-    for (int q = 0; q < p; ++q) {
-        const int nb = dec_nblk(a, n_act, q);
-        u += (unsigned)nb * (unsigned)(a.p[q].K >> 5);
-        g += (nb + 3) >> 2;
-    }
-    return ProjPos{u, g, dec_nblk(a, n_act, p), a.p[p].K >> 5};
-}
-
-__device__ __forceinline__ unsigned dec_units(const DecArgs& a, int n_act) {
-    unsigned u = 0;
-    for (int q = 0; q < a.n_proj; ++q) u += (unsigned)dec_nblk(a, n_act, q) * (unsigned)(a.p[q].K >> 5);
-    return u;
+__device__ __forceinline__ ProjPos dec_pos(const DecArgs& a, int p) {
+    return ProjPos{a.sub[p], a.sgb[p], a.snb[p], a.sks[p]};
 }
 
 // workgroup whose unit range holds unit u: largest b with floor(b U / G) <= u
@@ -66,28 +53,106 @@ __device__ __forceinline__ int dec_wg_of(unsigned u, unsigned U, int G) {
     return (int)(((u + 1) * (unsigned)G - 1) / U);
 }
 
+// A segment: the k-steps [k0, k1) of group gl of projection p that one
+// workgroup owns (its unit range cut at group ends).  Everything here is
+// uniform over the workgroup.
+struct DecSeg {
+    int p;
+    ProjPos pp;
+    int gl;           // group within the projection
+    unsigned goff;    // first unit of the group
+    int wdt;          // blocks in the group (4, fewer at a projection's end)
+    int k0, k1;
+    bool valid;
+};
+
+// cut the segment that starts at k-step g.k0 of the current group, moving to
+// the next group (and projection) when that group is used up; groups whose
+// first block belongs to an adapter position at or past n_act are skipped.
+// n_act arrives in a vector register (lane-uniform) and is read only for
+// adapter groups, so weight segments never wait for it.
+__device__ __forceinline__ void dec_cut(const DecArgs& a, int n_act_v, unsigned se, DecSeg& g) {
+    for (;;) {
+        if (g.k0 >= g.pp.KS) {
+            if (++g.gl >= ((g.pp.nb + 3) >> 2)) {
+                if (++g.p >= a.n_proj) {
+                    g.valid = false;
+                    return;
+                }
+                g.pp = dec_pos(a, g.p);
+                g.gl = 0;
+            }
+            g.goff = g.pp.ub + 4u * g.gl * g.pp.KS;
+            g.wdt = min(4, g.pp.nb - 4 * g.gl);
+            g.k0 = 0;
+            if (g.goff >= se) {
+                g.valid = false;
+                return;
+            }
+        }
+        g.k1 = (int)min((unsigned)g.pp.KS, (se - g.goff + g.wdt - 1) / (unsigned)g.wdt);
+        g.valid = g.k1 > g.k0;
+        const int vb0 = 4 * g.gl - a.p[g.p].nWb;
+        if (!g.valid || vb0 < 0) return;
+        if (vb0 < __builtin_amdgcn_readfirstlane(n_act_v) * a.p[g.p].nbA) return;
+        g.k0 = g.pp.KS;
+    }
+}
+
+// first segment of the unit range [sb, se): the group holding unit sb, from
+// its first k-step starting at or after sb
+__device__ __forceinline__ DecSeg dec_first(const DecArgs& a, int n_act_v, unsigned sb, unsigned se) {
+    DecSeg g;
+    g.p = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxProjs; ++q)
+        if (q < a.n_proj && sb >= a.sub[q]) g.p = q;
+    g.pp = dec_pos(a, g.p);
+    g.gl = min((int)((sb - g.pp.ub) / (4u * g.pp.KS)), ((g.pp.nb + 3) >> 2) - 1);
+    g.goff = g.pp.ub + 4u * g.gl * g.pp.KS;
+    g.wdt = min(4, g.pp.nb - 4 * g.gl);
+    g.k0 = (int)((sb - g.goff + g.wdt - 1) / (unsigned)g.wdt);
+    dec_cut(a, n_act_v, se, g);
+    return g;
+}
+
+__device__ __forceinline__ void dec_next(const DecArgs& a, int n_act_v, unsigned se, DecSeg& g) {
+    g.k0 = g.k1;
+    dec_cut(a, n_act_v, se, g);
+}
+
+// The k-steps of a segment that wave (column half cg, quarter kq) handles:
+// [*kw, *kw + items), none when the column half has no block in the group.
+__device__ __forceinline__ int dec_items(const DecSeg& g, int cg, int kq, int* kw) {
+    const int n = g.k1 - g.k0, q = n >> 2, r = n & 3;
+    *kw = g.k0 + kq * q + min(kq, r);
+    return 2 * cg < g.wdt ? q + (kq < r ? 1 : 0) : 0;
+}
+
+// element pointer of k-step 0 of virtual block vb of projection P; lane i of
+// gs holds the slot of the i-th adapter in use.  Positions at or past n_act
+// (in a group with a used one) read the first adapter's factor, unused.
+__device__ __forceinline__ const uint16_t* dec_block(const DecArgs& a, const DecProj& P, int vb, int KS, int gs,
+                                                     int n_act_v) {
+    if (vb < P.nWb) return P.W + frag_index(vb, 0, KS);
+    const int ai = (vb - P.nWb) / P.nbA, c = vb - P.nWb - ai * P.nbA;
+    const int slot = __builtin_amdgcn_readlane(gs, ai < __builtin_amdgcn_readfirstlane(n_act_v) ? ai : 0);
+    return a.pool + (size_t)slot * a.slot_stride + P.a_off + frag_index(c, 0, KS);
+}
+
 // Eight waves as 2 column halves x 4 K-quarters: wave w owns blocks
-// 2 (w & 1) and 2 (w & 1) + 1 of the group (nbw of them exist), over the
-// (w >> 1)-th quarter of the k-range.  The four quarters meet in LDS; all 512
-// threads then add them in a fixed order and store the group's fp32 partial
-// (rows < T, the group's wdt blocks) as 16-byte chunks.
+// 2 (w & 1) and 2 (w & 1) + 1 of the group, over the (w >> 1)-th quarter of
+// the segment's k-range.  At the end of a segment the four quarters meet in
+// LDS; all 512 threads add them in a fixed order and store the group's fp32
+// partial (rows < T, the group's wdt blocks) as 16-byte chunks.
 constexpr int kRedLd = 68;    // LDS row stride (floats): 4 rows apart land 16 banks apart
 
 template <int MB>
-__device__ __forceinline__ void seg_tile(const uint16_t* const (&ap)[MB], const uint16_t* const (&bp)[2],
-                                         int kb, int ke, int nbw, int wdt, float* red, float* dst, int T) {
+__device__ __forceinline__ void dec_flush(const DecArgs& a, const DecSeg& g, f32x4 (&acc)[MB][2], float* red, int b) {
     constexpr int REG = MB * 16 * kRedLd;
     const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1, kq = w >> 1;
-    f32x4 acc[MB][2];
-#pragma unroll
-    for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int n = ke - kb, q = n >> 2, r = n & 3;
-    const int k0 = kb + kq * q + min(kq, r), nk = q + (kq < r ? 1 : 0);
-    // a wave with one block loads it twice (second copy discarded): narrow
-    // groups only end a projection's column list
-    if (nk > 0 && nbw > 0) mma_range<MB, 2, kDecStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
     __syncthreads();                          // the previous segment's readers are done
-    if (nbw > 0) {
+    if (2 * cg < g.wdt) {
         float* reg = red + kq * REG + cg * 32 + (l & 15);
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb)
@@ -96,13 +161,16 @@ __device__ __forceinline__ void seg_tile(const uint16_t* const (&ap)[MB], const 
 #pragma unroll
                 for (int i = 0; i < 4; ++i) reg[(rb * 16 + 4 * (l >> 4) + i) * kRedLd + cb * 16] = acc[rb][cb][i];
     }
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     __syncthreads();
-    const int nc4 = wdt * 4;
+    float* dst = a.part + (size_t)min(g.pp.gb + g.gl + b, a.part_slots - 1) * kPartElems;
+    const int nc4 = g.wdt * 4;
 #pragma unroll
     for (int j = 0; j < (MB * 16 * 16 + kThreads - 1) / kThreads; ++j) {
         const int c = threadIdx.x + j * kThreads;
         const int row = c >> 4, c4 = c & 15;
-        if (c < MB * 16 * 16 && row < T && c4 < nc4) {
+        if (c < MB * 16 * 16 && row < a.T && c4 < nc4) {
             const float* src = red + row * kRedLd + c4 * 4;
             float4 v = *reinterpret_cast<const float4*>(src);
 #pragma unroll
@@ -115,59 +183,94 @@ __device__ __forceinline__ void seg_tile(const uint16_t* const (&ap)[MB], const 
     }
 }
 
-// element pointer of k-step 0 of virtual block vb of projection P
-__device__ __forceinline__ const uint16_t* dec_block(const DecArgs& a, const DecProj& P, int vb, int KS) {
-    if (vb < P.nWb) return P.W + frag_index(vb, 0, KS);
-    const int ai = (vb - P.nWb) / P.nbA, c = vb - P.nWb - ai * P.nbA;
-    const int slot = a.gslot[ai];
-    return a.pool + (size_t)slot * a.slot_stride + P.a_off + frag_index(c, 0, KS);
+// The workgroup's segments run through one load pipeline of two k-steps per
+// wave: a load cursor walks the wave's k-steps segment after segment two
+// k-steps ahead of the compute loop, so the loads of the next segment are in
+// flight while the current one is reduced and stored.  Loads are
+// unconditional (past the last k-step they repeat it), which keeps each
+// load's only consumer one pipeline turn later.
+template <int MB>
+__device__ __forceinline__ void mma2(f32x4 (&acc)[MB][2], const u32x4 (&xa)[MB], const u32x4 (&wb)[2]) {
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mfma(xa[rb], wb[cb], acc[rb][cb]);
 }
 
 template <int MB>
 __global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
     __shared__ float red[4 * MB * 16 * kRedLd];
-    const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1;
-    const int n_act = a.meta[0];
+    const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1, kq = w >> 1;
     const int G = gridDim.x, b = blockIdx.x;
-    const unsigned U = dec_units(a, n_act);
-    if (U == 0) return;
+    const unsigned U = a.units;               // the host launches with U >= 4 G
     const unsigned sb = (unsigned)b * U / (unsigned)G, se = (unsigned)(b + 1) * U / (unsigned)G;
+    // The plan's outputs (n_act, the slots of the adapters in use; at most
+    // kDecodeMaxT = 64 of them) are read with vector loads issued here and
+    // waited for only where an adapter segment first needs them, so the base
+    // weight's loads start without waiting for the plan.
+    const int gs = l < a.act_max ? a.gslot[l] : 0;
+    const int n_act_v = __builtin_amdgcn_raw_buffer_load_b32(
+        __builtin_amdgcn_make_buffer_rsrc((void*)a.meta, 0, 4, kRawBufferWord3), 0, 0, 0);
+    DecSeg cs = dec_first(a, n_act_v, sb, se);
+    if (!cs.valid) return;
 
-    // group holding unit sb, and its first k-step starting at or after sb
-    int p = 0;
-    ProjPos pp = dec_pos(a, n_act, 0);
-    while (p + 1 < a.n_proj && sb >= pp.ub + (unsigned)pp.nb * pp.KS) pp = dec_pos(a, n_act, ++p);
-    int gl = min((int)((sb - pp.ub) / (4u * pp.KS)), ((pp.nb + 3) >> 2) - 1);
-    unsigned goff = pp.ub + 4u * gl * pp.KS;
-    int wdt = min(4, pp.nb - 4 * gl);
-    int k0 = (int)((sb - goff + wdt - 1) / (unsigned)wdt);
-    for (;;) {
-        if (k0 >= pp.KS) {                    // next group (next projection after the last)
-            if (++gl >= ((pp.nb + 3) >> 2)) {
-                if (++p >= a.n_proj) break;
-                pp = dec_pos(a, n_act, p);
-                gl = 0;
-            }
-            goff = pp.ub + 4u * gl * pp.KS;
-            wdt = min(4, pp.nb - 4 * gl);
-            k0 = 0;
-            if (goff >= se) break;
-        }
-        const int KS = pp.KS;
-        const int k1 = (int)min((unsigned)KS, (se - goff + wdt - 1) / (unsigned)wdt);
-        if (k1 <= k0) break;
-        const DecProj& P = a.p[p];
-        const int nbw = max(0, min(2, wdt - 2 * cg));
-        const uint16_t* ap[MB];
-        const uint16_t* bp[2];
+    // load cursor: segment, this wave's k-steps in it (padded to an even
+    // count, so every segment starts on the first stage), the next one,
+    // operand bases (uniform; each lane adds its 16-byte offset)
+    DecSeg ls = cs;
+    int lkw, litems = dec_items(ls, cg, kq, &lkw), li = 0, lk = ls.k0;
+    const uint16_t* ap[MB];
+    const uint16_t* bp[2];
+    const unsigned lo = (unsigned)l * 16u;
+    auto point = [&]() {
+        const DecProj& P = a.p[ls.p];
 #pragma unroll
-        for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(rb, 0, KS) + l * 8;
+        for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(rb, 0, ls.pp.KS);
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
-            bp[cb] = dec_block(a, P, 4 * gl + min(2 * cg + cb, wdt - 1), KS) + l * 8;
-        const int slot = pp.gb + gl + b;
-        seg_tile<MB>(ap, bp, k0, k1, nbw, wdt, red, a.part + (size_t)min(slot, a.part_slots - 1) * kPartElems, a.T);
-        k0 = k1;
+            bp[cb] = dec_block(a, P, 4 * ls.gl + min(2 * cg + cb, ls.wdt - 1), ls.pp.KS, gs, n_act_v);
+        lk = ls.k0;                           // a k-step these bases may load
+    };
+    point();
+    auto issue = [&](u32x4 (&xa)[MB], u32x4 (&wb)[2]) {
+        while (ls.valid && li >= ((litems + 1) & ~1)) {
+            dec_next(a, n_act_v, se, ls);
+            if (ls.valid) {
+                litems = dec_items(ls, cg, kq, &lkw);
+                li = 0;
+                point();
+            }
+        }
+        if (ls.valid) {
+            if (li < litems) lk = lkw + li;   // else the padding slot repeats the last load
+            ++li;
+        }
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+            wb[cb] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(bp[cb] + (size_t)lk * kFrag) + lo);
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb)
+            xa[rb] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(ap[rb] + (size_t)lk * kFrag) + lo);
+    };
+
+    u32x4 xa0[MB], wb0[2], xa1[MB], wb1[2];
+    issue(xa0, wb0);
+    issue(xa1, wb1);
+    f32x4 acc[MB][2];
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (;;) {
+        int ckw;
+        const int n = dec_items(cs, cg, kq, &ckw);
+        for (int i = 0; i < n; i += 2) {
+            mma2<MB>(acc, xa0, wb0);
+            issue(xa0, wb0);
+            if (i + 1 < n) mma2<MB>(acc, xa1, wb1);
+            issue(xa1, wb1);
+        }
+        dec_flush<MB>(a, cs, acc, red, b);
+        dec_next(a, n_act_v, se, cs);
+        if (!cs.valid) break;
     }
 }
 
@@ -228,14 +331,13 @@ __device__ __forceinline__ void expand8(float (&acc)[8], const float (&z)[8], co
 // the first 16 ranks' B^T and of their Z partials is issued before any sum,
 // so a thread waits for two round trips (more only for ranks above 16 or
 // groups split over many workgroups).
-__device__ __forceinline__ void epi_acc(const DecArgs& a, int n_act, int p, int n, int t, int col,
-                                        float (&acc)[8]) {
+__device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, int col, float (&acc)[8]) {
     const DecProj& P = a.p[p];
     const int v = a.vid[t];
     const int r8s = a.tr8[t];
     const int ai = a.tgrp[t];
-    const ProjPos pp = dec_pos(a, n_act, p);
-    const unsigned U = dec_units(a, n_act);
+    const ProjPos pp = dec_pos(a, p);
+    const unsigned U = a.units;
     const int G = a.main_grid;
 
     // base partials of this tile
@@ -343,7 +445,6 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 // projection 1 being up), stored in bf16 in the fragment layout the second
 // projection reads (rows = tokens, k = these columns).
 __global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
-    const int n_act = a.meta[0];
     const int tile = blockIdx.x;
     int p = 0;
     while (p + 1 < a.n_proj && tile >= a.p[p + 1].tile_base) ++p;
@@ -353,14 +454,14 @@ __global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
     const int col = n * 64 + (threadIdx.x & 7) * 8;
     if (t >= a.T || col >= P.N) return;
     float acc[8];
-    epi_acc(a, n_act, p, n, t, col, acc);
+    epi_acc(a, p, n, t, col, acc);
     if (a.mlp_act < 0) {
         *reinterpret_cast<u32x4*>(P.out + (size_t)t * P.N + col) = pack_bf16x8(acc);
         return;
     }
     if (a.mlp_act == BDLORA_ACT_SILU_MUL) {
         float up[8];
-        epi_acc(a, n_act, 1, n, t, col, up);
+        epi_acc(a, 1, n, t, col, up);
 #pragma unroll
         for (int c = 0; c < 8; ++c) acc[c] = acc[c] / (1.f + __expf(-acc[c])) * up[c];
     }

@@ -111,6 +111,14 @@ struct DecProj {
 };
 
 struct DecArgs {
+    // Schedule of the main launch, computed by the host for act_max adapter
+    // positions: projection p's units start at sub[p] (sub[n_proj] = all
+    // units) and its groups at sgb[p]; it has snb[p] virtual blocks and
+    // sks[p] k-steps.  Kept first and compact so that a workgroup reads it
+    // with a few scalar loads.
+    unsigned units;
+    unsigned sub[kMaxProjs];
+    int sgb[kMaxProjs], snb[kMaxProjs], sks[kMaxProjs];
     DecProj p[kMaxProjs];
     int n_proj;
     int T;
@@ -121,7 +129,8 @@ struct DecArgs {
     const int* tr8;           // [T] padded rank of each token's adapter (0: none)
     const int* tgrp;          // [T] group (adapter in use) index of each token, -1: none
     const int* gslot;         // [groups] slot of each adapter in use
-    const int* meta;          // [0] number of adapters in use
+    const int* meta;          // [0] number of adapters in use (n_act)
+    int act_max;              // adapter positions in the column lists: the host's bound on n_act
     float* part;              // partial tiles: slot g + b for group g and workgroup b
     int part_slots;
     int main_grid;            // workgroups of the main launch
