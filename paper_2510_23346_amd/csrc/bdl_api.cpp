@@ -592,6 +592,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
             da.sgb[i] = g;
             da.snb[i] = nb;
             da.sks[i] = da.p[i].K / 32;
+            da.stb[i] = da.p[i].tile_base;
             u += (unsigned)nb * (unsigned)da.sks[i];
             g += (nb + 3) / 4;
         }

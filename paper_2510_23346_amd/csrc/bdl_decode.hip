@@ -357,7 +357,9 @@ __device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, i
     // LoRA operands of ranks 0..15: B^T rows and Z partials
     const bool lora = r8s > 0 && ai >= 0;
     int sig = 0;
-    while (sig + 1 < P.n_slices && col >= P.slice_col[sig + 1]) ++sig;
+#pragma unroll
+    for (int q = 1; q < kMaxSlices; ++q)
+        if (q < P.n_slices && col >= P.slice_col[q]) sig = q;
     const uint16_t* bb = a.pool + (size_t)max(v, 0) * a.slot_stride + P.b_off + (size_t)col * r8s;
     float sc = 0.f;
     u32x4 q[2][8];
@@ -447,14 +449,20 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 __global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
     const int tile = blockIdx.x;
     int p = 0;
-    while (p + 1 < a.n_proj && tile >= a.p[p + 1].tile_base) ++p;
+#pragma unroll
+    for (int q = 1; q < kMaxProjs; ++q)
+        if (q < a.n_proj && tile >= a.stb[q]) p = q;
     const DecProj& P = a.p[p];
-    const int n = tile - P.tile_base;
+    const int n = tile - a.stb[p];
     const int t = threadIdx.x >> 3;
     const int col = n * 64 + (threadIdx.x & 7) * 8;
-    if (t >= a.T || col >= P.N) return;
+    // threads past the last token or column compute on clamped indices and
+    // store nothing (no early exit: every load is issued without waiting on
+    // a branch)
+    const bool live = t < a.T && col < P.N;
     float acc[8];
-    epi_acc(a, p, n, t, col, acc);
+    epi_acc(a, p, n, min(t, a.T - 1), min(col, P.N - 8), acc);
+    if (!live) return;
     if (a.mlp_act < 0) {
         *reinterpret_cast<u32x4*>(P.out + (size_t)t * P.N + col) = pack_bf16x8(acc);
         return;

@@ -119,6 +119,7 @@ struct DecArgs {
     unsigned units;
     unsigned sub[kMaxProjs];
     int sgb[kMaxProjs], snb[kMaxProjs], sks[kMaxProjs];
+    int stb[kMaxProjs];       // first epilogue tile of each projection
     DecProj p[kMaxProjs];
     int n_proj;
     int T;
