@@ -16,8 +16,12 @@ Modules:
 * :mod:`oracle.plan`    -- id validation and grouping of tokens by adapter.
 * :mod:`oracle.costs`   -- the parameter, operation and byte counts of the
   paper's cost table (App. A).
+* :mod:`oracle.mlp`     -- the MLP shard of Alg. 1 (two projections with the
+  activation between them).
+* :mod:`oracle.quant`   -- the INT4 base weight (weight-only quantized base of
+  Sec. 5.2): decoding of the stored nibbles and scales.
 
 Every function is pinned by tests under ``tests/`` against facts the paper or
 plain mathematics fixes; see each module's header for its pins.
 """
-from . import bdlora, plan, costs  # noqa: F401
+from . import bdlora, plan, costs, mlp, quant  # noqa: F401

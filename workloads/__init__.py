@@ -169,6 +169,7 @@ class WorkloadSpec:
     segments: Tuple[int, ...] = ()    # prefill request lengths (segments/mixed)
     n_decode: int = 0                 # decode tokens after the segments (mixed)
     n_active: int = 0                 # active slot count (mixed)
+    weight_format: str = "bf16"       # base weight: "bf16" or "int4_g128"
     description: str = ""
     extra: Dict[str, object] = field(default_factory=dict)
 
@@ -247,6 +248,29 @@ class ProjInputs:
     X: np.ndarray         # float32 [T, d_in]
     W_bits: np.ndarray    # uint16 [d_in, d_out]  (paper layout: X @ W)
     W: np.ndarray         # float32 [d_in, d_out]
+    # INT4 base (weight_format "int4_g128"): nibbles q + 8, two per byte,
+    # [d_out, d_in / 2], and bf16 scales [d_out, d_in / 128]
+    Wq: Optional[np.ndarray] = None
+    Ws_bits: Optional[np.ndarray] = None
+
+
+def quantize_int4_g128(W: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Round-to-nearest symmetric INT4 quantization of a paper-layout weight
+    ``W [d_in, d_out]`` in groups of 128 input channels: the scale of a group
+    is the bf16 value nearest to max|W| / 7 (1 for an all-zero group), the
+    stored nibble ``clip(rint(W / scale), -8, 7) + 8``.  Returns
+    ``(qbytes [d_out, d_in / 2] uint8, scale_bits [d_out, d_in / 128])``;
+    input preparation only (the oracle decodes the stored values itself)."""
+    W = np.asarray(W, dtype=np.float32)
+    K, N = W.shape
+    if K % 128:
+        raise ValueError("d_in must be a multiple of 128")
+    g = np.abs(W.T.reshape(N, K // 128, 128)).max(axis=2) / np.float32(7.0)
+    g = np.where(g > 0, g, np.float32(1.0)).astype(np.float32)
+    s_bits, s = bf16_round(g)
+    q = np.clip(np.rint(W.T / np.repeat(s, 128, axis=1)), -8, 7).astype(np.int64) + 8
+    qbytes = (q[:, 0::2] | (q[:, 1::2] << 4)).astype(np.uint8)
+    return np.ascontiguousarray(qbytes), np.ascontiguousarray(s_bits)
 
 
 @dataclass
@@ -295,6 +319,11 @@ def draw_proj(spec: WorkloadSpec, p: int, T: Optional[int] = None) -> ProjInputs
     rng = np.random.default_rng([spec.seed, 1, p])
     Xb, X = _normal_bf16(rng, (T, ps.d_in), 1.0)
     Wb, W = _normal_bf16(rng, (ps.d_in, ps.d_out), 1.0 / ps.d_in)
+    if spec.weight_format == "int4_g128":
+        q, sb = quantize_int4_g128(W)
+        return ProjInputs(ps, Xb, X, Wb, W, q, sb)
+    if spec.weight_format != "bf16":
+        raise ValueError(spec.weight_format)
     return ProjInputs(ps, Xb, X, Wb, W)
 
 
@@ -325,15 +354,17 @@ def draw_layer(spec: WorkloadSpec, slots: Optional[Sequence[int]] = None) -> Lay
 
 def custom_workload(name: str, projs: List[ProjSpec], T: int, ranks: Sequence[int],
                     scales: Optional[Sequence[float]] = None, ids=None, seed: int = 0,
-                    ids_kind: str = "uniform") -> WorkloadSpec:
+                    ids_kind: str = "uniform", weight_format: str = "bf16") -> WorkloadSpec:
     """A generic test workload; ``ids`` may be given explicitly."""
     n = len(ranks)
     sc = list(scales) if scales is not None else [2.0] * n
     kind = "explicit" if ids is not None else ids_kind
     extra = {"ids": np.asarray(ids, dtype=np.int32)} if ids is not None else {}
     return WorkloadSpec(name, None, 0, list(projs), T=T, n_slots=n, ranks=list(ranks),
-                        scales=sc, ids_kind=kind, seed=seed, extra=extra)
+                        scales=sc, ids_kind=kind, seed=seed, extra=extra,
+                        weight_format=weight_format)
 
 
 __all__.append("custom_workload")
+__all__.append("quantize_int4_g128")
 __all__.append("tiny_mlp_projs")
