@@ -33,6 +33,15 @@ MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 matrix, published
 MALL_BYTES = 256 << 20
 
 
+def base_weight_bytes(spec, p):
+    """Bytes of one projection's base weight: bf16, or INT4 nibbles plus one
+    bf16 scale per 128 inputs of each output column."""
+    n = sum(p.slices)
+    if spec.weight_format == "int4_g128":
+        return p.d_in * n // 2 + n * (p.d_in // 128) * 2
+    return 2 * p.d_in * n
+
+
 def algorithmic_bytes(spec, ids, ranks):
     """Per-step bytes the method must move (bf16 = 2 bytes), split by launch.
 
@@ -46,13 +55,13 @@ def algorithmic_bytes(spec, ids, ranks):
     m = e = 0
     for p in spec.projs:
         n = sum(p.slices)
-        m += p.d_in * n + T * p.d_in
-        e += T * n
+        m += base_weight_bytes(spec, p) + 2 * T * p.d_in
+        e += 2 * T * n
         for a in active:
             r = ranks[a]
-            m += len(p.slices) * p.d_in * r
-            e += r * n
-    return 2 * m, 2 * e, len(active)
+            m += 2 * len(p.slices) * p.d_in * r
+            e += 2 * r * n
+    return m, e, len(active)
 
 
 def algorithmic_flops(spec, ids, ranks):
@@ -101,17 +110,18 @@ def committed_traffic(kernel, workload_name):
 def cpu_baseline(spec, layer, seconds):
     """Time the oracle (fp64 numpy) on this host: whole steps until
     ``seconds`` have passed."""
-    from oracle import bdlora
+    from oracle import bdlora, quant
+    forward = quant.layer_forward_w4 if spec.weight_format == "int4_g128" else bdlora.layer_forward
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    bdlora.layer_forward(layer)                     # warm-up
+    forward(layer)                                  # warm-up
     n = 0
     t0 = time.perf_counter()
     while True:
-        bdlora.layer_forward(layer)
+        forward(layer)
         n += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -131,7 +141,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", type=int, default=1, help="workload index 0..4 (default 1)")
+    ap.add_argument("--workload", type=int, default=1,
+                    help="workload index 0..5 (default 1; 5 = workload 1 with an INT4 base)")
     ap.add_argument("--rotate", type=int, default=0, help="input copies to rotate (0 = auto)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -283,6 +294,7 @@ def main():
             "adapters_resident": len(resident),
             "adapters_active": n_active,
             "ranks": sorted(set(spec.ranks)),
+            "base_weight": spec.weight_format,
             "parallelism": "one tensor-parallel shard (1 of 8) on one GPU",
             "timing": "eager launches" if args.eager else f"HIP graphs over {R} rotated input copies",
         },

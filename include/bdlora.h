@@ -74,17 +74,32 @@ extern "C" {
 #define BDLORA_ACT_NONE     0   /* H = first projection's output (Alg. 1)  */
 #define BDLORA_ACT_SILU_MUL 1   /* H = silu(gate) * up (gated MLP)         */
 
+/* Base weight formats (bdlora_proj_desc.weight_format).
+ * BDLORA_WEIGHT_BF16: bf16 W_s, packed by bdlora_pack_weight.
+ * BDLORA_WEIGHT_INT4_G128: weight-only INT4 base (the quantized backbone of
+ *   Sec. 5.2 / App. F; activations and adapters stay bf16): symmetric INT4
+ *   with one bf16 scale per output column and group of 128 inputs,
+ *   W[n][k] = scale[n][k / 128] * q[n][k], q in -8..7, packed by
+ *   bdlora_pack_weight_int4.  The kernels multiply the raw q by the bf16
+ *   activations on the matrix cores and apply the scale in fp32 per k-step,
+ *   so no dequantized weight is ever formed. */
+#define BDLORA_WEIGHT_BF16      0
+#define BDLORA_WEIGHT_INT4_G128 1
+
 typedef struct bdlora_pool* bdlora_pool_t;
 
 /* One projection on one shard.  d_in: local input width (K), a multiple of
  * 32.  slice_out[i]: local output width of slice i, a multiple of 16.
  * kind only documents the sharding (BDLORA_COLUMN / BDLORA_ROW); both kinds
- * run the same per-shard computation (Alg. 1 first and second projection). */
+ * run the same per-shard computation (Alg. 1 first and second projection).
+ * weight_format: BDLORA_WEIGHT_*; INT4 needs d_in a multiple of 128 and the
+ * total output width a multiple of 64. */
 typedef struct {
     int32_t kind;
     int32_t d_in;
     int32_t n_slices;
     int32_t slice_out[BDLORA_MAX_SLICES];
+    int32_t weight_format;
 } bdlora_proj_desc;
 
 /* Create an adapter pool on HIP device `device` for the `n_projs`
@@ -129,10 +144,30 @@ int bdlora_unload_adapter(bdlora_pool_t pool, int32_t slot);
  * Enqueued on `stream`.  Errors: INVALID_ARG, SHAPE, HIP. */
 int bdlora_pack_weight(const void* W, void* W_packed, int32_t N, int32_t K, void* stream);
 
+/* Bytes of a packed base weight [N x K] in format weight_format
+ * (BDLORA_WEIGHT_*): 2 N K for bf16, N K / 2 + N K / 64 for INT4.
+ * Returns 0 for an unknown format or sizes that format does not take. */
+size_t bdlora_packed_weight_bytes(int32_t weight_format, int32_t N, int32_t K);
+
+/* Pack an INT4 base weight (BDLORA_WEIGHT_INT4_G128) for forward calls.
+ * q: device uint8 [N x K/2], row n of the nn.Linear layout, byte (n, j)
+ * holding q[n][2j] + 8 in its low nibble and q[n][2j+1] + 8 in its high
+ * nibble.  scales: device bf16 [N x K/128].  W_packed: device,
+ * bdlora_packed_weight_bytes(BDLORA_WEIGHT_INT4_G128, N, K) bytes, 16-byte
+ * aligned, not overlapping the inputs.  Layout: first N K / 2 bytes of
+ * 32-bit words, word (rb (K/32) + ks) 64 + lane holding the 8 values
+ * W[16 rb + lane%16][32 ks + 8 (lane/16) + i], value i in bits
+ * 4 (i/2) + 16 (i%2) .. +3 (as q + 8); then the scales as bf16, entry
+ * (rb (K/128) + g) 16 + c = scale[16 rb + c][g].  N: multiple of 64; K:
+ * multiple of 128.  Enqueued on `stream`.  Errors: INVALID_ARG, SHAPE, HIP. */
+int bdlora_pack_weight_int4(const void* q, const void* scales, void* W_packed, int32_t N, int32_t K,
+                            void* stream);
+
 /* One projection call (Alg. 2 on one device; Alg. 1 first or second
  * projection): out = X W_s^T + scale_a (X A_a) B_a per token.
  * proj: index into the pool's projection list.  X: device [T x d_in];
- * W: device, the base weight [d_out_s x d_in] packed by bdlora_pack_weight;
+ * W: device, the base weight [d_out_s x d_in] packed by bdlora_pack_weight
+ * (or bdlora_pack_weight_int4 for an INT4 projection);
  * ids: device int32 [T]; out: device [T x d_out_s].
  * T: 0..max_tokens (T = 0 enqueues nothing).  Errors: INVALID_ARG, SHAPE, HIP. */
 int bdlora_forward_shard(bdlora_pool_t pool, int32_t proj, const void* X, const void* W,

@@ -110,3 +110,17 @@ def brute_force_w4(X, qbytes, scale_bits, ids, adapters, slices) -> np.ndarray:
             for n in range(int(slices[j])):
                 out[t, col0[j] + n] += gamma * sum(z[c] * B[c, n] for c in range(A.shape[1]))
     return out
+
+
+def layer_forward_w4(layer, rows=None):
+    """All projection calls of a drawn layer whose base weights are INT4
+    (``workloads.LayerInputs`` with ``Wq`` / ``Ws_bits`` set), optionally for
+    the token rows ``rows`` only."""
+    ids = np.asarray(layer.ids)
+    outs = []
+    for p, pi in enumerate(layer.projs):
+        ad = {s: (a.scale, a.A[p], a.B[p]) for s, a in layer.adapters.items()}
+        X = pi.X if rows is None else pi.X[np.asarray(rows)]
+        ii = ids if rows is None else ids[np.asarray(rows)]
+        outs.append(shard_forward_w4(X, pi.Wq, pi.Ws_bits, ii, ad, pi.spec.slices))
+    return outs

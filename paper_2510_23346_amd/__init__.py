@@ -18,13 +18,15 @@ import numpy as np
 __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
     "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T",
-    "ACT_NONE", "ACT_SILU_MUL",
+    "ACT_NONE", "ACT_SILU_MUL", "WEIGHT_BF16", "WEIGHT_INT4_G128", "pack_weight_int4",
+    "packed_weight_bytes",
 ]
 
 COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
 ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections
+WEIGHT_BF16, WEIGHT_INT4_G128 = 0, 1   # BDLORA_WEIGHT_*: base weight formats
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libbdlora.so")
 _LIB = None
@@ -42,7 +44,7 @@ _LP = _c.POINTER(_c.c_int64)
 
 class ProjDesc(ctypes.Structure):
     _fields_ = [("kind", _c.c_int32), ("d_in", _c.c_int32), ("n_slices", _c.c_int32),
-                ("slice_out", _c.c_int32 * MAX_SLICES)]
+                ("slice_out", _c.c_int32 * MAX_SLICES), ("weight_format", _c.c_int32)]
 
 
 _SIGS = {
@@ -57,6 +59,8 @@ _SIGS = {
     "bdlora_plan_device": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P]),
     "bdlora_get_device_error": (_I, [_P, _P, _IP]),
     "bdlora_pack_weight": (_I, [_P, _P, _I, _I, _P]),
+    "bdlora_packed_weight_bytes": (_c.c_size_t, [_I, _I, _I]),
+    "bdlora_pack_weight_int4": (_I, [_P, _P, _P, _I, _I, _P]),
     "bdlora_adapter_elems": (_I, [_c.POINTER(ProjDesc), _I, _I, _LP]),
     "bdlora_pool_size": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _I, _LP, _LP]),
     "bdlora_pool_bytes": (_I, [_P, _LP]),
@@ -98,7 +102,7 @@ def _check(rc: int):
         raise BDLoRAError(rc, lib().bdlora_last_error().decode())
 
 
-def _descs(projs) -> Tuple[ctypes.Array, List[Tuple[int, int, Tuple[int, ...]]]]:
+def _descs(projs, weight_formats=None) -> Tuple[ctypes.Array, List[Tuple[int, int, Tuple[int, ...]]]]:
     norm = []
     for p in projs:
         if hasattr(p, "d_in"):               # workloads.ProjSpec or similar
@@ -109,7 +113,14 @@ def _descs(projs) -> Tuple[ctypes.Array, List[Tuple[int, int, Tuple[int, ...]]]]
             kind = ROW if kind in ("row", ROW) else COLUMN
             norm.append((kind, int(d_in), tuple(int(s) for s in slices)))
     arr = (ProjDesc * max(1, len(norm)))()
+    if weight_formats is None:
+        weight_formats = [WEIGHT_BF16] * len(norm)
+    elif isinstance(weight_formats, int):
+        weight_formats = [weight_formats] * len(norm)
+    if len(weight_formats) != len(norm):
+        raise ValueError("one weight format per projection")
     for i, (kind, d_in, slices) in enumerate(norm):
+        arr[i].weight_format = int(weight_formats[i])
         if not 1 <= len(slices) <= MAX_SLICES:
             raise ValueError("a projection has 1..4 slices")
         arr[i].kind = kind
@@ -144,6 +155,33 @@ def pack_weight(W, W_packed=None, stream=None):
     if tuple(W_packed.shape) != (N, K) or not W.is_contiguous() or not W_packed.is_contiguous():
         raise ValueError("W and W_packed must be contiguous [N, K] tensors")
     _check(lib().bdlora_pack_weight(_ptr(W), _ptr(W_packed), N, K, _stream_handle(stream)))
+    return W_packed
+
+
+def packed_weight_bytes(weight_format: int, N: int, K: int) -> int:
+    """Bytes of a packed base weight (0 if the format does not take the shape)."""
+    return int(lib().bdlora_packed_weight_bytes(int(weight_format), int(N), int(K)))
+
+
+def pack_weight_int4(q, scales, W_packed=None, stream=None):
+    """Pack an INT4 base weight for forward calls: ``q`` uint8 device tensor
+    ``[N, K/2]`` (nibbles q+8, low nibble = even input), ``scales`` bf16
+    ``[N, K/128]``; returns the packed uint8 tensor."""
+    N, K2 = int(q.shape[0]), int(q.shape[1])
+    K = 2 * K2
+    nbytes = packed_weight_bytes(WEIGHT_INT4_G128, N, K)
+    if nbytes == 0:
+        raise ValueError("an INT4 base weight needs N a multiple of 64 and K of 128")
+    if tuple(scales.shape) != (N, K // 128) or scales.element_size() != 2:
+        raise ValueError(f"scales must be a 2-byte [N, K/128] = [{N}, {K // 128}] tensor")
+    if q.element_size() != 1 or not q.is_contiguous() or not scales.is_contiguous():
+        raise ValueError("q must be a contiguous uint8 tensor, scales contiguous")
+    if W_packed is None:
+        import torch
+        W_packed = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    if W_packed.numel() * W_packed.element_size() < nbytes:
+        raise ValueError(f"W_packed must hold {nbytes} bytes")
+    _check(lib().bdlora_pack_weight_int4(_ptr(q), _ptr(scales), _ptr(W_packed), N, K, _stream_handle(stream)))
     return W_packed
 
 
@@ -198,8 +236,10 @@ class Pool:
     or objects with ``kind``, ``d_in`` and ``slices`` attributes.
     """
 
-    def __init__(self, projs, max_slots: int, max_rank: int, max_tokens: int, device: int = 0):
-        self._arr, self.projs = _descs(projs)
+    def __init__(self, projs, max_slots: int, max_rank: int, max_tokens: int, device: int = 0,
+                 weight_formats=None):
+        self._arr, self.projs = _descs(projs, weight_formats)
+        self.weight_formats = [int(self._arr[i].weight_format) for i in range(len(self.projs))]
         self.max_slots, self.max_rank, self.max_tokens = int(max_slots), int(max_rank), int(max_tokens)
         self.device = int(device)
         h = _c.c_void_p()
@@ -268,6 +308,11 @@ class Pool:
             return                               # the library reports the bad index
         kind, d_in, slices = self.projs[p]
         n = sum(slices)
+        if self.weight_formats[p] != WEIGHT_BF16 and hasattr(W, "shape"):
+            need = packed_weight_bytes(self.weight_formats[p], n, d_in)
+            if W.numel() * W.element_size() < need or not W.is_contiguous():
+                raise ValueError(f"packed INT4 W must be a contiguous buffer of {need} bytes")
+            W = None
         for name, t, shape in (("X", X, (T, d_in)), ("W", W, (n, d_in)), ("out", out, (T, n))):
             if hasattr(t, "shape"):
                 if tuple(t.shape) != shape:

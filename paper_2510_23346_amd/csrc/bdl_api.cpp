@@ -34,6 +34,7 @@ int rank8(int r) { return (r + 7) / 8 * 8; }
 
 struct ProjInfo {
     int kind, K, S, N, zs;
+    int wfmt;                         // BDLORA_WEIGHT_*
     int slice_out[bdl::kMaxSlices];
     int slice_col[bdl::kMaxSlices + 1];
     long long a_off, b_off;           // element offsets inside a slot
@@ -94,6 +95,11 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
         P.slice_col[bdl::kMaxSlices] = col;
         for (int s = d.n_slices; s <= bdl::kMaxSlices; ++s) P.slice_col[s] = col;
         P.N = col;
+        if (d.weight_format != BDLORA_WEIGHT_BF16 && d.weight_format != BDLORA_WEIGHT_INT4_G128)
+            return fail(BDLORA_ERR_INVALID_ARG, "unknown weight_format");
+        if (d.weight_format == BDLORA_WEIGHT_INT4_G128 && (P.K % 128 || P.N % 64))
+            return fail(BDLORA_ERR_SHAPE, "an INT4 base needs d_in a multiple of 128 and d_out a multiple of 64");
+        P.wfmt = d.weight_format;
         P.zs = P.S * L->r8max;
         P.a_off = off;                                   // packed A^T_cat, rows padded to 16
         off = round_up(off + round_up((long long)P.S * L->r8max, 16) * P.K, kAlign);
@@ -542,6 +548,12 @@ struct DecMode {
     int h_KS = 0;
 };
 
+// scales of a packed INT4 base weight (null for a bf16 base)
+static const uint16_t* int4_scales(const ProjInfo& pi, const void* W) {
+    if (pi.wfmt != BDLORA_WEIGHT_INT4_G128) return nullptr;
+    return reinterpret_cast<const uint16_t*>(static_cast<const char*>(W) + (size_t)pi.N * pi.K / 2);
+}
+
 static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
                           const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s,
                           const DecMode& mode = DecMode()) {
@@ -559,6 +571,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         bdl::DecProj& d = da.p[i];
         d.Xp = P->d_Xp[projs[i]];
         d.W = (const uint16_t*)W[i];
+        d.Ws = int4_scales(pi, W[i]);
         d.out = (uint16_t*)out[i];
         d.K = pi.K;
         d.N = pi.N;
@@ -702,6 +715,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         pl.X = (const uint16_t*)X[i];
         pl.Xp = P->d_Xp[projs[i]];
         pl.W = (const uint16_t*)W[i];
+        pl.Ws = int4_scales(pi, W[i]);
         pl.out = (uint16_t*)out[i];
         pl.out_f32 = out_f32 ? out_f32[i] : nullptr;
         pl.Z = P->d_Z[projs[i]];
@@ -895,6 +909,37 @@ int bdlora_pack_weight(const void* W, void* W_packed, int32_t N, int32_t K, void
     if (N < 16 || N % 16 || K < 32 || K % 32) return fail(BDLORA_ERR_SHAPE, "N must be a multiple of 16, K of 32");
     if (!aligned16(W) || !aligned16(W_packed)) return fail(BDLORA_ERR_INVALID_ARG, "pointers must be 16-byte aligned");
     BDL_HIP(bdl::launch_pack_rows((const uint16_t*)W, (uint16_t*)W_packed, N, K, (hipStream_t)stream));
+    return BDLORA_OK;
+}
+
+size_t bdlora_packed_weight_bytes(int32_t weight_format, int32_t N, int32_t K) {
+    if (N < 16 || K < 32 || N > (1 << 20) || K > (1 << 20)) return 0;
+    if (weight_format == BDLORA_WEIGHT_BF16)
+        return N % 16 || K % 32 ? 0 : (size_t)N * K * 2;
+    if (weight_format == BDLORA_WEIGHT_INT4_G128)
+        return N % 64 || K % 128 ? 0 : (size_t)N * K / 2 + (size_t)N * (K / 128) * 2;
+    return 0;
+}
+
+int bdlora_pack_weight_int4(const void* q, const void* scales, void* W_packed, int32_t N, int32_t K,
+                            void* stream) {
+    if (!q || !scales || !W_packed) return fail(BDLORA_ERR_INVALID_ARG, "null pointer");
+    if (N < 64 || N % 64 || K < 128 || K % 128 || N > (1 << 20) || K > (1 << 20))
+        return fail(BDLORA_ERR_SHAPE, "N must be a multiple of 64, K of 128");
+    if (!aligned16(W_packed)) return fail(BDLORA_ERR_INVALID_ARG, "W_packed must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(scales) % 2) return fail(BDLORA_ERR_INVALID_ARG, "scales must be 2-byte aligned");
+    const size_t bytes = bdlora_packed_weight_bytes(BDLORA_WEIGHT_INT4_G128, N, K);
+    const char* d0 = static_cast<const char*>(W_packed);
+    auto overlaps = [&](const void* p, size_t n) {
+        const char* c = static_cast<const char*>(p);
+        return c < d0 + bytes && d0 < c + n;
+    };
+    if (overlaps(q, (size_t)N * K / 2) || overlaps(scales, (size_t)N * (K / 128) * 2))
+        return fail(BDLORA_ERR_INVALID_ARG, "packing cannot overlap its inputs");
+    uint32_t* dw = static_cast<uint32_t*>(W_packed);
+    uint16_t* ds = reinterpret_cast<uint16_t*>(static_cast<char*>(W_packed) + (size_t)N * K / 2);
+    BDL_HIP(bdl::launch_pack_int4(static_cast<const uint8_t*>(q), static_cast<const uint16_t*>(scales), dw, ds, N, K,
+                                  (hipStream_t)stream));
     return BDLORA_OK;
 }
 

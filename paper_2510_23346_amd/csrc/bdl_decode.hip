@@ -197,8 +197,17 @@ __device__ __forceinline__ void mma2(f32x4 (&acc)[MB][2], const u32x4 (&xa)[MB],
         for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mfma(xa[rb], wb[cb], acc[rb][cb]);
 }
 
+// INT4 base blocks: wb[cb].x holds the lane's word, wb[cb].y the scale bits
 template <int MB>
-__global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
+__device__ __forceinline__ void mma2_int4(f32x4 (&acc)[MB][2], const u32x4 (&xa)[MB], const u32x4 (&wb)[2]) {
+    const uint32_t q[2] = {wb[0].x, wb[1].x}, sc[2] = {wb[0].y, wb[1].y};
+    mma_int4_kstep<MB, 2>(acc, xa, q, sc);
+}
+
+// Q4: some projection of the launch has an INT4 base (the kernel then handles
+// both operand types; without it the INT4 code is compiled out).
+template <int MB, bool Q4>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void dec_main_kernel(DecArgs a) {
     __shared__ float red[4 * MB * 16 * kRedLd];
     const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1, kq = w >> 1;
     const int G = gridDim.x, b = blockIdx.x;
@@ -220,19 +229,29 @@ __global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
     DecSeg ls = cs;
     int lkw, litems = dec_items(ls, cg, kq, &lkw), li = 0, lk = ls.k0;
     const uint16_t* ap[MB];
-    const uint16_t* bp[2];
+    // the two blocks' bases (bytes) and, for INT4 base blocks, their scales
+    const char *bp0 = nullptr, *bp1 = nullptr;
+    const uint16_t *sp0 = nullptr, *sp1 = nullptr;
+    bool lq = false;                          // the loader's segment streams INT4 base blocks
     const unsigned lo = (unsigned)l * 16u;
-    auto point = [&]() {
+    auto point = [&]() __attribute__((always_inline)) {
         const DecProj& P = a.p[ls.p];
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(rb, 0, ls.pp.KS);
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-            bp[cb] = dec_block(a, P, 4 * ls.gl + min(2 * cg + cb, ls.wdt - 1), ls.pp.KS, gs, n_act_v);
+        lq = Q4 && P.Ws && 4 * ls.gl < P.nWb;
+        const int vb0 = 4 * ls.gl + min(2 * cg, ls.wdt - 1), vb1 = 4 * ls.gl + min(2 * cg + 1, ls.wdt - 1);
+        // both candidates are formed and one is selected (no branch: the
+        // bases stay in registers)
+        const char* wq = reinterpret_cast<const char*>(P.W);
+        const size_t qs = (size_t)ls.pp.KS * kInt4FragBytes, ss = (size_t)(ls.pp.KS / kInt4Group) * 16;
+        bp0 = lq ? wq + vb0 * qs : reinterpret_cast<const char*>(dec_block(a, P, vb0, ls.pp.KS, gs, n_act_v));
+        bp1 = lq ? wq + vb1 * qs : reinterpret_cast<const char*>(dec_block(a, P, vb1, ls.pp.KS, gs, n_act_v));
+        sp0 = lq ? P.Ws + vb0 * ss : P.Ws;
+        sp1 = lq ? P.Ws + vb1 * ss : P.Ws;
         lk = ls.k0;                           // a k-step these bases may load
     };
     point();
-    auto issue = [&](u32x4 (&xa)[MB], u32x4 (&wb)[2]) {
+    auto issue = [&](u32x4 (&xa)[MB], u32x4 (&wb)[2]) __attribute__((always_inline)) {
         while (ls.valid && li >= ((litems + 1) & ~1)) {
             dec_next(a, n_act_v, se, ls);
             if (ls.valid) {
@@ -245,9 +264,16 @@ __global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
             if (li < litems) lk = lkw + li;   // else the padding slot repeats the last load
             ++li;
         }
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-            wb[cb] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(bp[cb] + (size_t)lk * kFrag) + lo);
+        if (lq) {
+            const size_t qo = (size_t)lk * kInt4FragBytes + (lo >> 2);
+            const int so = (lk / kInt4Group) * 16 + (l & 15);
+            wb[0] = u32x4{*reinterpret_cast<const uint32_t*>(bp0 + qo), sp0[so], 0u, 0u};
+            wb[1] = u32x4{*reinterpret_cast<const uint32_t*>(bp1 + qo), sp1[so], 0u, 0u};
+        } else {
+            const size_t fo = (size_t)lk * kFrag * 2 + lo;
+            wb[0] = *reinterpret_cast<const u32x4*>(bp0 + fo);
+            wb[1] = *reinterpret_cast<const u32x4*>(bp1 + fo);
+        }
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb)
             xa[rb] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(ap[rb] + (size_t)lk * kFrag) + lo);
@@ -262,10 +288,19 @@ __global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
     for (;;) {
         int ckw;
         const int n = dec_items(cs, cg, kq, &ckw);
+        const bool cq = Q4 && a.p[cs.p].Ws && 4 * cs.gl < a.p[cs.p].nWb;   // INT4 base blocks
         for (int i = 0; i < n; i += 2) {
-            mma2<MB>(acc, xa0, wb0);
+            if (cq)
+                mma2_int4<MB>(acc, xa0, wb0);
+            else
+                mma2<MB>(acc, xa0, wb0);
             issue(xa0, wb0);
-            if (i + 1 < n) mma2<MB>(acc, xa1, wb1);
+            if (i + 1 < n) {
+                if (cq)
+                    mma2_int4<MB>(acc, xa1, wb1);
+                else
+                    mma2<MB>(acc, xa1, wb1);
+            }
             issue(xa1, wb1);
         }
         dec_flush<MB>(a, cs, acc, red, b);
@@ -277,13 +312,23 @@ __global__ __launch_bounds__(kThreads) void dec_main_kernel(DecArgs a) {
 hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s) {
     const int grid = a.main_grid;
     if (grid <= 0 || grid > kDecMaxGrid) return hipErrorInvalidValue;
+    bool q4 = false;
+    for (int i = 0; i < a.n_proj; ++i) q4 = q4 || a.p[i].Ws != nullptr;
+#define BDL_DEC_CASE(M)                                                                                  \
+    case M:                                                                                              \
+        if (q4)                                                                                          \
+            hipLaunchKernelGGL((dec_main_kernel<M, true>), dim3(grid), dim3(kThreads), 0, s, a);         \
+        else                                                                                             \
+            hipLaunchKernelGGL((dec_main_kernel<M, false>), dim3(grid), dim3(kThreads), 0, s, a);        \
+        break;
     switch (mb) {
-        case 1: hipLaunchKernelGGL(dec_main_kernel<1>, dim3(grid), dim3(kThreads), 0, s, a); break;
-        case 2: hipLaunchKernelGGL(dec_main_kernel<2>, dim3(grid), dim3(kThreads), 0, s, a); break;
-        case 3: hipLaunchKernelGGL(dec_main_kernel<3>, dim3(grid), dim3(kThreads), 0, s, a); break;
-        case 4: hipLaunchKernelGGL(dec_main_kernel<4>, dim3(grid), dim3(kThreads), 0, s, a); break;
+        BDL_DEC_CASE(1)
+        BDL_DEC_CASE(2)
+        BDL_DEC_CASE(3)
+        BDL_DEC_CASE(4)
         default: return hipErrorInvalidValue;
     }
+#undef BDL_DEC_CASE
     return hipGetLastError();
 }
 

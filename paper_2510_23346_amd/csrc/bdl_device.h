@@ -100,6 +100,85 @@ __device__ __forceinline__ void mma_range(f32x4 (&acc)[MB][NB], const uint16_t* 
         if (d < rem) comp(d);
 }
 
+// INT4 base weights.  One 32-bit word per lane and k-step holds the 8 values
+// of the lane's B operand as nibbles q + 8, value i in bits 4 (i/2) + 16 (i%2).
+// Each nibble u becomes the bf16 number 128 + u (exponent of 128, u in the low
+// mantissa bits), which is exact; an extra MFMA against -136 removes the
+// offset, so the matrix cores see exactly sum_k x_k q_k for the k-step.  The
+// group scale is applied in fp32 to that k-step's product.
+constexpr int kInt4Group = 4;                 // k-steps per scale group (128 inputs)
+constexpr int kInt4FragBytes = 256;           // one k-step of one 16-column block
+
+__device__ __forceinline__ u32x4 unpack_int4(uint32_t w) {
+    return u32x4{(w & 0x000F000Fu) | 0x43004300u, ((w >> 4) & 0x000F000Fu) | 0x43004300u,
+                 ((w >> 8) & 0x000F000Fu) | 0x43004300u, ((w >> 12) & 0x000F000Fu) | 0x43004300u};
+}
+
+__device__ __forceinline__ u32x4 int4_offset_operand() {
+    return u32x4{0xC308C308u, 0xC308C308u, 0xC308C308u, 0xC308C308u};   // bf16 -136 x 8
+}
+
+// acc[rb][cb] += s_cb * (x_rb . q_cb) for one k-step: xa = activation
+// fragments, q[cb] = the INT4 words, sc[cb] = bf16 scale bits (low half).
+template <int MB, int NB>
+__device__ __forceinline__ void mma_int4_kstep(f32x4 (&acc)[MB][NB], const u32x4 (&xa)[MB], const uint32_t (&q)[NB],
+                                               const uint32_t (&sc)[NB]) {
+    const u32x4 off = int4_offset_operand();
+    const f32x4 zero = f32x4{0.f, 0.f, 0.f, 0.f};
+    u32x4 w[NB];
+    float s[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+        w[cb] = unpack_int4(q[cb]);
+        s[cb] = __uint_as_float(sc[cb] << 16);
+    }
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) {
+        const f32x4 corr = mfma(xa[rb], off, zero);
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+            const f32x4 t = mfma(xa[rb], w[cb], corr);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[rb][cb][i] = fmaf(s[cb], t[i], acc[rb][cb][i]);
+        }
+    }
+}
+
+// mma_range for an INT4 B operand: wq[cb] points at this lane's word of
+// k-step 0 of block cb (k-steps kInt4FragBytes apart), ws[cb] at the block's
+// scale of group 0 for this lane's column (groups 16 entries apart).
+template <int MB, int NB, int D>
+__device__ __forceinline__ void mma_range_int4(f32x4 (&acc)[MB][NB], const uint16_t* const (&ap)[MB],
+                                               const char* const (&wq)[NB], const uint16_t* const (&ws)[NB],
+                                               int k0, int n) {
+    u32x4 a[D][MB];
+    uint32_t q[D][NB], sc[D][NB];
+    const int last = k0 + n - 1;
+    auto load = [&](int d, int ks) {
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+            q[d][cb] = *reinterpret_cast<const uint32_t*>(wq[cb] + (size_t)ks * kInt4FragBytes);
+            sc[d][cb] = ws[cb][(ks / kInt4Group) * 16];
+        }
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) a[d][rb] = ld16(ap[rb] + (size_t)ks * kFrag);
+    };
+#pragma unroll
+    for (int d = 0; d < D; ++d) load(d, min(k0 + d, last));
+    int i = 0;
+    for (; i + D <= n; i += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            mma_int4_kstep<MB, NB>(acc, a[d], q[d], sc[d]);
+            load(d, min(k0 + i + d + D, last));
+        }
+    }
+    const int rem = n - i;
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+        if (d < rem) mma_int4_kstep<MB, NB>(acc, a[d], q[d], sc[d]);
+}
+
 // Contiguous k-step range of wave w when KS k-steps are split over kWaves.
 __device__ __forceinline__ void wave_krange(int KS, int w, int* k0, int* n) {
     const int q = KS / kWaves, r = KS - q * kWaves;

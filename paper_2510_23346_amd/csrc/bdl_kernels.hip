@@ -161,7 +161,20 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(FwdArgs a) {
         for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
     int k0, nk;
     wave_krange(KS, w, &k0, &nk);
-    if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
+    if (P.Ws) {
+        // INT4 base: same tile, the raw q on the matrix cores, scales in fp32
+        const char* wq[NB];
+        const uint16_t* wsc[NB];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+            const int blk = min(nt * NB + cb, ncb - 1);
+            wq[cb] = reinterpret_cast<const char*>(P.W) + (size_t)blk * KS * kInt4FragBytes + l * 4;
+            wsc[cb] = P.Ws + (size_t)blk * (KS / kInt4Group) * 16 + lr;
+        }
+        if (nk > 0) mma_range_int4<MB, NB, kStages>(acc, ap, wq, wsc, k0, nk);
+    } else if (nk > 0) {
+        mma_range<MB, NB, kStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
+    }
 
     // ---- expand: acc += Zhat B over the tile's octets (masked per token)
     int sig[NB];
@@ -263,6 +276,49 @@ hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K,
     long long blocks = (frags + 3) / 4;
     if (blocks > 16384) blocks = 16384;
     hipLaunchKernelGGL(pack_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, src, dst, rows, K, frags);
+    return hipGetLastError();
+}
+
+// INT4 base weight: nn.Linear rows of nibbles (low nibble = even input) and
+// bf16 scales [N x K/128] -> the forward layout (one 32-bit word per lane and
+// k-step, then the scales grouped per 16-column block).  Thread = one word or
+// one scale.
+__global__ void pack_int4_kernel(const uint8_t* q, const uint16_t* scales, uint32_t* dst_w, uint16_t* dst_s, int N,
+                                 int K) {
+    const long long words = (long long)N * K / 8, nsc = (long long)N * (K / 128);
+    const int KS = K >> 5, G = K >> 7;
+    for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < words + nsc;
+         i += (long long)gridDim.x * blockDim.x) {
+        if (i < words) {
+            const int l = (int)(i & 63);
+            const long long f = i >> 6;
+            const int rb = (int)(f / KS), ks = (int)(f - (long long)rb * KS);
+            const int n = rb * 16 + (l & 15), k0 = ks * 32 + (l >> 4) * 8;
+            const uint8_t* src = q + (size_t)n * (K / 2) + k0 / 2;
+            uint32_t w = 0;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                const uint32_t nib = (src[v >> 1] >> (4 * (v & 1))) & 15u;
+                w |= nib << (4 * (v >> 1) + 16 * (v & 1));
+            }
+            dst_w[i] = w;
+        } else {
+            const long long j = i - words;
+            const int c = (int)(j & 15);
+            const long long r = j >> 4;
+            const int rb = (int)(r / G), g = (int)(r - (long long)rb * G);
+            dst_s[j] = scales[(size_t)(rb * 16 + c) * G + g];
+        }
+    }
+}
+
+hipError_t launch_pack_int4(const uint8_t* q, const uint16_t* scales, uint32_t* dst_w, uint16_t* dst_s, int N,
+                            int K, hipStream_t s) {
+    const long long total = (long long)N * K / 8 + (long long)N * (K / 128);
+    if (total == 0) return hipSuccess;
+    long long blocks = (total + 255) / 256;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(pack_int4_kernel, dim3((unsigned)blocks), dim3(256), 0, s, q, scales, dst_w, dst_s, N, K);
     return hipGetLastError();
 }
 

@@ -19,6 +19,7 @@ struct ProjLaunch {
     const uint16_t* X;        // [T x K] bf16 activations (row-major)
     const uint16_t* Xp;       // packed activations, fragment layout, rows padded to 16
     const uint16_t* W;        // packed base weight, fragment layout ([N x K] nn.Linear rows)
+    const uint16_t* Ws;       // INT4 base: its scales (null for a bf16 base)
     uint16_t* out;            // [T x N] bf16
     float* out_f32;           // when set: the output in fp32 [T x N] instead of out
     uint16_t* Z;              // [2 x max_tokens x zs] workspace: scale * X A per slice as a
@@ -101,6 +102,7 @@ constexpr int kPartElems = 64 * 64;  // fp32 partial tile: 64 rows x 64 virtual 
 struct DecProj {
     const uint16_t* Xp;       // packed activations (fragment layout)
     const uint16_t* W;        // packed base weight
+    const uint16_t* Ws;       // INT4 base: its scales (null for a bf16 base)
     uint16_t* out;            // [T x N] bf16
     int K, N, n_slices;
     int slice_col[kMaxSlices + 1];
@@ -151,6 +153,8 @@ hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K,
                                int n_slices, const int* slice_out, int rank, int r8, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s);
+hipError_t launch_pack_int4(const uint8_t* q, const uint16_t* scales, uint32_t* dst_w, uint16_t* dst_s, int N,
+                            int K, hipStream_t s);
 hipError_t launch_mlp_pack(const float* G, const float* U, uint16_t* dst, int T, int N, hipStream_t s);
 
 }  // namespace bdl

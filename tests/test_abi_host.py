@@ -25,7 +25,7 @@ def L():
 
 def _header_functions():
     text = open(os.path.join(ROOT, "include", "bdlora.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:int|const char\s*\*)\s+(bdlora_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\s*\*)\s+(bdlora_\w+)\s*\(", text, re.M)))
 
 
 def test_exports_every_declared_function(L):
@@ -43,6 +43,8 @@ def test_binding_constants_match_header():
     assert (int(macros["BDLORA_ACT_NONE"]), int(macros["BDLORA_ACT_SILU_MUL"])) == (bd.ACT_NONE, bd.ACT_SILU_MUL)
     assert int(macros["BDLORA_MAX_SLICES"]) == bd.MAX_SLICES
     assert (int(macros["BDLORA_COLUMN"]), int(macros["BDLORA_ROW"])) == (bd.COLUMN, bd.ROW)
+    assert (int(macros["BDLORA_WEIGHT_BF16"]), int(macros["BDLORA_WEIGHT_INT4_G128"])) == \
+        (bd.WEIGHT_BF16, bd.WEIGHT_INT4_G128)
     for code, name in bd.STATUS.items():
         assert int(macros["BDLORA_" + ("OK" if code == 0 else "ERR_" + name)]) == code
 
@@ -125,3 +127,30 @@ def test_no_gpu_means_a_loud_error(L):
     with pytest.raises(bd.BDLoRAError) as e:
         bd.Pool([("column", 64, (16,))], 4, 8, 16)
     assert e.value.code in (-6, -5)
+
+
+def test_packed_weight_bytes(L):
+    # bf16: 2 bytes per element; INT4: half a byte per element plus one bf16
+    # scale per 128 inputs of each column
+    assert bd.packed_weight_bytes(bd.WEIGHT_BF16, 1792, 4096) == 1792 * 4096 * 2
+    assert bd.packed_weight_bytes(bd.WEIGHT_INT4_G128, 1792, 4096) == 1792 * 4096 // 2 + 1792 * 32 * 2
+    assert bd.packed_weight_bytes(bd.WEIGHT_INT4_G128, 4096, 512) == 4096 * 256 + 4096 * 4 * 2
+    # shapes the format does not take, and unknown formats
+    assert bd.packed_weight_bytes(bd.WEIGHT_INT4_G128, 48, 4096) == 0       # N % 64
+    assert bd.packed_weight_bytes(bd.WEIGHT_INT4_G128, 64, 96) == 0         # K % 128
+    assert bd.packed_weight_bytes(bd.WEIGHT_BF16, 24, 64) == 0
+    assert bd.packed_weight_bytes(7, 64, 128) == 0
+
+
+def test_int4_descriptor_validation(L):
+    ok = [("column", 256, (64,))]
+    assert bd.pool_size(ok, 4, 8, 16)[0] > 0
+    import ctypes
+    arr, _ = bd._descs(ok, bd.WEIGHT_INT4_G128)
+    a, b = ctypes.c_int64(), ctypes.c_int64()
+    assert L.bdlora_pool_size(arr, 1, 4, 8, 16, ctypes.byref(a), ctypes.byref(b)) == 0
+    for projs in ([("column", 96, (64,))], [("column", 256, (48,))]):        # K % 128, N % 64
+        arr, _ = bd._descs(projs, bd.WEIGHT_INT4_G128)
+        assert L.bdlora_pool_size(arr, 1, 4, 8, 16, ctypes.byref(a), ctypes.byref(b)) == -4
+    arr, _ = bd._descs(ok, 5)
+    assert L.bdlora_pool_size(arr, 1, 4, 8, 16, ctypes.byref(a), ctypes.byref(b)) == -1

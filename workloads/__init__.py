@@ -217,6 +217,13 @@ def workload(index: int) -> WorkloadSpec:
             description="Llama-3.1-70B layer shard, 4 prefill requests x 1024 tokens "
                         "plus 192 decode tokens, 512-adapter pool, r_s in {8,16,32,64}, "
                         "64 active adapters")
+    if index == 5:
+        w = workload(1)
+        return WorkloadSpec(
+            "8b-layer-decode-T64-int4", w.model, w.tp, w.projs, w.T, w.n_slots, w.ranks, w.scales,
+            w.ids_kind, w.seed, weight_format="int4_g128",
+            description="workload 1 (Llama-3.1-8B layer shard, 64 decode tokens, 32 adapters "
+                        "r_s=16, Zipf ids) with an INT4 base (one bf16 scale per 128 inputs)")
     raise KeyError(index)
 
 

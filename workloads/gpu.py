@@ -51,7 +51,12 @@ class DeviceLayer:
         self.X, self.W, self.out = [], [], []
         for pi in layer.projs:
             self.X.append(bits_to_device(pi.X_bits[:T], device))
-            self.W.append(pack_weight(bits_to_device(np.ascontiguousarray(pi.W_bits.T), device)))
+            if pi.Wq is not None:
+                from paper_2510_23346_amd import pack_weight_int4
+                q = torch.from_numpy(np.ascontiguousarray(pi.Wq)).to(device)
+                self.W.append(pack_weight_int4(q, bits_to_device(pi.Ws_bits, device)))
+            else:
+                self.W.append(pack_weight(bits_to_device(np.ascontiguousarray(pi.W_bits.T), device)))
             self.out.append(torch.empty((T, pi.spec.d_out), dtype=torch.bfloat16, device=device))
 
     def outputs(self) -> List[np.ndarray]:
@@ -60,9 +65,10 @@ class DeviceLayer:
 
 def make_pool(spec: WorkloadSpec, max_tokens: Optional[int] = None, max_rank: Optional[int] = None,
               device: int = 0):
-    from paper_2510_23346_amd import Pool
+    from paper_2510_23346_amd import Pool, WEIGHT_BF16, WEIGHT_INT4_G128
     mr = max(spec.ranks) if max_rank is None else max_rank
-    return Pool(spec.projs, spec.n_slots, mr, max_tokens or spec.T, device=device)
+    wf = WEIGHT_INT4_G128 if spec.weight_format == "int4_g128" else WEIGHT_BF16
+    return Pool(spec.projs, spec.n_slots, mr, max_tokens or spec.T, device=device, weight_formats=wf)
 
 
 def load_adapters(pool, spec: WorkloadSpec, slots: Sequence[int],
