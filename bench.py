@@ -136,6 +136,143 @@ def cpu_baseline(spec, layer, seconds):
     }
 
 
+def adapter_load_bench(args):
+    """Adapter load pipeline on the default layer shard (Llama-3.1-8B, 1/8
+    TP, 5 projections): per-adapter load time against its parameter count,
+    and decode steps whose adapters are not cached (every step loads the
+    adapters its batch uses before its forward), with the loads serialized
+    before the forward or overlapped with the previous step's forward on a
+    second stream.  Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    import paper_2510_23346_amd as bd
+    import workloads as wl
+    from workloads.gpu import DeviceLayer
+
+    base = wl.workload(1)
+    projs = list(range(len(base.projs)))
+    out = {"metric": "adapter load", "workload": base.name, "loads": []}
+    # 1. load time per adapter against its parameter count
+    for r in (8, 16, 32, 64):
+        spec = wl.WorkloadSpec(f"load-r{r}", base.model, base.tp, base.projs, base.T, 64, [r] * 64,
+                               [2.0] * 64, "uniform", 11)
+        pool = bd.Pool(spec.projs, 64, r, spec.T)
+        ad = wl.draw_adapter(spec, 0)
+        params = bd.adapter_elems(spec.projs, r)
+        slab = torch.empty(pool.slot_bytes, dtype=torch.uint8).pin_memory()
+        pool.pack_adapter_host(r, ad.A_bits, ad.B_bits, out=slab)
+        s = torch.cuda.Stream()
+        n = 64
+        for i in range(4):
+            pool.load_adapter_packed(i, r, 2.0, slab, stream=s)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(n):
+            pool.load_adapter_packed(i % 64, r, 2.0, slab, stream=s)
+        torch.cuda.synchronize()
+        t_packed = (time.perf_counter() - t0) / n
+        t0 = time.perf_counter()
+        for i in range(8):
+            pool.load_adapter(i, r, 2.0, ad.A_bits, ad.B_bits)
+        t_sync = (time.perf_counter() - t0) / 8
+        many = torch.empty(16 * pool.slot_bytes, dtype=torch.uint8).pin_memory()
+        for i in range(16):
+            many[i * pool.slot_bytes:(i + 1) * pool.slot_bytes].copy_(slab)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(8):
+            pool.load_adapters_packed(16 * (i % 4), [r] * 16, [2.0] * 16, many, stream=s)
+        torch.cuda.synchronize()
+        t_batch = (time.perf_counter() - t0) / (8 * 16)
+        out["loads"].append({"rank": r, "params": params, "bytes": 2 * params,
+                             "packed_pinned_us": round(t_packed * 1e6, 1),
+                             "packed_GBps": round(2 * params / t_packed / 1e9, 1),
+                             "slot_bytes": pool.slot_bytes,
+                             "packed_batch16_us_per_adapter": round(t_batch * 1e6, 1),
+                             "packed_batch16_GBps": round(pool.slot_bytes / t_batch / 1e9, 1),
+                             "paper_layout_sync_us": round(t_sync * 1e6, 1)})
+        pool.close()
+    # 2. no adapter cache: each decode step loads its batch's adapters first,
+    # back to back into consecutive slots with one copy (slot i of a half
+    # holds the batch's i-th adapter)
+    spec = base
+    ids = wl.draw_ids(spec)
+    active = sorted(int(a) for a in np.unique(ids) if a >= 0)
+    layer = wl.draw_layer(spec, slots=active)
+    nS = len(active)
+    pool = bd.Pool(spec.projs, 2 * nS, max(spec.ranks), spec.T)     # two halves of slots
+    sb = pool.slot_bytes
+    slabs = torch.empty(nS * sb, dtype=torch.uint8).pin_memory()
+    for i, a in enumerate(active):
+        ad = layer.adapters[a]
+        pool.pack_adapter_host(ad.rank, ad.A_bits, ad.B_bits, out=slabs[i * sb:(i + 1) * sb])
+    ranks = [spec.ranks[a] for a in active]
+    scales = [spec.scales[a] for a in active]
+    dl = DeviceLayer(layer)
+    pos = np.full(spec.n_slots, -1, np.int64)
+    pos[active] = np.arange(nS)
+    local = torch.from_numpy(np.where(ids >= 0, pos[np.maximum(ids, 0)], -1).astype(np.int32)).cuda()
+    ids_half = [local, torch.where(local >= 0, local + nS, local)]
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+
+    def load_step(half, stream):
+        pool.load_adapters_packed(half * nS, ranks, scales, slabs, stream=stream)
+
+    K = 50
+    for h in (0, 1):
+        load_step(h, main)
+    pool.forward_layer(projs, dl.X, dl.W, dl.out, ids_half[0], stream=main)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        pool.forward_layer(projs, dl.X, dl.W, dl.out, ids_half[0], stream=main)
+    torch.cuda.synchronize()
+    t_fwd = (time.perf_counter() - t0) / K
+    t0 = time.perf_counter()
+    for i in range(K):
+        load_step(0, main)
+        pool.forward_layer(projs, dl.X, dl.W, dl.out, ids_half[0], stream=main)
+    torch.cuda.synchronize()
+    t_serial = (time.perf_counter() - t0) / K
+    # overlapped: the loads of step i+1 go to the other half of the slots on
+    # the side stream while step i runs; each forward waits for its loads
+    loaded = [torch.cuda.Event() for _ in range(2)]
+    freed = [torch.cuda.Event() for _ in range(2)]
+    for h in (0, 1):
+        freed[h].record(main)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    side.wait_event(freed[0])
+    load_step(0, side)
+    loaded[0].record(side)
+    for i in range(K):
+        h = i % 2
+        side.wait_event(freed[1 - h])
+        load_step(1 - h, side)
+        loaded[1 - h].record(side)
+        main.wait_event(loaded[h])
+        pool.forward_layer(projs, dl.X, dl.W, dl.out, ids_half[h], stream=main)
+        freed[h].record(main)
+    torch.cuda.synchronize()
+    t_overlap = (time.perf_counter() - t0) / K
+    # the load alone
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        load_step(i % 2, main)
+    torch.cuda.synchronize()
+    t_load = (time.perf_counter() - t0) / K
+    pool.close()
+    out["no_cache_decode"] = {
+        "tokens": spec.T, "adapters_loaded_per_step": len(active),
+        "bytes_loaded_per_step": int(nS * sb),
+        "load_only_us": round(t_load * 1e6, 1), "load_GBps": round(nS * sb / t_load / 1e9, 1),
+        "forward_only_us": round(t_fwd * 1e6, 1), "load_then_forward_us": round(t_serial * 1e6, 1),
+        "overlapped_us": round(t_overlap * 1e6, 1), "timing": "eager launches, host clock"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,6 +287,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before the benchmark, run 3 plain device copies of MIB MiB (untimed), "
                          "a known-size reference for hardware byte counters")
+    ap.add_argument("--adapter-load", action="store_true",
+                    help="measure the adapter load pipeline instead (one JSON line of its own)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs one GPU's shard only; --gpus {args.gpus} is not supported "
@@ -165,6 +304,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     bd.lib()
+    if args.adapter_load:
+        adapter_load_bench(args)
+        return
     if args.copy_calibration:
         n = args.copy_calibration << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)

@@ -133,6 +133,47 @@ int bdlora_destroy_pool(bdlora_pool_t pool);
 int bdlora_load_adapter(bdlora_pool_t pool, int32_t slot, int32_t rank, float scale,
                         const uint16_t* const* A_host, const uint16_t* const* B_host);
 
+/* Adapter load pipeline (the per-request adapter loading of Sec. 5.2 / App. F:
+ * an adapter that is not cached on the GPU is brought in before its request
+ * runs; the time scales with its parameter count).  A host-side cache keeps
+ * adapters already in the pool's slot layout; loading one is then a single
+ * host-to-device copy of bdlora_slot_bytes(pool) bytes plus a table update,
+ * both enqueued on the caller's stream so they can overlap forward calls that
+ * use other slots on another stream. */
+
+/* Bytes of one adapter slot of the pool (0 for a null pool). */
+int64_t bdlora_slot_bytes(bdlora_pool_t pool);
+
+/* Pack one adapter on the host into the pool's slot layout (for a host-side
+ * cache): slab_host receives bdlora_slot_bytes(pool) bytes (padding zeroed).
+ * rank, A_host and B_host as for bdlora_load_adapter.  Pure host code; the
+ * result is byte-identical, in every region the kernels read, to what
+ * bdlora_load_adapter writes on the device.  Errors: INVALID_ARG (bad rank,
+ * null pointer, non-finite value). */
+int bdlora_pack_adapter_host(bdlora_pool_t pool, int32_t rank, const uint16_t* const* A_host,
+                             const uint16_t* const* B_host, void* slab_host);
+
+/* Enqueue on `stream` the copy of a host-packed slab into `slot` and the
+ * update of the slot's rank and scale; returns without waiting.  The whole
+ * slot is copied (bdlora_slot_bytes: about 2 bytes per parameter for an
+ * adapter of the pool's max_rank).  With
+ * slab_host in pinned memory (hipHostMalloc, or a pinned torch tensor) the
+ * copy is asynchronous; pageable memory is staged by the runtime.  The caller
+ * keeps slab_host alive until the stream has passed the copy, orders forward
+ * calls that use the slot after it (same stream, or an event), and must not
+ * overwrite a slot that a forward in flight still reads.  Errors:
+ * INVALID_ARG, HIP. */
+int bdlora_load_adapter_packed(bdlora_pool_t pool, int32_t slot, int32_t rank, float scale,
+                               const void* slab_host, void* stream);
+
+/* As bdlora_load_adapter_packed for n (1..64) adapters into the consecutive
+ * slots first_slot .. first_slot + n - 1: slabs_host holds their host-packed
+ * slabs back to back (n * bdlora_slot_bytes bytes), ranks[i] and scales[i]
+ * (host arrays) belong to slot first_slot + i.  One copy and one table
+ * update for the whole batch.  Errors: INVALID_ARG, HIP. */
+int bdlora_load_adapters_packed(bdlora_pool_t pool, int32_t first_slot, int32_t n, const int32_t* ranks,
+                                const float* scales, const void* slabs_host, void* stream);
+
 /* Mark `slot` empty; later ids naming it are invalid.  Errors: INVALID_ARG. */
 int bdlora_unload_adapter(bdlora_pool_t pool, int32_t slot);
 

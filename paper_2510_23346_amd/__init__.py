@@ -52,6 +52,10 @@ _SIGS = {
     "bdlora_destroy_pool": (_I, [_P]),
     "bdlora_load_adapter": (_I, [_P, _I, _I, _c.c_float, _c.POINTER(_P), _c.POINTER(_P)]),
     "bdlora_unload_adapter": (_I, [_P, _I]),
+    "bdlora_slot_bytes": (_c.c_int64, [_P]),
+    "bdlora_pack_adapter_host": (_I, [_P, _I, _c.POINTER(_P), _c.POINTER(_P), _P]),
+    "bdlora_load_adapter_packed": (_I, [_P, _I, _I, _c.c_float, _P, _P]),
+    "bdlora_load_adapters_packed": (_I, [_P, _I, _I, _IP, _c.POINTER(_c.c_float), _P, _P]),
     "bdlora_forward_shard": (_I, [_P, _I, _P, _P, _P, _I, _P, _P]),
     "bdlora_forward_layer": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _I, _P]),
     "bdlora_forward_mlp": (_I, [_P, _I, _IP, _I, _P, _c.POINTER(_P), _P, _P, _P, _I, _P]),
@@ -277,6 +281,67 @@ class Pool:
         return out.value
 
     # -- adapters ---------------------------------------------------------
+    def _flat_factors(self, rank: int, A, B):
+        flatA, flatB, keep = [], [], []
+        for p, (_, d_in, slices) in enumerate(self.projs):
+            for s, n in enumerate(slices):
+                a = np.ascontiguousarray(np.asarray(A[p][s]).view(np.uint16) if rank else np.zeros((d_in, 0), np.uint16))
+                b = np.ascontiguousarray(np.asarray(B[p][s]).view(np.uint16) if rank else np.zeros((0, n), np.uint16))
+                if a.shape != (d_in, rank) or b.shape != (rank, n):
+                    raise ValueError(f"adapter factor shapes {a.shape}, {b.shape} do not match "
+                                     f"({d_in}, {rank}), ({rank}, {n})")
+                keep += [a, b]
+                flatA.append(a.ctypes.data)
+                flatB.append(b.ctypes.data)
+        pa = (_c.c_void_p * max(1, len(flatA)))(*flatA)
+        pb = (_c.c_void_p * max(1, len(flatB)))(*flatB)
+        return pa, pb, keep
+
+    @property
+    def slot_bytes(self) -> int:
+        return int(lib().bdlora_slot_bytes(self._h))
+
+    def pack_adapter_host(self, rank: int, A, B, out=None):
+        """Pack one adapter on the host into the pool's slot layout (for a
+        host-side adapter cache).  ``out``: a CPU uint8 tensor or numpy array
+        of ``slot_bytes`` bytes (pinned memory makes later loads
+        asynchronous); returns it."""
+        if out is None:
+            out = np.empty(self.slot_bytes, dtype=np.uint8)
+        n = out.numel() * out.element_size() if hasattr(out, "numel") else out.nbytes
+        if n < self.slot_bytes:
+            raise ValueError(f"out must hold {self.slot_bytes} bytes")
+        ptr = out.data_ptr() if hasattr(out, "data_ptr") else out.ctypes.data
+        pa, pb, keep = self._flat_factors(int(rank), A, B)
+        _check(lib().bdlora_pack_adapter_host(self._h, int(rank), pa, pb, ptr))
+        del keep
+        return out
+
+    def load_adapter_packed(self, slot: int, rank: int, scale: float, slab, stream=None):
+        """Enqueue the copy of a host-packed slab into ``slot`` on ``stream``
+        (asynchronous for pinned memory; keep ``slab`` alive until the stream
+        has passed the copy)."""
+        n = slab.numel() * slab.element_size() if hasattr(slab, "numel") else slab.nbytes
+        if n < self.slot_bytes:
+            raise ValueError(f"slab must hold {self.slot_bytes} bytes")
+        ptr = slab.data_ptr() if hasattr(slab, "data_ptr") else slab.ctypes.data
+        _check(lib().bdlora_load_adapter_packed(self._h, int(slot), int(rank), float(scale), ptr,
+                                                _stream_handle(stream)))
+        self.loaded[int(slot)] = 1
+
+    def load_adapters_packed(self, first_slot: int, ranks, scales, slabs, stream=None):
+        """Enqueue one copy of ``len(ranks)`` host-packed slabs (back to back
+        in ``slabs``) into the consecutive slots from ``first_slot``."""
+        n = len(ranks)
+        nbytes = slabs.numel() * slabs.element_size() if hasattr(slabs, "numel") else slabs.nbytes
+        if len(scales) != n or nbytes < n * self.slot_bytes:
+            raise ValueError(f"slabs must hold {n} x {self.slot_bytes} bytes, one rank and scale each")
+        ptr = slabs.data_ptr() if hasattr(slabs, "data_ptr") else slabs.ctypes.data
+        r = (_c.c_int32 * max(1, n))(*[int(x) for x in ranks])
+        sc = (_c.c_float * max(1, n))(*[float(x) for x in scales])
+        _check(lib().bdlora_load_adapters_packed(self._h, int(first_slot), n, r, sc, ptr, _stream_handle(stream)))
+        self.loaded[int(first_slot):int(first_slot) + n] = 1
+
     def load_adapter(self, slot: int, rank: int, scale: float, A, B):
         """``A[p][s]``: uint16 bf16 bits ``[d_in, rank]``; ``B[p][s]``:
         ``[rank, slice_out]`` (paper layout), for every projection p and

@@ -478,6 +478,99 @@ int bdlora_load_adapter(bdlora_pool_t P, int32_t slot, int32_t rank, float scale
     return upload_slot_tables(P, slot);
 }
 
+int64_t bdlora_slot_bytes(bdlora_pool_t P) {
+    return P ? P->L.slot_stride * 2 : 0;
+}
+
+int bdlora_pack_adapter_host(bdlora_pool_t P, int32_t rank, const uint16_t* const* A_host,
+                             const uint16_t* const* B_host, void* slab_host) {
+    if (!P || !slab_host) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    const Layout& L = P->L;
+    if (rank < 0 || rank > L.max_rank) return fail(BDLORA_ERR_INVALID_ARG, "rank out of range 0..max_rank");
+    if (rank > 0 && (!A_host || !B_host)) return fail(BDLORA_ERR_INVALID_ARG, "null factor arrays");
+    const int r8 = rank8(rank);
+    uint16_t* slab = static_cast<uint16_t*>(slab_host);
+    std::memset(slab, 0, (size_t)L.slot_stride * 2);
+    int k = 0;
+    for (int p = 0; p < L.n_projs; ++p) {
+        const ProjInfo& pi = L.proj[p];
+        if (rank == 0) {
+            k += pi.S;
+            continue;
+        }
+        for (int s = 0; s < pi.S; ++s) {
+            if (!A_host[k + s] || !B_host[k + s]) return fail(BDLORA_ERR_INVALID_ARG, "null factor pointer");
+        }
+        // A^T_cat in the fragment layout: row s*r8 + j is column j of A_s
+        // (zero for j >= rank), rows padded to 16; element
+        // [(rb KS + ks) 512 + lane 8 + i] = A^T_cat[16 rb + lane%16][32 ks + 8 (lane/16) + i]
+        const int KS = pi.K / 32, arows = pi.S * r8;
+        uint16_t* da = slab + pi.a_off;
+        for (int row = 0; row < arows; ++row) {
+            const int s = row / r8, j = row - s * r8;
+            if (j >= rank) continue;
+            const uint16_t* a = A_host[k + s];
+            const int rb = row / 16, lr = row % 16;
+            for (int kk = 0; kk < pi.K; ++kk) {
+                const uint16_t v = a[(size_t)kk * rank + j];
+                if ((v & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in A");
+                const int ks = kk / 32, w = kk % 32, lane = lr + 16 * (w / 8), i = w % 8;
+                da[((size_t)rb * KS + ks) * 512 + lane * 8 + i] = v;
+            }
+        }
+        // B^T_cat [N x r8] row-major: row n is column n of its slice's B
+        uint16_t* db = slab + pi.b_off;
+        for (int s = 0; s < pi.S; ++s) {
+            const uint16_t* b = B_host[k + s];
+            const int n_s = pi.slice_out[s];
+            for (int j = 0; j < rank; ++j)
+                for (int n = 0; n < n_s; ++n) {
+                    const uint16_t v = b[(size_t)j * n_s + n];
+                    if ((v & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in B");
+                    db[(size_t)(pi.slice_col[s] + n) * r8 + j] = v;
+                }
+        }
+        k += pi.S;
+    }
+    return BDLORA_OK;
+}
+
+int bdlora_load_adapters_packed(bdlora_pool_t P, int32_t first_slot, int32_t n, const int32_t* ranks,
+                                const float* scales, const void* slabs_host, void* stream) {
+    if (!P || !slabs_host || !ranks || !scales) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    const Layout& L = P->L;
+    if (n < 1 || n > bdl::kMaxSlotBatch) return fail(BDLORA_ERR_INVALID_ARG, "n must be 1..64");
+    if (first_slot < 0 || first_slot + n > L.max_slots) return fail(BDLORA_ERR_INVALID_ARG, "slots out of range");
+    bdl::SlotBatch sb;
+    sb.first = first_slot;
+    sb.n = n;
+    for (int i = 0; i < n; ++i) {
+        if (ranks[i] < 0 || ranks[i] > L.max_rank) return fail(BDLORA_ERR_INVALID_ARG, "rank out of range 0..max_rank");
+        if (!std::isfinite(scales[i])) return fail(BDLORA_ERR_INVALID_ARG, "scale must be finite");
+        sb.r8[i] = rank8(ranks[i]);
+        sb.scale[i] = scales[i];
+    }
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    hipStream_t s = (hipStream_t)stream;
+    // consecutive slots are one contiguous range of the pool: one copy
+    BDL_HIP(hipMemcpyAsync(P->d_slabs + (long long)first_slot * L.slot_stride, slabs_host,
+                           (size_t)n * L.slot_stride * 2, hipMemcpyHostToDevice, s));
+    BDL_HIP(bdl::launch_set_slots(P->d_r8, P->d_scale, P->d_loaded, sb, s));
+    for (int i = 0; i < n; ++i) {
+        P->h_rank[first_slot + i] = ranks[i];
+        P->h_r8[first_slot + i] = sb.r8[i];
+        P->h_scale[first_slot + i] = scales[i];
+        P->h_loaded[first_slot + i] = 1;
+    }
+    return BDLORA_OK;
+}
+
+int bdlora_load_adapter_packed(bdlora_pool_t P, int32_t slot, int32_t rank, float scale, const void* slab_host,
+                               void* stream) {
+    return bdlora_load_adapters_packed(P, slot, 1, &rank, &scale, slab_host, stream);
+}
+
 int bdlora_unload_adapter(bdlora_pool_t P, int32_t slot) {
     if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
     if (slot < 0 || slot >= P->L.max_slots) return fail(BDLORA_ERR_INVALID_ARG, "slot out of range");

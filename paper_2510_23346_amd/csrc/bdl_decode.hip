@@ -183,8 +183,8 @@ __device__ __forceinline__ void dec_flush(const DecArgs& a, const DecSeg& g, f32
     }
 }
 
-// The workgroup's segments run through one load pipeline of two k-steps per
-// wave: a load cursor walks the wave's k-steps segment after segment two
+// The workgroup's segments run through one load pipeline of kDecStages k-steps per
+// wave: a load cursor walks the wave's k-steps segment after segment that many
 // k-steps ahead of the compute loop, so the loads of the next segment are in
 // flight while the current one is reduced and stored.  Loads are
 // unconditional (past the last k-step they repeat it), which keeps each
@@ -223,8 +223,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     DecSeg cs = dec_first(a, n_act_v, sb, se);
     if (!cs.valid) return;
 
-    // load cursor: segment, this wave's k-steps in it (padded to an even
-    // count, so every segment starts on the first stage), the next one,
+    // load cursor: segment, this wave's k-steps in it (padded to a multiple
+    // of kDecStages, so every segment starts on the first stage), the next one,
     // operand bases (uniform; each lane adds its 16-byte offset)
     DecSeg ls = cs;
     int lkw, litems = dec_items(ls, cg, kq, &lkw), li = 0, lk = ls.k0;
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     };
     point();
     auto issue = [&](u32x4 (&xa)[MB], u32x4 (&wb)[2]) __attribute__((always_inline)) {
-        while (ls.valid && li >= ((litems + 1) & ~1)) {
+        while (ls.valid && li >= (litems + kDecStages - 1) / kDecStages * kDecStages) {
             dec_next(a, n_act_v, se, ls);
             if (ls.valid) {
                 litems = dec_items(ls, cg, kq, &lkw);
@@ -279,9 +279,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
             xa[rb] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(ap[rb] + (size_t)lk * kFrag) + lo);
     };
 
-    u32x4 xa0[MB], wb0[2], xa1[MB], wb1[2];
-    issue(xa0, wb0);
-    issue(xa1, wb1);
+    u32x4 xs[kDecStages][MB], ws[kDecStages][2];
+#pragma unroll
+    for (int d = 0; d < kDecStages; ++d) issue(xs[d], ws[d]);
     f32x4 acc[MB][2];
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -289,19 +289,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
         int ckw;
         const int n = dec_items(cs, cg, kq, &ckw);
         const bool cq = Q4 && a.p[cs.p].Ws && 4 * cs.gl < a.p[cs.p].nWb;   // INT4 base blocks
-        for (int i = 0; i < n; i += 2) {
-            if (cq)
-                mma2_int4<MB>(acc, xa0, wb0);
-            else
-                mma2<MB>(acc, xa0, wb0);
-            issue(xa0, wb0);
-            if (i + 1 < n) {
-                if (cq)
-                    mma2_int4<MB>(acc, xa1, wb1);
-                else
-                    mma2<MB>(acc, xa1, wb1);
+        for (int i = 0; i < n; i += kDecStages) {
+#pragma unroll
+            for (int d = 0; d < kDecStages; ++d) {
+                if (d == 0 || i + d < n) {
+                    if (cq)
+                        mma2_int4<MB>(acc, xs[d], ws[d]);
+                    else
+                        mma2<MB>(acc, xs[d], ws[d]);
+                }
+                issue(xs[d], ws[d]);
             }
-            issue(xa1, wb1);
         }
         dec_flush<MB>(a, cs, acc, red, b);
         dec_next(a, n_act_v, se, cs);

@@ -322,6 +322,23 @@ hipError_t launch_pack_int4(const uint8_t* q, const uint16_t* scales, uint32_t* 
     return hipGetLastError();
 }
 
+// slot tables of consecutive adapter slots, written in stream order after
+// their slabs
+__global__ void set_slots_kernel(int* r8, float* scale, int* loaded, SlotBatch b) {
+    const int i = threadIdx.x;
+    if (i < b.n) {
+        r8[b.first + i] = b.r8[i];
+        scale[b.first + i] = b.scale[i];
+        loaded[b.first + i] = 1;
+    }
+}
+
+hipError_t launch_set_slots(int* r8, float* scale, int* loaded, const SlotBatch& b, hipStream_t s) {
+    if (b.n < 1 || b.n > kMaxSlotBatch) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(set_slots_kernel, dim3(1), dim3(64), 0, s, r8, scale, loaded, b);
+    return hipGetLastError();
+}
+
 // adapter: paper layout -> pool layout
 //   stage = [A_0 .. A_{S-1} | B_0 .. B_{S-1}],  A_s [K x r], B_s [r x n_s]
 //   dst_a = A^T_cat in fragment layout: row s*r8 + j of A^T_cat is column j

@@ -153,6 +153,14 @@ hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K,
                                int n_slices, const int* slice_out, int rank, int r8, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s);
+// rank and scale tables of up to kMaxSlotBatch consecutive slots (kernel argument)
+constexpr int kMaxSlotBatch = 64;
+struct SlotBatch {
+    int first, n;
+    int r8[kMaxSlotBatch];
+    float scale[kMaxSlotBatch];
+};
+hipError_t launch_set_slots(int* r8, float* scale, int* loaded, const SlotBatch& b, hipStream_t s);
 hipError_t launch_pack_int4(const uint8_t* q, const uint16_t* scales, uint32_t* dst_w, uint16_t* dst_s, int N,
                             int K, hipStream_t s);
 hipError_t launch_mlp_pack(const float* G, const float* U, uint16_t* dst, int T, int N, hipStream_t s);

@@ -25,7 +25,7 @@ def L():
 
 def _header_functions():
     text = open(os.path.join(ROOT, "include", "bdlora.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\s*\*)\s+(bdlora_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:int|int64_t|size_t|const char\s*\*)\s+(bdlora_\w+)\s*\(", text, re.M)))
 
 
 def test_exports_every_declared_function(L):
