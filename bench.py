@@ -78,8 +78,8 @@ def algorithmic_flops(spec, ids, ranks):
     return g, s
 
 
-KERNEL_SOURCES = ("bdl_prep.hip", "bdl_decode.hip", "bdl_kernels.hip", "bdl_device.h", "bdl_launch.h",
-                  "bdl_api.cpp")
+KERNEL_SOURCES = ("bdl_prep.hip", "bdl_decode.hip", "bdl_kernels.hip", "bdl_gemm.hip", "bdl_device.h",
+                  "bdl_launch.h", "bdl_api.cpp")
 
 
 def kernel_source_hash():
@@ -406,7 +406,10 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBS, 4)}
     else:
         names = ("prep", "shrink", "gemm")
-        dom, dom_name = 2, "bdl::gemm_kernel"
+        # the library's choice of base GEMM: the 256 x 256 LDS-staged kernel for
+        # bf16 weights above 256 tokens, the 64-row kernel otherwise
+        big = spec.T > 256 and spec.weight_format == "bf16"
+        dom, dom_name = 2, "bdl::gemm_big_kernel" if big else "bdl::gemm_kernel"
         achieved = g_flops / (k_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFS,
                 "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4)}

@@ -799,7 +799,14 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     });
     int n_loaded = 0;
     for (int v : P->h_loaded) n_loaded += v != 0;
+    // bf16 weights above one 256-row tile: the 256 x 256 LDS-staged kernel
+    // (its octet lists are those of 64-row blocks, as planned for T > 32);
+    // smaller batches have too few such tiles to occupy the chip
+    bool big = T > bdl::kBigM && MT == 64;
+    for (int i = 0; i < n; ++i) big = big && L.proj[projs[i]].wfmt == BDLORA_WEIGHT_BF16;
     const int tiles_m = (T + MT - 1) / MT;
+    const int tm = big ? (T + bdl::kBigM - 1) / bdl::kBigM : tiles_m;
+    const int tn = big ? bdl::kBigN : NT;
     int tile = 0, cch = 1;
     for (int q = 0; q < n; ++q) {
         const int i = order[q];
@@ -820,9 +827,9 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         for (int s = 0; s <= bdl::kMaxSlices; ++s) pl.slice_col[s] = pi.slice_col[s];
         pl.a_off = pi.a_off;
         pl.b_off = pi.b_off;
-        pl.tiles_n = (pi.N + NT - 1) / NT;
+        pl.tiles_n = (pi.N + tn - 1) / tn;
         pl.tile_base = tile;
-        tile += tiles_m * pl.tiles_n;
+        tile += tm * pl.tiles_n;
         cch = std::max(cch, (pi.S * L.r8max + nts - 1) / nts);
     }
     fa.n_proj = n;
@@ -839,7 +846,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.cchunks = cch;
     fa.tile_oct = P->d_tile_oct;
     fa.oct_cap = oct_cap(L, MT);
-    fa.tiles_m = tiles_m;
+    fa.tiles_m = tm;
     fa.total_tiles = tile;
     if (fa.items_bound > P->items_cap || (long long)tiles_m * fa.oct_cap > P->oct_elems)
         return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
@@ -872,7 +879,10 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     BDL_HIP(bdl::launch_shrink(fa, k.smb, k.snb, s));
     if (ev) BDL_HIP(hipEventRecord(ev[3], s));
     if (ev) BDL_HIP(hipEventRecord(ev[4], s));
-    BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
+    if (big)
+        BDL_HIP(bdl::launch_gemm_big(fa, s));
+    else
+        BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
     if (ev) BDL_HIP(hipEventRecord(ev[5], s));
     return BDLORA_OK;
 }

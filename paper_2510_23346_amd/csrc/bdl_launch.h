@@ -13,6 +13,7 @@ constexpr int kMaxSlices = 4;
 constexpr int kMaxSlots = 8192;
 constexpr int kMaxRank8 = 128;       // largest supported rank, rounded up to 8
 constexpr int kPlanLdsTokens = 4096; // plan keeps validated ids in LDS up to this batch size
+constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base GEMM (prefill)
 
 // One projection of a forward launch.
 struct ProjLaunch {
@@ -150,6 +151,7 @@ hipError_t launch_dec_epi(const DecArgs& a, hipStream_t s);
 hipError_t launch_prep(const PrepArgs& a, hipStream_t s);
 hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);
+hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s);
 hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K,
                                int n_slices, const int* slice_out, int rank, int r8, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s);

@@ -1,0 +1,80 @@
+"""GPU parity of the large-tile (256 x 256) prefill base GEMM with the fused
+expand, against the fp64 oracle.
+
+Batches above 256 tokens with bf16 base weights take that kernel.  The
+projections here are wider than one 256-column tile, with a ragged column
+tail, slice boundaries inside a tile, and more row tiles than one with a
+ragged row tail, so that the clamped edge blocks, the per-64-row octet lists
+and the slice lookup of the expand are all exercised.  Ranks go up to 64
+(eight octets per adapter) and a 64-row block holds many adapters, so the
+expand loop runs several passes.  Error rule as in test_gpu_parity.
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from workloads.gpu import DeviceLayer, device_to_float, load_adapters, make_pool
+from oracle import bdlora
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-2
+
+RANKS = [0, 1, 8, 16, 24, 33, 64, 5, 40, 12, 56, 32]
+
+
+def _projs():
+    return [
+        wl.ProjSpec("qkv", "column", 128, (272, 256, 16)),   # 544 columns: 3 tiles, slices cut tiles
+        wl.ProjSpec("o", "row", 160, (528,)),                 # 528 columns, K of 5 k-steps
+        wl.ProjSpec("up", "column", 96, (256,)),              # exactly one tile wide
+    ]
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_2510_23346_amd as bd
+    bd.lib()
+    return torch
+
+
+@pytest.mark.parametrize("T,kind", [(257, "uniform"), (520, "uniform"), (777, "segments")])
+def test_big_tile_parity(torch_cuda, T, kind):
+    torch = torch_cuda
+    rng = np.random.default_rng(1000 + T)
+    if kind == "segments":
+        # contiguous runs of one adapter, as in sorted prefill batches
+        cuts = np.sort(rng.choice(np.arange(1, T), size=9, replace=False))
+        ids = np.zeros(T, np.int64)
+        for i, (a, b) in enumerate(zip(np.r_[0, cuts], np.r_[cuts, T])):
+            ids[a:b] = rng.integers(-1, len(RANKS)) if i % 3 else i % len(RANKS)
+    else:
+        ids = rng.integers(-1, len(RANKS), size=T)
+    spec = wl.custom_workload(f"big-{T}", _projs(), T, RANKS,
+                              scales=[0.5 + 0.125 * i for i in range(len(RANKS))], ids=ids, seed=T)
+    layer = wl.draw_layer(spec, slots=range(len(RANKS)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(RANKS)), cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, dl.out, dl.ids)
+    torch.cuda.synchronize()
+    ys = dl.outputs()
+    ids_none = torch.full_like(dl.ids, -1)
+    base = [torch.empty_like(o) for o in dl.out]
+    pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, base, ids_none)
+    torch.cuda.synchronize()
+    yb = [device_to_float(o) for o in base]
+    refs = bdlora.layer_forward(layer)
+    for p, pi in enumerate(layer.projs):
+        rbase = pi.X.astype(np.float64) @ pi.W.astype(np.float64)
+        e = bdlora.rel_errors(ys[p], refs[p])
+        assert e["pointwise"] <= TOL, f"T={T} {pi.spec.name}: {e}"
+        assert bdlora.rel_errors(yb[p], rbase)["pointwise"] <= TOL, f"T={T} {pi.spec.name} base"
+        d = bdlora.delta_errors(ys[p], yb[p], refs[p], rbase)
+        assert d <= TOL, f"T={T} {pi.spec.name}: LoRA-term error {d}"
+        # rows without an adapter carry the base product only, bit for bit
+        none = np.asarray(ids) < 0
+        assert np.array_equal(ys[p][none], yb[p][none])
+    assert pool.device_error() == 0
+    pool.close()
