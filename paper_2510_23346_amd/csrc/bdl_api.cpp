@@ -803,7 +803,12 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     // (its octet lists are those of 64-row blocks, as planned for T > 32);
     // smaller batches have too few such tiles to occupy the chip
     bool big = T > bdl::kBigM && MT == 64;
-    for (int i = 0; i < n; ++i) big = big && L.proj[projs[i]].wfmt == BDLORA_WEIGHT_BF16;
+    for (int i = 0; i < n; ++i) {
+        // its buffer loads take 32-bit byte offsets into the packed X and W
+        const ProjInfo& pi = L.proj[projs[i]];
+        const long long xb = ((long long)T + 15) / 16 * 16 * pi.K * 2, wb = (long long)pi.N * pi.K * 2;
+        big = big && pi.wfmt == BDLORA_WEIGHT_BF16 && xb < (1LL << 31) && wb < (1LL << 31);
+    }
     const int tiles_m = (T + MT - 1) / MT;
     const int tm = big ? (T + bdl::kBigM - 1) / bdl::kBigM : tiles_m;
     const int tn = big ? bdl::kBigN : NT;

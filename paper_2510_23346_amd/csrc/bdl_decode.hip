@@ -30,9 +30,6 @@ namespace bdl {
 
 constexpr int kDecStages = 2;
 
-// word 3 of a raw buffer resource on gfx950 (32-bit untyped data)
-constexpr int kRawBufferWord3 = 0x00020000;
-
 // Position of projection p in the unit and group orders.  The column lists
 // hold act_max adapter positions (the host's bound on the number of adapters
 // a batch uses, so the schedule is known before the plan is); positions at

@@ -20,6 +20,9 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// word 3 of a raw buffer resource on gfx950 (32-bit untyped data)
+constexpr int kRawBufferWord3 = 0x00020000;
+
 constexpr int kWaves = 8;                 // waves per workgroup (split K)
 constexpr int kThreads = kWaves * 64;
 

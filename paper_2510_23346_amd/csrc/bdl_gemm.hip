@@ -5,7 +5,7 @@
 // their sum of Alg. 1 / Alg. 2 in one pass over the tile.  The operands are
 // the packed fragment layouts (1 KB per 16 rows x 32 k), so a k-step of the
 // tile is 16 activation and 16 weight fragments.  They go from global memory
-// straight into LDS (global_load_lds_dwordx4: lane l of a wave writes the
+// straight into LDS (buffer_load_dwordx4 ... lds: lane l of a wave writes the
 // 16 bytes at offset 16 l of the wave's 1 KB destination, which is exactly a
 // fragment), kBigStages k-steps deep, with one barrier per k-step.  Eight
 // waves, 4 row quarters x 2 column halves, each own a 64 x 128 sub-tile for
@@ -21,32 +21,36 @@
 // expand sees Z to about 16 bits).
 //
 // Tile order: projections heaviest first (set by the host), inside a
-// projection bands of kBigBand row tiles walked column by column, so that
-// the workgroups running at one time share activation rows and weight
-// columns.
+// projection bands of kBigBand row tiles walked column by column.
 #include "bdl_device.h"
 
 namespace bdl {
 
-constexpr int kBigThreads = 512;
 constexpr int kBigFrags = 32;                    // fragments per k-step: 16 X + 16 W
 constexpr int kBigStages = 4;                    // k-steps in LDS (32 KB each)
 constexpr int kBigBand = 4;                      // row tiles per band of the tile order
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// the LDS fragments one wave multiplies in one k-step
-struct BigFrags {
-    u32x4 x[4];   // activation row blocks 4 wr .. 4 wr + 3
-    u32x4 w[8];   // weight column blocks 8 wc .. 8 wc + 7
+// Where this thread's copies of a k-step come from: copies i < CP / 2 are
+// activation fragments, the others weight fragments (fragment w + NW i of
+// the k-step's 32), each a buffer load of 16 bytes per lane at byte offset
+// vo[i] + 1024 ks.  Buffer loads (not global ones) so that the compiler's
+// wait-count bookkeeping treats them as plain vector-memory operations and
+// keeps its LDS wait counts exact.
+template <int CP>
+struct BigSrc {
+    __amdgpu_buffer_rsrc_t rx, rw;
+    int vo[CP];   // this lane's byte offset at k-step 0
 };
 
-// issue the 4 fragment copies of this thread for one k-step into one stage
-__device__ __forceinline__ void big_issue(const uint16_t* const (&src)[4], size_t koff, u32x4* stage, int w) {
+// issue this thread's CP fragment copies of k-step ks into one stage
+template <int CP, int NW>
+__device__ __forceinline__ void big_issue(const BigSrc<CP>& s, int ks, u32x4* stage, int w) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        __builtin_amdgcn_global_load_lds(static_cast<const void*>(src[i] + koff),
-                                         (lds_void*)(stage + (w + 8 * i) * 64), 16, 0, 0);
+    for (int i = 0; i < CP; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(i < CP / 2 ? s.rx : s.rw, (lds_void*)(stage + (w + NW * i) * 64), 16,
+                                                 s.vo[i] + ks * 1024, 0, 0, 0);
 }
 
 // wait until at most n of this thread's copies (and none of its LDS reads)
@@ -58,17 +62,36 @@ __device__ __forceinline__ void big_issue(const uint16_t* const (&src)[4], size_
 // there, which costs nothing once satisfied).
 template <int n>
 __device__ __forceinline__ void big_wait_barrier() {
-    static_assert(n >= 0 && n < 16, "vmcnt field");
-    __builtin_amdgcn_s_waitcnt(n | (7 << 4));   // vmcnt(n) expcnt(7) lgkmcnt(0)
+    static_assert(n >= 0 && n < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4));   // vmcnt(n) expcnt(7) lgkmcnt(0)
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(n) : "memory");
 }
 
-__global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
+// wait until the k-step issued before the last `ahead` ones (0..3) is in LDS
+template <int CP>
+__device__ __forceinline__ void big_wait_ahead(int ahead) {
+    if (ahead >= 3)
+        big_wait_barrier<3 * CP>();
+    else if (ahead == 2)
+        big_wait_barrier<2 * CP>();
+    else if (ahead == 1)
+        big_wait_barrier<CP>();
+    else
+        big_wait_barrier<0>();
+}
+
+// RB = 16-row blocks per wave: 4 (eight waves, 4 x 2) or 8 (four waves, 2 x 2).
+template <int RB>
+__global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
+    constexpr int NWR = 16 / RB, NW = 2 * NWR;   // row waves, waves
+    constexpr int CP = kBigFrags / NW;           // fragment copies per thread and k-step
+    constexpr int NH = RB / 4;                   // 64-row blocks per wave
     __shared__ u32x4 lds[kBigStages * kBigFrags * 64];
     const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15, lg = l >> 4;
-    const int wr = w & 3, wc = w >> 2;           // rows 64 wr .., columns 128 wc .. of the tile
+    const int wr = w % NWR, wc = w / NWR;        // rows 16 RB wr .., columns 128 wc .. of the tile
 
     const int bid = blockIdx.x;
+    if (bid >= a.total_tiles) return;
     int p = 0;
 #pragma unroll
     for (int q = 1; q < kMaxProjs; ++q)
@@ -80,38 +103,41 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
     const int nt = off / bh, mt = band * kBigBand + (off - nt * bh);
     const int T = a.T, N = P.N, KS = P.K >> 5;
     const int nrb = (T + 15) >> 4, ncb = N >> 4;
-    const int rbase = mt * kBigM + wr * 64;      // first row of this wave
+    const int rbase = mt * kBigM + wr * 16 * RB; // first row of this wave
     const int c0 = nt * kBigN + wc * 128;        // first column of this wave
 
     // expand inputs that do not depend on the base product: fetched first.
-    // Octet lists are per 64-row block; a wave wholly past T has none.
-    const int* codes = a.tile_oct + (size_t)(mt * 4 + wr) * a.oct_cap;
-    int code = rbase < T ? codes[lg] : -1;
-    int rvid[4];
+    // Octet lists are per 64-row block; a block wholly past T has none.
+    int code[NH], rvid[RB];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
+    for (int h = 0; h < NH; ++h) {
+        const int* codes = a.tile_oct + (size_t)(mt * 4 + wr * NH + h) * a.oct_cap;
+        code[h] = rbase + 64 * h < T ? codes[lg] : -1;
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
         const int row = rbase + rb * 16 + lr;
         rvid[rb] = row < T ? a.vid[row] : -1;
     }
 
-    // staging: this thread copies lane l of fragments w + 8 i (i = 0..3) of
-    // every k-step; fragments 0..15 are the tile's activation row blocks,
-    // 16..31 its weight column blocks (blocks past the edge are clamped, their
-    // results are never stored)
-    const uint16_t* src[4];
+    // staging: fragments 0..15 of a k-step are the tile's activation row
+    // blocks, 16..31 its weight column blocks (blocks past the edge are
+    // clamped, their results are never stored)
+    BigSrc<CP> src;
+    src.rx = __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
+    src.rw = __builtin_amdgcn_make_buffer_rsrc((void*)P.W, 0, ncb * KS * 1024, kRawBufferWord3);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int f = w + 8 * i;
-        src[i] = (f < 16 ? P.Xp + frag_index(min(mt * 16 + f, nrb - 1), 0, KS)
-                         : P.W + frag_index(min(nt * 16 + f - 16, ncb - 1), 0, KS)) + l * 8;
+    for (int i = 0; i < CP; ++i) {
+        const int f = w + NW * i;
+        src.vo[i] = (i < CP / 2 ? min(mt * 16 + f, nrb - 1) : min(nt * 16 + f - 16, ncb - 1)) * KS * 1024 + l * 16;
     }
 #pragma unroll
     for (int d = 0; d < kBigStages - 1; ++d)
-        if (d < KS) big_issue(src, (size_t)d * kFrag, lds + d * kBigFrags * 64, w);
+        if (d < KS) big_issue<CP, NW>(src, d, lds + d * kBigFrags * 64, w);
 
-    f32x4 acc[4][8];
+    f32x4 acc[RB][8];
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -122,32 +148,33 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
     // the next k-step.  The barrier between the halves makes the next k-step
     // visible; the copies issued right after it refill the stage of k-step
     // ks - 1, whose LDS reads every wave finished before the previous barrier.
-    static_assert(kBigStages == 4, "the waits below are written for four stages");
+    static_assert(kBigStages >= 3 && kBigStages <= 5, "big_wait_ahead covers up to three k-steps in flight");
     auto stage = [&](int step) __attribute__((always_inline)) {
         return lds + (step % kBigStages) * kBigFrags * 64;
     };
-    auto read_x = [&](u32x4 (&x)[4], int step) __attribute__((always_inline)) {
+    auto read_x = [&](u32x4 (&x)[RB], int step) __attribute__((always_inline)) {
         const u32x4* S0 = stage(step);
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb) x[rb] = S0[(wr * 4 + rb) * 64 + l];
+        for (int rb = 0; rb < RB; ++rb) x[rb] = S0[(wr * RB + rb) * 64 + l];
     };
     auto read_w = [&](u32x4 (&wv)[4], int step, int half) __attribute__((always_inline)) {
         const u32x4* S0 = stage(step);
 #pragma unroll
         for (int c = 0; c < 4; ++c) wv[c] = S0[(16 + wc * 8 + 4 * half + c) * 64 + l];
     };
-    auto mma = [&](const u32x4 (&x)[4], const u32x4 (&wv)[4], int half) __attribute__((always_inline)) {
+    auto mma = [&](const u32x4 (&x)[RB], const u32x4 (&wv)[4], int half) __attribute__((always_inline)) {
 #pragma unroll
-        for (int rb = 0; rb < 4; ++rb)
+        for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int c = 0; c < 4; ++c)
                 acc[rb][4 * half + c] = mfma(wv[c], x[rb], acc[rb][4 * half + c]);
     };
-    u32x4 xa[4], xb[4], w0[4], w1[4];
-    // k-step ks < KS - 1 (x holds its activations, w0 its first-half weights)
+    u32x4 xa[RB], xb[RB], w0[4], w1[4];
+    // k-step ks < KS - 1 (x holds its activations, w0 its first-half
+    // weights; the next k-step's activations arrive in xn)
     // (the scheduling groups pin the reads ahead of the MFMAs they overlap:
     // masks 0x100 = LDS read, 0x008 = MFMA)
-    auto k_step = [&](int ks, const u32x4 (&x)[4], u32x4 (&xn)[4]) __attribute__((always_inline)) {
+    auto k_step = [&](int ks, const u32x4 (&x)[RB], u32x4 (&xn)[RB]) __attribute__((always_inline)) {
         read_w(w1, ks, 1);
         mma(x, w0, 0);
 #pragma unroll
@@ -155,32 +182,26 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 12, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * RB - 4, 0);
         __builtin_amdgcn_sched_barrier(0);
-        // k-step ks + 1 is complete once at most the copies of ks + 2 are in flight
-        if (ks + 2 < KS)
-            big_wait_barrier<4>();
-        else
-            big_wait_barrier<0>();
+        // k-step ks + 1 is complete once at most the copies issued after it
+        // (k-steps ks + 2 .. ks + kBigStages - 2 below KS) are in flight
+        big_wait_ahead<CP>(min(kBigStages - 3, KS - 2 - ks));
         const int nx = ks + kBigStages - 1;
-        if (nx < KS) big_issue(src, (size_t)nx * kFrag, stage(nx), w);
+        if (nx < KS) big_issue<CP, NW>(src, nx, stage(nx), w);
         read_x(xn, ks + 1);
         read_w(w0, ks + 1, 0);
         mma(x, w1, 1);
+        // RB + 4 reads spread over the 4 RB MFMAs
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
+        for (int i = 0; i < RB + 4; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, (4 * RB) / (RB + 4) > 0 ? (4 * RB) / (RB + 4) : 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
     };
-    // k-step 0 is complete once at most the copies of k-steps 1 and 2 are in flight
-    if (KS >= 3)
-        big_wait_barrier<8>();
-    else if (KS == 2)
-        big_wait_barrier<4>();
-    else
-        big_wait_barrier<0>();
+    // k-step 0 is complete once at most the copies of k-steps 1 .. kBigStages - 2 are in flight
+    big_wait_ahead<CP>(min(kBigStages - 2, KS - 1));
     read_x(xa, 0);
     read_w(w0, 0, 0);
     int ks = 0;
@@ -191,12 +212,12 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
     // one or two k-steps left; the last one reads nothing ahead
     const bool two = ks + 1 < KS;
     if (two) k_step(ks, xa, xb);
-    const u32x4 (&xl)[4] = two ? xb : xa;
+    const u32x4 (&xl)[RB] = two ? xb : xa;
     read_w(w1, KS - 1, 1);
     mma(xl, w0, 0);
     mma(xl, w1, 1);
 
-    // expand: acc += Zhat B over the octets of this wave's 64 rows
+    // expand: acc += Zhat B over the octets of each 64-row block of the wave
     int sig[8];
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
@@ -208,43 +229,49 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
         sig[cb] = sgm;
     }
     const u32x4 zero4 = u32x4{0u, 0u, 0u, 0u};
-    for (int e = 0;;) {
-        if (!__any(code >= 0)) break;
-        const int slot = code >> 12, r8s = (code >> 4) & 0xff, j0 = (code & 15) * 8;
-        u32x4 bv[8];
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb) {
-            const int col = min(c0 + cb * 16 + lr, N - 1);
-            bv[cb] = code >= 0 ? ld16(a.pool + (size_t)slot * a.slot_stride + P.b_off + (size_t)col * r8s + j0)
-                               : zero4;
-        }
-        u32x4 zh[4], zl[4];
+    for (int h = 0; h < NH; ++h) {
+        const int* codes = a.tile_oct + (size_t)(mt * 4 + wr * NH + h) * a.oct_cap;
+        int cd = code[h];
+        for (int e = 0;;) {
+            if (!__any(cd >= 0)) break;
+            const int slot = cd >> 12, r8s = (cd >> 4) & 0xff, j0 = (cd & 15) * 8;
+            u32x4 bv[8];
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb) {
-            if (cb == 0 || sig[cb] != sig[cb - 1]) {
+            for (int cb = 0; cb < 8; ++cb) {
+                const int col = min(c0 + cb * 16 + lr, N - 1);
+                bv[cb] = cd >= 0 ? ld16(a.pool + (size_t)slot * a.slot_stride + P.b_off + (size_t)col * r8s + j0)
+                                 : zero4;
+            }
+            u32x4 zh[4], zl[4];
+#pragma unroll
+            for (int cb = 0; cb < 8; ++cb) {
+                if (cb == 0 || sig[cb] != sig[cb - 1]) {
+#pragma unroll
+                    for (int rb = 0; rb < 4; ++rb) {
+                        const bool match = cd >= 0 && rvid[4 * h + rb] == slot;
+                        const uint16_t* zp =
+                            P.Z + (size_t)(rbase + 64 * h + rb * 16 + lr) * P.zs + sig[cb] * a.r8max + j0;
+                        zh[rb] = match ? ld16(zp) : zero4;
+                        zl[rb] = match ? ld16(zp + P.zplane) : zero4;
+                    }
+                }
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) {
-                    const bool match = code >= 0 && rvid[rb] == slot;
-                    const uint16_t* zp = P.Z + (size_t)(rbase + rb * 16 + lr) * P.zs + sig[cb] * a.r8max + j0;
-                    zh[rb] = match ? ld16(zp) : zero4;
-                    zl[rb] = match ? ld16(zp + P.zplane) : zero4;
+                    acc[4 * h + rb][cb] = mfma(bv[cb], zh[rb], acc[4 * h + rb][cb]);
+                    acc[4 * h + rb][cb] = mfma(bv[cb], zl[rb], acc[4 * h + rb][cb]);
                 }
             }
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                acc[rb][cb] = mfma(bv[cb], zh[rb], acc[rb][cb]);
-                acc[rb][cb] = mfma(bv[cb], zl[rb], acc[rb][cb]);
-            }
+            e += 4;
+            if (e + 4 > a.oct_cap) break;
+            cd = codes[e + lg];
         }
-        e += 4;
-        if (e + 4 > a.oct_cap) break;
-        code = codes[e + lg];
     }
 
     // store: lane (lr, lg) of block (rb, cb) holds row rbase + 16 rb + lr,
     // columns c0 + 16 cb + 4 lg + i
 #pragma unroll
-    for (int rb = 0; rb < 4; ++rb) {
+    for (int rb = 0; rb < RB; ++rb) {
         const int row = rbase + rb * 16 + lr;
         if (row >= T) continue;
 #pragma unroll
@@ -263,9 +290,12 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(FwdArgs a) {
     }
 }
 
+// wave tile height of the launch: 4 row blocks (eight waves of 64 x 128)
+constexpr int kBigRB = 4;
+
 hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s) {
     if (a.total_tiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(gemm_big_kernel, dim3(a.total_tiles), dim3(kBigThreads), 0, s, a);
+    hipLaunchKernelGGL(gemm_big_kernel<kBigRB>, dim3(a.total_tiles), dim3(128 * (16 / kBigRB)), 0, s, a);
     return hipGetLastError();
 }
 
