@@ -13,8 +13,8 @@
 //                     blocks form groups of 4, and workgroup b takes the
 //                     k-steps whose first unit lies in [b U / G, (b+1) U / G),
 //                     so all G workgroups stream the same number of bytes.
-//                     Workgroups are 8 waves: 2 column halves x 4 quarters of
-//                     the k-range.
+//                     Workgroups are 4 waves that split the group's
+//                     blocks and the k-range (see dec_flush).
 //                     Each (group, workgroup) pair writes one fp32 partial
 //                     tile to slot g + b (injective: along the unit order both
 //                     indices only grow).
@@ -118,12 +118,12 @@ __device__ __forceinline__ void dec_next(const DecArgs& a, int n_act_v, unsigned
     dec_cut(a, n_act_v, se, g);
 }
 
-// The k-steps of a segment that wave (column half cg, quarter kq) handles:
-// [*kw, *kw + items), none when the column half has no block in the group.
-__device__ __forceinline__ int dec_items(const DecSeg& g, int cg, int kq, int* kw) {
-    const int n = g.k1 - g.k0, q = n >> 2, r = n & 3;
+// The k-steps of a segment that K-part kq of NKQ handles: [*kw, *kw + items).
+template <int NKQ>
+__device__ __forceinline__ int dec_items(const DecSeg& g, int kq, int* kw) {
+    const int n = g.k1 - g.k0, q = n / NKQ, r = n - q * NKQ;
     *kw = g.k0 + kq * q + min(kq, r);
-    return 2 * cg < g.wdt ? q + (kq < r ? 1 : 0) : 0;
+    return q + (kq < r ? 1 : 0);
 }
 
 // element pointer of k-step 0 of virtual block vb of projection P; lane i of
@@ -137,41 +137,46 @@ __device__ __forceinline__ const uint16_t* dec_block(const DecArgs& a, const Dec
     return a.pool + (size_t)slot * a.slot_stride + P.a_off + frag_index(c, 0, KS);
 }
 
-// Eight waves as 2 column halves x 4 K-quarters: wave w owns blocks
-// 2 (w & 1) and 2 (w & 1) + 1 of the group, over the (w >> 1)-th quarter of
-// the segment's k-range.  At the end of a segment the four quarters meet in
-// LDS; all 512 threads add them in a fixed order and store the group's fp32
-// partial (rows < T, the group's wdt blocks) as 16-byte chunks.
+// Four waves per workgroup as 4 / NB column groups x NB parts of the
+// segment's k-range; a wave takes NB of the group's 4 blocks (4 for bf16
+// weights, 2 in launches with an INT4 base, whose unpacking needs the
+// registers): per k-step it loads MB activation fragments and NB weight
+// fragments and issues NB MB MFMAs, so every activation fragment it loads
+// serves NB blocks.  At the end of a segment the K-parts meet in LDS; all
+// 256 threads add them in a fixed order and store the group's fp32 partial
+// (rows < T, the group's wdt blocks) as 16-byte chunks.
+constexpr int kDecWaves = 4;
+constexpr int kDecThreads = 64 * kDecWaves;
 constexpr int kRedLd = 68;    // LDS row stride (floats): 4 rows apart land 16 banks apart
 
-template <int MB>
-__device__ __forceinline__ void dec_flush(const DecArgs& a, const DecSeg& g, f32x4 (&acc)[MB][2], float* red, int b) {
-    constexpr int REG = MB * 16 * kRedLd;
-    const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1, kq = w >> 1;
+template <int MB, int NB>
+__device__ __forceinline__ void dec_flush(const DecArgs& a, const DecSeg& g, f32x4 (&acc)[MB][NB], float* red, int b) {
+    constexpr int REG = MB * 16 * kRedLd, NCG = 4 / NB, NKQ = kDecWaves / NCG;
+    const int w = wave_id(), l = threadIdx.x & 63, cg = w % NCG, kq = w / NCG;
     __syncthreads();                          // the previous segment's readers are done
-    if (2 * cg < g.wdt) {
-        float* reg = red + kq * REG + cg * 32 + (l & 15);
+    float* reg = red + kq * REG + cg * NB * 16 + (l & 15);
 #pragma unroll
-        for (int rb = 0; rb < MB; ++rb)
+    for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
+        for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) reg[(rb * 16 + 4 * (l >> 4) + i) * kRedLd + cb * 16] = acc[rb][cb][i];
-    }
+            for (int i = 0; i < 4; ++i) reg[(rb * 16 + 4 * (l >> 4) + i) * kRedLd + cb * 16] = acc[rb][cb][i];
 #pragma unroll
-    for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
     __syncthreads();
     float* dst = a.part + (size_t)min(g.pp.gb + g.gl + b, a.part_slots - 1) * kPartElems;
     const int nc4 = g.wdt * 4;
 #pragma unroll
-    for (int j = 0; j < (MB * 16 * 16 + kThreads - 1) / kThreads; ++j) {
-        const int c = threadIdx.x + j * kThreads;
+    for (int j = 0; j < MB; ++j) {
+        const int c = threadIdx.x + j * kDecThreads;   // MB * 16 rows x 16 four-column chunks
         const int row = c >> 4, c4 = c & 15;
-        if (c < MB * 16 * 16 && row < a.T && c4 < nc4) {
+        if (row < a.T && c4 < nc4) {
             const float* src = red + row * kRedLd + c4 * 4;
             float4 v = *reinterpret_cast<const float4*>(src);
 #pragma unroll
-            for (int k = 1; k < 4; ++k) {
+            for (int k = 1; k < NKQ; ++k) {
                 const float4 u = *reinterpret_cast<const float4*>(src + k * REG);
                 v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
             }
@@ -180,33 +185,43 @@ __device__ __forceinline__ void dec_flush(const DecArgs& a, const DecSeg& g, f32
     }
 }
 
-// The workgroup's segments run through one load pipeline of kDecStages k-steps per
-// wave: a load cursor walks the wave's k-steps segment after segment that many
-// k-steps ahead of the compute loop, so the loads of the next segment are in
-// flight while the current one is reduced and stored.  Loads are
-// unconditional (past the last k-step they repeat it), which keeps each
-// load's only consumer one pipeline turn later.
-template <int MB>
-__device__ __forceinline__ void mma2(f32x4 (&acc)[MB][2], const u32x4 (&xa)[MB], const u32x4 (&wb)[2]) {
+template <int MB, int NB>
+__device__ __forceinline__ void mma_nb(f32x4 (&acc)[MB][NB], const u32x4 (&xa)[MB], const u32x4 (&wb)[NB]) {
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = mfma(xa[rb], wb[cb], acc[rb][cb]);
+        for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = mfma(xa[rb], wb[cb], acc[rb][cb]);
 }
 
 // INT4 base blocks: wb[cb].x holds the lane's word, wb[cb].y the scale bits
-template <int MB>
-__device__ __forceinline__ void mma2_int4(f32x4 (&acc)[MB][2], const u32x4 (&xa)[MB], const u32x4 (&wb)[2]) {
-    const uint32_t q[2] = {wb[0].x, wb[1].x}, sc[2] = {wb[0].y, wb[1].y};
-    mma_int4_kstep<MB, 2>(acc, xa, q, sc);
+template <int MB, int NB>
+__device__ __forceinline__ void mma_nb_int4(f32x4 (&acc)[MB][NB], const u32x4 (&xa)[MB], const u32x4 (&wb)[NB]) {
+    uint32_t q[NB], sc[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+        q[cb] = wb[cb].x;
+        sc[cb] = wb[cb].y;
+    }
+    mma_int4_kstep<MB, NB>(acc, xa, q, sc);
 }
 
+// The workgroup's segments run through one load pipeline of kDecStages
+// k-steps per wave: a load cursor walks the wave's k-steps segment after
+// segment that many k-steps ahead of the compute loop, so the loads of the
+// next segment are in flight while the current one is reduced and stored.
+// Each segment's k-steps are padded to a multiple of kDecStages (the padding
+// repeats the last load), so every segment starts on the first stage and
+// each load's only consumer is one pipeline turn later.  Operand bases are
+// wave-uniform (scalar registers); per k-step only the lanes' byte offset
+// moves, so the steady state costs one vector add per k-step.
+//
 // Q4: some projection of the launch has an INT4 base (the kernel then handles
 // both operand types; without it the INT4 code is compiled out).
 template <int MB, bool Q4>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) void dec_main_kernel(DecArgs a) {
-    __shared__ float red[4 * MB * 16 * kRedLd];
-    const int w = wave_id(), l = threadIdx.x & 63, cg = w & 1, kq = w >> 1;
+__global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))) void dec_main_kernel(DecArgs a) {
+    constexpr int NB = Q4 ? 2 : 4, NCG = 4 / NB, NKQ = kDecWaves / NCG;
+    __shared__ float red[NKQ * MB * 16 * kRedLd];
+    const int w = wave_id(), l = threadIdx.x & 63, cg = w % NCG, kq = w / NCG;
     const int G = gridDim.x, b = blockIdx.x;
     const unsigned U = a.units;               // the host launches with U >= 4 G
     const unsigned sb = (unsigned)b * U / (unsigned)G, se = (unsigned)(b + 1) * U / (unsigned)G;
@@ -220,85 +235,112 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4))) v
     DecSeg cs = dec_first(a, n_act_v, sb, se);
     if (!cs.valid) return;
 
-    // load cursor: segment, this wave's k-steps in it (padded to a multiple
-    // of kDecStages, so every segment starts on the first stage), the next one,
-    // operand bases (uniform; each lane adds its 16-byte offset)
+    // load cursor: segment, this wave's first k-step and load count in it
+    // (padded), loads left; operand bases (uniform)
     DecSeg ls = cs;
-    int lkw, litems = dec_items(ls, cg, kq, &lkw), li = 0, lk = ls.k0;
-    const uint16_t* ap[MB];
-    // the two blocks' bases (bytes) and, for INT4 base blocks, their scales
-    const char *bp0 = nullptr, *bp1 = nullptr;
-    const uint16_t *sp0 = nullptr, *sp1 = nullptr;
+    int lkw = 0, lrem = 0, lk = 0, llast = 0;
+    const char* xb[MB];                       // activation row blocks (bytes, k-step 0)
+    const char* wbp[NB];                      // this wave's blocks (bytes, k-step 0)
+    const char* sbp[NB];                      // INT4 blocks: their scales (bytes, group 0)
     bool lq = false;                          // the loader's segment streams INT4 base blocks
-    const unsigned lo = (unsigned)l * 16u;
+#pragma unroll
+    for (int c = 0; c < NB; ++c) wbp[c] = sbp[c] = nullptr;
+#pragma unroll
+    for (int rb = 0; rb < MB; ++rb) xb[rb] = nullptr;
     auto point = [&]() __attribute__((always_inline)) {
         const DecProj& P = a.p[ls.p];
+        const int KS = ls.pp.KS;
 #pragma unroll
-        for (int rb = 0; rb < MB; ++rb) ap[rb] = P.Xp + frag_index(rb, 0, ls.pp.KS);
+        for (int rb = 0; rb < MB; ++rb) xb[rb] = reinterpret_cast<const char*>(P.Xp + frag_index(rb, 0, KS));
         lq = Q4 && P.Ws && 4 * ls.gl < P.nWb;
-        const int vb0 = 4 * ls.gl + min(2 * cg, ls.wdt - 1), vb1 = 4 * ls.gl + min(2 * cg + 1, ls.wdt - 1);
-        // both candidates are formed and one is selected (no branch: the
-        // bases stay in registers)
-        const char* wq = reinterpret_cast<const char*>(P.W);
-        const size_t qs = (size_t)ls.pp.KS * kInt4FragBytes, ss = (size_t)(ls.pp.KS / kInt4Group) * 16;
-        bp0 = lq ? wq + vb0 * qs : reinterpret_cast<const char*>(dec_block(a, P, vb0, ls.pp.KS, gs, n_act_v));
-        bp1 = lq ? wq + vb1 * qs : reinterpret_cast<const char*>(dec_block(a, P, vb1, ls.pp.KS, gs, n_act_v));
-        sp0 = lq ? P.Ws + vb0 * ss : P.Ws;
-        sp1 = lq ? P.Ws + vb1 * ss : P.Ws;
-        lk = ls.k0;                           // a k-step these bases may load
+        const size_t qs = (size_t)KS * kInt4FragBytes, ss = (size_t)(KS / kInt4Group) * 32;
+#pragma unroll
+        for (int c = 0; c < NB; ++c) {
+            const int vb = 4 * ls.gl + min(cg * NB + c, ls.wdt - 1);
+            // both candidates are formed and one is selected (no branch: the
+            // bases stay in registers)
+            const char* wq = reinterpret_cast<const char*>(P.W) + vb * qs;
+            const char* wf = reinterpret_cast<const char*>(dec_block(a, P, vb, KS, gs, n_act_v));
+            wbp[c] = lq ? wq : wf;
+            sbp[c] = lq ? reinterpret_cast<const char*>(P.Ws) + vb * ss : reinterpret_cast<const char*>(P.Ws);
+        }
     };
-    point();
-    auto issue = [&](u32x4 (&xa)[MB], u32x4 (&wb)[2]) __attribute__((always_inline)) {
-        while (ls.valid && li >= (litems + kDecStages - 1) / kDecStages * kDecStages) {
+    // Move the cursor to the next segment in which this wave has k-steps.
+    // The bases and [lk, llast] always describe k-steps of a valid segment:
+    // past the last segment the cursor stays on the last one it pointed at,
+    // so the loads that fill the pipeline's tail repeat a valid address.
+    auto advance = [&]() __attribute__((always_inline)) {
+        while (lrem == 0) {
             dec_next(a, n_act_v, se, ls);
-            if (ls.valid) {
-                litems = dec_items(ls, cg, kq, &lkw);
-                li = 0;
+            if (!ls.valid) return;
+            const int n = dec_items<NKQ>(ls, kq, &lkw);
+            if (n > 0) {
+                lrem = (n + kDecStages - 1) / kDecStages * kDecStages;
+                lk = lkw;
+                llast = lkw + n - 1;
                 point();
             }
         }
-        if (ls.valid) {
-            if (li < litems) lk = lkw + li;   // else the padding slot repeats the last load
-            ++li;
+    };
+    {
+        // the first segment is valid (k1 > k0); a wave without k-steps in it
+        // still points at it (k-step k0) before looking further
+        const int n = dec_items<NKQ>(ls, kq, &lkw);
+        point();
+        lrem = (n + kDecStages - 1) / kDecStages * kDecStages;
+        lk = n > 0 ? lkw : ls.k0;
+        llast = n > 0 ? lkw + n - 1 : ls.k0;
+        if (lrem == 0) advance();
+    }
+    const unsigned lo16 = (unsigned)l * 16u, lo4 = (unsigned)l * 4u, lsc = (unsigned)(l & 15) * 2u;
+    auto issue = [&](u32x4 (&xa)[MB], u32x4 (&wb)[NB]) __attribute__((always_inline)) {
+        if (lrem == 0 && ls.valid) advance();
+        const int kk = min(lk, llast);        // padding (and the end) repeats the last load
+        if (ls.valid && lrem > 0) {
+            ++lk;
+            --lrem;
         }
-        if (lq) {
-            const size_t qo = (size_t)lk * kInt4FragBytes + (lo >> 2);
-            const int so = (lk / kInt4Group) * 16 + (l & 15);
-            wb[0] = u32x4{*reinterpret_cast<const uint32_t*>(bp0 + qo), sp0[so], 0u, 0u};
-            wb[1] = u32x4{*reinterpret_cast<const uint32_t*>(bp1 + qo), sp1[so], 0u, 0u};
-        } else {
-            const size_t fo = (size_t)lk * kFrag * 2 + lo;
-            wb[0] = *reinterpret_cast<const u32x4*>(bp0 + fo);
-            wb[1] = *reinterpret_cast<const u32x4*>(bp1 + fo);
-        }
+        if (Q4 && lq) {
+            const unsigned qo = (unsigned)kk * kInt4FragBytes + lo4, so = (unsigned)(kk / kInt4Group) * 32u + lsc;
 #pragma unroll
-        for (int rb = 0; rb < MB; ++rb)
-            xa[rb] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(ap[rb] + (size_t)lk * kFrag) + lo);
+            for (int c = 0; c < NB; ++c)
+                wb[c] = u32x4{*reinterpret_cast<const uint32_t*>(wbp[c] + qo),
+                              (uint32_t)*reinterpret_cast<const uint16_t*>(sbp[c] + so), 0u, 0u};
+        } else {
+            const unsigned fo = (unsigned)kk * 1024u + lo16;
+#pragma unroll
+            for (int c = 0; c < NB; ++c) wb[c] = *reinterpret_cast<const u32x4*>(wbp[c] + fo);
+        }
+        const unsigned xo = (unsigned)kk * 1024u + lo16;
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb) xa[rb] = *reinterpret_cast<const u32x4*>(xb[rb] + xo);
     };
 
-    u32x4 xs[kDecStages][MB], ws[kDecStages][2];
+    u32x4 xs[kDecStages][MB], ws[kDecStages][NB];
 #pragma unroll
     for (int d = 0; d < kDecStages; ++d) issue(xs[d], ws[d]);
-    f32x4 acc[MB][2];
+    f32x4 acc[MB][NB];
 #pragma unroll
-    for (int rb = 0; rb < MB; ++rb) acc[rb][0] = acc[rb][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (;;) {
         int ckw;
-        const int n = dec_items(cs, cg, kq, &ckw);
+        const int n = dec_items<NKQ>(cs, kq, &ckw);
         const bool cq = Q4 && a.p[cs.p].Ws && 4 * cs.gl < a.p[cs.p].nWb;   // INT4 base blocks
         for (int i = 0; i < n; i += kDecStages) {
 #pragma unroll
             for (int d = 0; d < kDecStages; ++d) {
-                if (d == 0 || i + d < n) {
-                    if (cq)
-                        mma2_int4<MB>(acc, xs[d], ws[d]);
+                if (i + d < n) {
+                    if (Q4 && cq)
+                        mma_nb_int4<MB, NB>(acc, xs[d], ws[d]);
                     else
-                        mma2<MB>(acc, xs[d], ws[d]);
+                        mma_nb<MB, NB>(acc, xs[d], ws[d]);
                 }
                 issue(xs[d], ws[d]);
             }
         }
-        dec_flush<MB>(a, cs, acc, red, b);
+        dec_flush<MB, NB>(a, cs, acc, red, b);
         dec_next(a, n_act_v, se, cs);
         if (!cs.valid) break;
     }
@@ -312,9 +354,9 @@ hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s) {
 #define BDL_DEC_CASE(M)                                                                                  \
     case M:                                                                                              \
         if (q4)                                                                                          \
-            hipLaunchKernelGGL((dec_main_kernel<M, true>), dim3(grid), dim3(kThreads), 0, s, a);         \
+            hipLaunchKernelGGL((dec_main_kernel<M, true>), dim3(grid), dim3(kDecThreads), 0, s, a);      \
         else                                                                                             \
-            hipLaunchKernelGGL((dec_main_kernel<M, false>), dim3(grid), dim3(kThreads), 0, s, a);        \
+            hipLaunchKernelGGL((dec_main_kernel<M, false>), dim3(grid), dim3(kDecThreads), 0, s, a);     \
         break;
     switch (mb) {
         BDL_DEC_CASE(1)
