@@ -528,7 +528,11 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 // intermediate H = out_0 (act none) or silu(out_0) * out_1 (act silu_mul,
 // projection 1 being up), stored in bf16 in the fragment layout the second
 // projection reads (rows = tokens, k = these columns).
-__global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
+// Epilogue workgroups: kEpiTok tokens x 8 column octets of one 64-column tile.
+constexpr int kEpiTok = 32;
+constexpr int kEpiThreads = kEpiTok * 8;
+
+__global__ __launch_bounds__(kEpiThreads) void dec_epi_kernel(DecArgs a) {
     const int tile = blockIdx.x;
     int p = 0;
 #pragma unroll
@@ -536,7 +540,7 @@ __global__ __launch_bounds__(kThreads) void dec_epi_kernel(DecArgs a) {
         if (q < a.n_proj && tile >= a.stb[q]) p = q;
     const DecProj& P = a.p[p];
     const int n = tile - a.stb[p];
-    const int t = threadIdx.x >> 3;
+    const int t = blockIdx.y * kEpiTok + (threadIdx.x >> 3);
     const int col = n * 64 + (threadIdx.x & 7) * 8;
     // threads past the last token or column compute on clamped indices and
     // store nothing (no early exit: every load is issued without waiting on
@@ -566,7 +570,7 @@ hipError_t launch_dec_epi(const DecArgs& a, hipStream_t s) {
     if (a.T > kDecodeMaxT || a.main_grid <= 0) return hipErrorInvalidValue;
     if (a.mlp_act >= 0 && (!a.h_dst || (a.mlp_act == BDLORA_ACT_SILU_MUL && (a.n_proj != 2 || a.p[1].N != a.p[0].N))))
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL(dec_epi_kernel, dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(dec_epi_kernel, dim3(grid, (a.T + kEpiTok - 1) / kEpiTok), dim3(kEpiThreads), 0, s, a);
     return hipGetLastError();
 }
 
