@@ -12,7 +12,7 @@ constexpr int kMaxProjs = 8;
 constexpr int kMaxSlices = 4;
 constexpr int kMaxSlots = 8192;
 constexpr int kMaxRank8 = 128;       // largest supported rank, rounded up to 8
-constexpr int kPlanLdsTokens = 4096; // plan keeps validated ids in LDS up to this batch size
+constexpr int kPlanLdsTokens = 8192; // plan keeps validated ids in LDS up to this batch size
 constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base GEMM (prefill)
 
 // One projection of a forward launch.

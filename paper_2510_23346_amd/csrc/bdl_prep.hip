@@ -114,25 +114,44 @@ __device__ void decode_plan(const PrepArgs& a) {
 }
 
 // activations -> fragment layout (all workgroups but 0)
+// Each wave packs PER consecutive fragments per turn (consecutive k-steps of
+// a row block, so a row's PER x 64 bytes are contiguous), all loads before
+// the stores.  Large batches take 4 (fewer, longer streams); small ones 1
+// (more waves issue their single load at once).
+constexpr int kPackWide = 4;
+constexpr int kPackWideFrags = 32768;   // total fragments from which the wide form is used
+
+template <int PER>
 __device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
     const int l = threadIdx.x & 63;
-    for (int f = blk * 16 + (threadIdx.x >> 6); f < a.total_frags; f += nblk * 16) {
-        int j = 0;
-        while (j + 1 < a.n_jobs && f >= a.jobs[j + 1].frag_base) ++j;
-        const PackJob& J = a.jobs[j];
-        const int KS = J.K >> 5;
-        const int local = f - J.frag_base;
-        const int rb = local / KS, ks = local - rb * KS;
-        const int row = rb * 16 + (l & 15);
-        u32x4 v = u32x4{0u, 0u, 0u, 0u};
-        if (row < J.rows) v = ld16(J.src + (size_t)row * J.K + ks * 32 + (l >> 4) * 8);
-        *reinterpret_cast<u32x4*>(J.dst + (size_t)local * kFrag + l * 8) = v;
+    for (int f0 = (blk * 16 + (threadIdx.x >> 6)) * PER; f0 < a.total_frags; f0 += nblk * 16 * PER) {
+        u32x4 v[PER];
+        uint16_t* dst[PER];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int f = min(f0 + i, a.total_frags - 1);
+            int j = 0;
+            while (j + 1 < a.n_jobs && f >= a.jobs[j + 1].frag_base) ++j;
+            const PackJob& J = a.jobs[j];
+            const int KS = J.K >> 5;
+            const int local = f - J.frag_base;
+            const int rb = local / KS, ks = local - rb * KS;
+            const int row = rb * 16 + (l & 15);
+            v[i] = row < J.rows ? ld16(J.src + (size_t)row * J.K + ks * 32 + (l >> 4) * 8) : u32x4{0u, 0u, 0u, 0u};
+            dst[i] = J.dst + (size_t)local * kFrag + l * 8;
+        }
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+            if (f0 + i < a.total_frags) *reinterpret_cast<u32x4*>(dst[i]) = v[i];
     }
 }
 
 __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     if (blockIdx.x > 0) {
-        pack_activations(a, blockIdx.x - 1, gridDim.x - 1);
+        if (a.total_frags >= kPackWideFrags)
+            pack_activations<kPackWide>(a, blockIdx.x - 1, gridDim.x - 1);
+        else
+            pack_activations<1>(a, blockIdx.x - 1, gridDim.x - 1);
         return;
     }
     if (a.decode_plan) {
@@ -159,15 +178,28 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     }
     if (tid == 0) s_err = 0;
     __syncthreads();
-    for (int t = tid; t < a.T; t += 1024) {
-        const int id = a.ids[t];
-        const bool ok = id >= 0 && id < a.max_slots && ldl[id] != 0;
-        if (!ok && id != -1) s_err = 1;
-        const int v = ok ? id : -1;
-        a.vid[t] = v;
-        a.tr8[t] = ok ? r8l[id] : 0;
-        if (in_lds) vid_l[t] = v;
-        if (ok) atomicAdd(&cnt[id], 1);
+    // ids in batches of 8 per thread: all loads of a batch are issued before
+    // any of its stores, so a batch costs one round trip
+    for (int t0 = 0; t0 < a.T; t0 += 8 * 1024) {
+        int idv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int t = t0 + j * 1024 + tid;
+            idv[j] = t < a.T ? a.ids[t] : -1;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int t = t0 + j * 1024 + tid;
+            if (t >= a.T) break;
+            const int id = idv[j];
+            const bool ok = id >= 0 && id < a.max_slots && ldl[id] != 0;
+            if (!ok && id != -1) s_err = 1;
+            const int v = ok ? id : -1;
+            a.vid[t] = v;
+            a.tr8[t] = ok ? r8l[id] : 0;
+            if (in_lds) vid_l[t] = v;
+            if (ok) atomicAdd(&cnt[id], 1);
+        }
     }
     __syncthreads();
 
@@ -290,7 +322,8 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
 }
 
 hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
-    int pack_blocks = (a.total_frags + 15) / 16;
+    const int per = a.total_frags >= kPackWideFrags ? kPackWide : 1;
+    int pack_blocks = (a.total_frags + 16 * per - 1) / (16 * per);
     if (pack_blocks > 1024) pack_blocks = 1024;
     const int nwords = (a.max_slots + 31) >> 5;
     const size_t lds = a.decode_plan ? 0 : 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
