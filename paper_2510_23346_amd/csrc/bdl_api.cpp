@@ -50,6 +50,7 @@ struct Layout {
     long long xp_elems[bdl::kMaxProjs];
     long long part_slots = 0;          // decode partial tiles
     long long mlp_elems = 0;           // prefill MLP: gate and up outputs, fp32
+    long long bigpart_elems = 0;       // large-tile GEMM: fp32 partials of split tiles
 };
 
 // Validates the pool arguments and computes the memory layout.
@@ -131,6 +132,10 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
         if (L->proj[p].kind == BDLORA_COLUMN && L->proj[p].S == 1) max_n = std::max(max_n, L->proj[p].N);
     L->mlp_elems = 2LL * max_tokens * max_n;
     ws += L->mlp_elems * 4;
+    // fp32 partials of the large-tile GEMM's split tiles (pools for batches
+    // above the decode size)
+    L->bigpart_elems = max_tokens > bdl::kDecodeMaxT ? (long long)bdl::kBigPartSlots * bdl::kBigPartElems : 0;
+    ws += L->bigpart_elems * 4;
     ws += max_slots * 12LL;                                       // slot tables
     L->ws_bytes = ws;
     return BDLORA_OK;
@@ -173,6 +178,7 @@ struct bdlora_pool {
     int* d_tgrp = nullptr;
     float* d_part = nullptr;
     float* d_mlp = nullptr;
+    float* d_bigpart = nullptr;
     int n_cu = 0;
     uint16_t* d_Xp[bdl::kMaxProjs] = {};
     uint16_t* d_stage = nullptr;
@@ -210,6 +216,7 @@ void free_pool(bdlora_pool* P) {
     f(P->d_tgrp);
     f(P->d_part);
     f(P->d_mlp);
+    f(P->d_bigpart);
     for (auto x : P->d_Xp) f(x);
     f(P->d_stage);
     for (auto e : P->prof_ev) (void)hipEventDestroy(e);
@@ -340,6 +347,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_tgrp, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_part, L.part_slots * bdl::kPartElems, &tot));
     BDL_TRY(dev_alloc(&P->d_mlp, L.mlp_elems, &tot));
+    if (L.bigpart_elems > 0) BDL_TRY(dev_alloc(&P->d_bigpart, L.bigpart_elems, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
@@ -800,9 +808,12 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     int n_loaded = 0;
     for (int v : P->h_loaded) n_loaded += v != 0;
     // bf16 weights above one 256-row tile: the 256 x 256 LDS-staged kernel
-    // (its octet lists are those of 64-row blocks, as planned for T > 32);
-    // smaller batches have too few such tiles to occupy the chip
-    bool big = T > bdl::kBigM && MT == 64;
+    // (its octet lists are those of 64-row blocks, as planned for T > 32),
+    // with long-K tiles split into k-ranges when the batch has too few tiles
+    // to occupy the chip.  Batches of one row tile stay on the 64-row kernel:
+    // they are weight-streaming bound, and the large tile streams its weight
+    // through LDS at under half the rate that kernel reaches.
+    bool big = T > bdl::kBigM && MT == 64 && P->d_bigpart != nullptr;
     for (int i = 0; i < n; ++i) {
         // its buffer loads take 32-bit byte offsets into the packed X and W
         const ProjInfo& pi = L.proj[projs[i]];
@@ -812,7 +823,24 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     const int tiles_m = (T + MT - 1) / MT;
     const int tm = big ? (T + bdl::kBigM - 1) / bdl::kBigM : tiles_m;
     const int tn = big ? bdl::kBigN : NT;
-    int tile = 0, cch = 1;
+    // Large tiles: a projection's tiles are cut into ksplit k-ranges of about
+    // q k-steps, q = (all tile k-steps) / (compute units), so that the work
+    // items fill the chip once; ksplit = 1 when its K is at most q.  The
+    // split items' partials fit kBigPartSlots (sum of tiles x ksplit over the
+    // split projections <= all tile k-steps / q <= the compute units used).
+    int ksplit[bdl::kMaxProjs];
+    for (int i = 0; i < n; ++i) ksplit[i] = 1;
+    if (big) {
+        long long work = 0;
+        for (int i = 0; i < n; ++i) {
+            const ProjInfo& pi = L.proj[projs[i]];
+            work += (long long)tm * ((pi.N + tn - 1) / tn) * (pi.K / 32);
+        }
+        const long long units = std::min<long long>(P->n_cu, bdl::kBigPartSlots);
+        const long long q = std::max(1LL, (work + units - 1) / units);
+        for (int i = 0; i < n; ++i) ksplit[i] = (int)std::max(1LL, (long long)(L.proj[projs[i]].K / 32) / q);
+    }
+    int tile = 0, cch = 1, fix = 0, pslot = 0;
     for (int q = 0; q < n; ++q) {
         const int i = order[q];
         const ProjInfo& pi = L.proj[projs[i]];
@@ -834,7 +862,13 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         pl.b_off = pi.b_off;
         pl.tiles_n = (pi.N + tn - 1) / tn;
         pl.tile_base = tile;
-        tile += tm * pl.tiles_n;
+        pl.ksplit = ksplit[i];
+        tile += tm * pl.tiles_n * pl.ksplit;
+        pl.fix_base = fix;
+        pl.fix_count = pl.ksplit > 1 ? tm * pl.tiles_n : 0;
+        pl.part_base = pslot;
+        fix += pl.fix_count;
+        pslot += pl.fix_count * pl.ksplit;
         cch = std::max(cch, (pi.S * L.r8max + nts - 1) / nts);
     }
     fa.n_proj = n;
@@ -853,6 +887,10 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.oct_cap = oct_cap(L, MT);
     fa.tiles_m = tm;
     fa.total_tiles = tile;
+    fa.bigpart = P->d_bigpart;
+    fa.fixup = 0;
+    fa.total_fix = fix;
+    if (pslot > bdl::kBigPartSlots) return fail(BDLORA_ERR_SHAPE, "large-tile split exceeds its partial workspace");
     if (fa.items_bound > P->items_cap || (long long)tiles_m * fa.oct_cap > P->oct_elems)
         return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
 

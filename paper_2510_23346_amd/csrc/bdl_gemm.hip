@@ -90,14 +90,20 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15, lg = l >> 4;
     const int wr = w % NWR, wc = w / NWR;        // rows 16 RB wr .., columns 128 wc .. of the tile
 
+    // Main launch: workgroup = one work item, a tile's k-range (split tiles
+    // have ksplit items, item = tile * ksplit + range).  Fix-up launch:
+    // workgroup = one split tile, whose partials it adds before the expand.
     const int bid = blockIdx.x;
-    if (bid >= a.total_tiles) return;
+    const bool fix = a.fixup != 0;
+    if (bid >= (fix ? a.total_fix : a.total_tiles)) return;
     int p = 0;
 #pragma unroll
     for (int q = 1; q < kMaxProjs; ++q)
-        if (q < a.n_proj && bid >= a.p[q].tile_base) p = q;
+        if (q < a.n_proj && (fix ? bid >= a.p[q].fix_base && a.p[q].fix_count > 0 : bid >= a.p[q].tile_base)) p = q;
     const ProjLaunch& P = a.p[p];
-    const int local = bid - P.tile_base;
+    const int S = P.ksplit;
+    const int item = fix ? bid - P.fix_base : bid - P.tile_base;
+    const int local = fix ? item : item / S, split = fix ? 0 : item - local * S;
     const int band = local / (kBigBand * P.tiles_n), off = local - band * kBigBand * P.tiles_n;
     const int bh = min(kBigBand, a.tiles_m - band * kBigBand);
     const int nt = off / bh, mt = band * kBigBand + (off - nt * bh);
@@ -120,6 +126,29 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         rvid[rb] = row < T ? a.vid[row] : -1;
     }
 
+    f32x4 acc[RB][8];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // a split tile's partials: fp32, 16 bytes per lane per (wave, rb, cb),
+    // kBigPartElems floats per partial, ksplit consecutive partials per tile
+    const size_t part_lane = ((size_t)w * RB * 8) * 64 + l;
+    f32x4* const part = reinterpret_cast<f32x4*>(a.bigpart) + (size_t)(P.part_base + local * S) * (kBigPartElems / 4);
+
+    if (fix) {
+        // partials in range order (fixed order: reproducible sums)
+        for (int j = 0; j < S; ++j) {
+            const f32x4* src = part + (size_t)j * (kBigPartElems / 4) + part_lane;
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int cb = 0; cb < 8; ++cb) acc[rb][cb] += src[(rb * 8 + cb) * 64];
+        }
+    } else {
+    // this item's k-steps [k0, k0 + NK)
+    const int k0 = split * KS / S, NK = (split + 1) * KS / S - k0;
+
     // staging: fragments 0..15 of a k-step are the tile's activation row
     // blocks, 16..31 its weight column blocks (blocks past the edge are
     // clamped, their results are never stored)
@@ -129,17 +158,12 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
 #pragma unroll
     for (int i = 0; i < CP; ++i) {
         const int f = w + NW * i;
-        src.vo[i] = (i < CP / 2 ? min(mt * 16 + f, nrb - 1) : min(nt * 16 + f - 16, ncb - 1)) * KS * 1024 + l * 16;
+        src.vo[i] = (i < CP / 2 ? min(mt * 16 + f, nrb - 1) : min(nt * 16 + f - 16, ncb - 1)) * KS * 1024 + k0 * 1024 +
+                    l * 16;
     }
 #pragma unroll
     for (int d = 0; d < kBigStages - 1; ++d)
-        if (d < KS) big_issue<CP, NW>(src, d, lds + d * kBigFrags * 64, w);
-
-    f32x4 acc[RB][8];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int cb = 0; cb < 8; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (d < NK) big_issue<CP, NW>(src, d, lds + d * kBigFrags * 64, w);
 
     // Software pipeline over half k-steps (column blocks 0..3, then 4..7 of
     // the wave).  While the MFMAs of the first half run, the second half's
@@ -170,7 +194,7 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
                 acc[rb][4 * half + c] = mfma(wv[c], x[rb], acc[rb][4 * half + c]);
     };
     u32x4 xa[RB], xb[RB], w0[4], w1[4];
-    // k-step ks < KS - 1 (x holds its activations, w0 its first-half
+    // k-step ks < NK - 1 (x holds its activations, w0 its first-half
     // weights; the next k-step's activations arrive in xn)
     // (the scheduling groups pin the reads ahead of the MFMAs they overlap:
     // masks 0x100 = LDS read, 0x008 = MFMA)
@@ -185,10 +209,10 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         __builtin_amdgcn_sched_group_barrier(0x008, 4 * RB - 4, 0);
         __builtin_amdgcn_sched_barrier(0);
         // k-step ks + 1 is complete once at most the copies issued after it
-        // (k-steps ks + 2 .. ks + kBigStages - 2 below KS) are in flight
-        big_wait_ahead<CP>(min(kBigStages - 3, KS - 2 - ks));
+        // (k-steps ks + 2 .. ks + kBigStages - 2 below NK) are in flight
+        big_wait_ahead<CP>(min(kBigStages - 3, NK - 2 - ks));
         const int nx = ks + kBigStages - 1;
-        if (nx < KS) big_issue<CP, NW>(src, nx, stage(nx), w);
+        if (nx < NK) big_issue<CP, NW>(src, nx, stage(nx), w);
         read_x(xn, ks + 1);
         read_w(w0, ks + 1, 0);
         mma(x, w1, 1);
@@ -201,21 +225,31 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         __builtin_amdgcn_sched_barrier(0);
     };
     // k-step 0 is complete once at most the copies of k-steps 1 .. kBigStages - 2 are in flight
-    big_wait_ahead<CP>(min(kBigStages - 2, KS - 1));
+    big_wait_ahead<CP>(min(kBigStages - 2, NK - 1));
     read_x(xa, 0);
     read_w(w0, 0, 0);
     int ks = 0;
-    for (; ks + 2 < KS; ks += 2) {
+    for (; ks + 2 < NK; ks += 2) {
         k_step(ks, xa, xb);
         k_step(ks + 1, xb, xa);
     }
     // one or two k-steps left; the last one reads nothing ahead
-    const bool two = ks + 1 < KS;
+    const bool two = ks + 1 < NK;
     if (two) k_step(ks, xa, xb);
     const u32x4 (&xl)[RB] = two ? xb : xa;
-    read_w(w1, KS - 1, 1);
+    read_w(w1, NK - 1, 1);
     mma(xl, w0, 0);
     mma(xl, w1, 1);
+    if (S > 1) {
+        // a range of a split tile: store the partial, the fix-up launch adds it
+        f32x4* dst = part + (size_t)split * (kBigPartElems / 4) + part_lane;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < 8; ++cb) dst[(rb * 8 + cb) * 64] = acc[rb][cb];
+        return;
+    }
+    }
 
     // expand: acc += Zhat B over the octets of each 64-row block of the wave
     int sig[8];
@@ -296,6 +330,11 @@ constexpr int kBigRB = 4;
 hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s) {
     if (a.total_tiles <= 0) return hipSuccess;
     hipLaunchKernelGGL(gemm_big_kernel<kBigRB>, dim3(a.total_tiles), dim3(128 * (16 / kBigRB)), 0, s, a);
+    if (a.total_fix > 0) {
+        FwdArgs f = a;
+        f.fixup = 1;
+        hipLaunchKernelGGL(gemm_big_kernel<kBigRB>, dim3(a.total_fix), dim3(128 * (16 / kBigRB)), 0, s, f);
+    }
     return hipGetLastError();
 }
 

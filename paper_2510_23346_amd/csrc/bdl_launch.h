@@ -14,6 +14,8 @@ constexpr int kMaxSlots = 8192;
 constexpr int kMaxRank8 = 128;       // largest supported rank, rounded up to 8
 constexpr int kPlanLdsTokens = 8192; // plan keeps validated ids in LDS up to this batch size
 constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base GEMM (prefill)
+constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-tile GEMM's split tiles
+constexpr int kBigPartElems = kBigM * kBigN;
 
 // One projection of a forward launch.
 struct ProjLaunch {
@@ -30,7 +32,11 @@ struct ProjLaunch {
     int slice_col[kMaxSlices + 1];   // first column of each slice; [n_slices] = N
     long long a_off, b_off;   // element offsets of packed A^T_cat and of B^T_cat in a slot
     int tiles_n;              // base GEMM: column tiles of this projection
-    int tile_base;            // base GEMM: first flattened tile of this projection
+    int tile_base;            // base GEMM: first flattened tile (large tiles: work item) of this projection
+    int ksplit;               // large-tile GEMM: k-ranges per tile (1: not split)
+    int fix_base;             // large-tile GEMM: first split tile of this projection in the fix-up order
+    int fix_count;            // large-tile GEMM: split tiles of this projection (0 when ksplit is 1)
+    int part_base;            // large-tile GEMM: first partial tile of this projection's split tiles
 };
 
 // Everything one forward launch needs (passed by value as a kernel argument).
@@ -51,7 +57,10 @@ struct FwdArgs {
     const int* tile_oct;      // expand octet codes per row tile (-1 padded)
     int oct_cap;              // entries per row tile in tile_oct
     int tiles_m;              // base GEMM: row tiles
-    int total_tiles;          // base GEMM: flattened tiles over all projections
+    int total_tiles;          // base GEMM: flattened tiles (large tiles: work items) over all projections
+    float* bigpart;           // large-tile GEMM: fp32 partials of split tiles (kBigPartSlots tiles)
+    int fixup;                // large-tile GEMM: 0 main launch, 1 fix-up launch of the split tiles
+    int total_fix;            // large-tile GEMM: split tiles over all projections
 };
 
 // Activation packing job of the prep launch.

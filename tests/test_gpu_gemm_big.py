@@ -1,7 +1,12 @@
 """GPU parity of the large-tile (256 x 256) prefill base GEMM with the fused
 expand, against the fp64 oracle.
 
-Batches above 256 tokens with bf16 base weights take that kernel.  The
+Batches above 256 tokens with bf16 base weights take that kernel; when a
+batch has too few tiles to fill the chip, long-K tiles are split into
+k-ranges whose fp32 partials a fix-up launch adds (the small shapes above
+256 tokens here are all split; the full-size prefill workloads in
+test_gpu_parity are not).  65 and 130 tokens check the 64-row kernel on the
+same shapes.  The
 projections here are wider than one 256-column tile, with a ragged column
 tail, slice boundaries inside a tile, and more row tiles than one with a
 ragged row tail, so that the clamped edge blocks, the per-64-row octet lists
@@ -39,7 +44,7 @@ def torch_cuda():
     return torch
 
 
-@pytest.mark.parametrize("T,kind", [(257, "uniform"), (520, "uniform"), (777, "segments")])
+@pytest.mark.parametrize("T,kind", [(65, "uniform"), (130, "segments"), (257, "uniform"), (520, "uniform"), (777, "segments")])
 def test_big_tile_parity(torch_cuda, T, kind):
     torch = torch_cuda
     rng = np.random.default_rng(1000 + T)
