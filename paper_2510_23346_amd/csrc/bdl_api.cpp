@@ -112,7 +112,7 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
     L->slot_stride = off;
     L->slab_bytes = (long long)max_slots * off * 2;
     long long ws = 0;
-    ws += 8LL * max_tokens * 4;                                   // vid, perm (+ slack)
+    ws += 9LL * max_tokens * 4;                                   // vid, perm, rowtok (+ slack)
     ws += 4LL * (max_slots + 2) * 4 + 2 * 4;                      // group tables, meta, err
     ws += ((long long)max_slots + max_tokens / 16 + 2) * 16;      // shrink items
     ws += std::max(((long long)max_tokens / 16 + 1) * (2LL * L->r8max + 64),
@@ -171,6 +171,7 @@ struct bdlora_pool {
     int* d_gcount = nullptr;
     int4* d_items = nullptr;
     int* d_tile_oct = nullptr;
+    int* d_rowtok = nullptr;
     long long items_cap = 0, oct_elems = 0;
     int* d_meta = nullptr;
     int* d_err = nullptr;
@@ -210,6 +211,7 @@ void free_pool(bdlora_pool* P) {
     f(P->d_gcount);
     f(P->d_items);
     f(P->d_tile_oct);
+    f(P->d_rowtok);
     f(P->d_meta);
     f(P->d_err);
     for (auto z : P->d_Z) f(z);
@@ -349,6 +351,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_mlp, L.mlp_elems, &tot));
     if (L.bigpart_elems > 0) BDL_TRY(dev_alloc(&P->d_bigpart, L.bigpart_elems, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_rowtok, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gcount, S + 1, &tot));
@@ -625,6 +628,8 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->tr8 = P->d_tr8;
     a->tgrp = nullptr;
     a->perm = P->d_perm;
+    a->rowtok = nullptr;
+    a->oct_perm = 0;
     a->gslot = P->d_gslot;
     a->gstart = P->d_gstart;
     a->gcount = P->d_gcount;
@@ -896,6 +901,12 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
 
     bdl::PrepArgs pa;
     fill_plan_args(P, ids, T, &pa, k);
+    if (big) {
+        // the large tiles take their rows in adapter order
+        pa.rowtok = P->d_rowtok;
+        pa.oct_perm = 1;
+        fa.rowtok = P->d_rowtok;
+    }
     int frags = 0, jobs = 0;
     for (int q = 0; q < n && pack; ++q) {
         bdl::PackJob& J = pa.jobs[jobs++];

@@ -114,7 +114,10 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
 
     // expand inputs that do not depend on the base product: fetched first.
     // Octet lists are per 64-row block; a block wholly past T has none.
-    int code[NH], rvid[RB];
+    // Tile rows are positions in rowtok order (tokens grouped by adapter, so
+    // a 64-row block holds few adapters and the expand few octets); tok[rb]
+    // is the token of this lane's row of block rb (-1 past T).
+    int code[NH], rvid[RB], tok[RB];
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
         const int* codes = a.tile_oct + (size_t)(mt * 4 + wr * NH + h) * a.oct_cap;
@@ -123,7 +126,9 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = rbase + rb * 16 + lr;
-        rvid[rb] = row < T ? a.vid[row] : -1;
+        // (clamped: a bad entry can cost a wrong row, never an access past X or out)
+        tok[rb] = row < T ? (a.rowtok ? (int)min((unsigned)a.rowtok[row], (unsigned)(T - 1)) : row) : -1;
+        rvid[rb] = tok[rb] >= 0 ? a.vid[tok[rb]] : -1;
     }
 
     f32x4 acc[RB][8];
@@ -158,8 +163,15 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
 #pragma unroll
     for (int i = 0; i < CP; ++i) {
         const int f = w + NW * i;
-        src.vo[i] = (i < CP / 2 ? min(mt * 16 + f, nrb - 1) : min(nt * 16 + f - 16, ncb - 1)) * KS * 1024 + k0 * 1024 +
-                    l * 16;
+        if (i < CP / 2 && a.rowtok) {
+            // the lane's row is gathered: its token's fragment, lane slot
+            // (token mod 16) + 16 (l / 16); rows past T repeat a valid token
+            const int t = (int)min((unsigned)a.rowtok[min((mt * 16 + f) * 16 + lr, T - 1)], (unsigned)(T - 1));
+            src.vo[i] = ((t >> 4) * KS + k0) * 1024 + ((t & 15) + 16 * lg) * 16;
+        } else {
+            src.vo[i] = (i < CP / 2 ? min(mt * 16 + f, nrb - 1) : min(nt * 16 + f - 16, ncb - 1)) * KS * 1024 +
+                        k0 * 1024 + l * 16;
+        }
     }
 #pragma unroll
     for (int d = 0; d < kBigStages - 1; ++d)
@@ -285,7 +297,7 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
                     for (int rb = 0; rb < 4; ++rb) {
                         const bool match = cd >= 0 && rvid[4 * h + rb] == slot;
                         const uint16_t* zp =
-                            P.Z + (size_t)(rbase + 64 * h + rb * 16 + lr) * P.zs + sig[cb] * a.r8max + j0;
+                            P.Z + (size_t)max(tok[4 * h + rb], 0) * P.zs + sig[cb] * a.r8max + j0;
                         zh[rb] = match ? ld16(zp) : zero4;
                         zl[rb] = match ? ld16(zp + P.zplane) : zero4;
                     }
@@ -302,12 +314,12 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         }
     }
 
-    // store: lane (lr, lg) of block (rb, cb) holds row rbase + 16 rb + lr,
-    // columns c0 + 16 cb + 4 lg + i
+    // store: lane (lr, lg) of block (rb, cb) holds row rbase + 16 rb + lr
+    // (token tok[rb]), columns c0 + 16 cb + 4 lg + i
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-        const int row = rbase + rb * 16 + lr;
-        if (row >= T) continue;
+        const int row = tok[rb];
+        if (row < 0) continue;
 #pragma unroll
         for (int cb = 0; cb < 8; ++cb) {
             const int col = c0 + cb * 16 + 4 * lg;

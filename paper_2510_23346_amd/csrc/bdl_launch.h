@@ -50,6 +50,7 @@ struct FwdArgs {
     const float* scale;       // [max_slots]
     const int* vid;           // [T] validated ids
     const int* perm;          // [T] tokens grouped by adapter
+    const int* rowtok;        // large-tile GEMM: token of each tile row (adapter order), or null
     const int4* items;        // shrink items {slot, first perm index, rows, r8}
     const int* meta;          // [1] number of shrink items
     int items_bound;          // shrink: upper bound on items
@@ -85,6 +86,8 @@ struct PrepArgs {
     int* tr8;                 // [T] rank (padded to 8) of each token's adapter, 0 if none
     int* tgrp;                // [T] group index of each token's adapter, -1 if none (optional)
     int* perm;
+    int* rowtok;              // optional [T]: the adapted tokens in perm order, then the others in order
+    int oct_perm;             // 1: octet lists for the 64-row blocks of rowtok order (large-tile GEMM)
     int* gslot;
     int* gstart;
     int* gcount;

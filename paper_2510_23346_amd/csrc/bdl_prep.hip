@@ -256,7 +256,10 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
             a.tgrp[t] = v >= 0 ? ldl[v] : -1;
         }
 
-    // stable placement: perm[start(v) + #{t' < t : vid[t'] == v}] = t
+    // stable placement: perm[start(v) + #{t' < t : vid[t'] == v}] = t; with
+    // rowtok, the same order followed by the tokens without an adapter
+    // (rowtok[n_ad + #{t' < t : no adapter}] = t), a permutation of all rows
+    const int n_ad = wpre[15][0] + wsum[15][0];   // tokens with an adapter
     if (a.T <= 1024) {
         const int t = tid;
         const int v = t < a.T ? vid_l[t] : -1;
@@ -264,12 +267,21 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
             int rank = 0;
             for (int u = 0; u < t; ++u) rank += vid_l[u] == v;
             a.perm[cnt[v] + rank] = t;
+            if (a.rowtok) a.rowtok[cnt[v] + rank] = t;
+        } else if (t < a.T && a.rowtok) {
+            int rank = 0;
+            for (int u = 0; u < t; ++u) rank += vid_l[u] < 0;
+            a.rowtok[n_ad + rank] = t;
         }
     } else if (wv == 0) {
+        int ubase = n_ad;
         for (int base = 0; base < a.T; base += 64) {
             const int t = base + lane;
             const int v = t < a.T ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
             bool ok = v >= 0;
+            const unsigned long long um = __ballot(t < a.T && !ok);
+            if (a.rowtok && t < a.T && !ok) a.rowtok[ubase + __popcll(um & ((1ull << lane) - 1ull))] = t;
+            ubase += __popcll(um);
             unsigned long long act = __ballot(ok);
             while (act) {
                 const int leader = __ffsll((long long)act) - 1;
@@ -279,7 +291,9 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
                 const int b = cnt[s];
                 if (lane == leader) cnt[s] = b + __popcll(m);
                 if (mine) {
-                    a.perm[b + __popcll(m & ((1ull << lane) - 1ull))] = t;
+                    const int pos = b + __popcll(m & ((1ull << lane) - 1ull));
+                    a.perm[pos] = t;
+                    if (a.rowtok) a.rowtok[pos] = t;
                     ok = false;
                 }
                 act &= ~m;
@@ -292,14 +306,37 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
         const int mt = a.gemm_mt;
         const int tiles = (a.T + mt - 1) / mt;
         unsigned* bm = bits + (size_t)(wv - 1) * nwords;
+        const int n_groups = wpre[15][1] + wsum[15][1];
         for (int m = wv - 1; m < tiles; m += 15) {
+            int* dst = a.tile_oct + (size_t)m * a.oct_cap;
+            if (a.oct_perm) {
+                // rowtok order: block m holds rows [m mt, m mt + mt) of the
+                // groups laid end to end (slot order, then the tokens without
+                // an adapter): its adapters are the groups overlapping it,
+                // read from the group tables (no need to wait for the
+                // placement)
+                const int r0 = m * mt, r1 = min(r0 + mt, n_ad);
+                int base = 0;
+                for (int g0 = 0; g0 < n_groups; g0 += 64) {
+                    const int g = g0 + lane;
+                    const bool in = g < n_groups && a.gstart[g] < r1 && a.gstart[g] + a.gcount[g] > r0;
+                    const int slot = in ? a.gslot[g] : 0;
+                    const int r8s = in ? r8l[slot] : 0;
+                    const int c = r8s >> 3;
+                    const int inc = wave_incl_scan(c);
+                    int o = base + inc - c;
+                    for (int j = 0; j < c; ++j) dst[o++] = (slot << 12) | (r8s << 4) | j;
+                    base += wave_total(inc);
+                }
+                for (int i = base + lane; i < a.oct_cap; i += 64) dst[i] = -1;
+                continue;
+            }
             for (int i = lane; i < nwords; i += 64) bm[i] = 0u;
             __builtin_amdgcn_wave_barrier();
             const int t = m * mt + lane;
             const int v = (lane < mt && t < a.T) ? (in_lds ? vid_l[t] : a.vid[t]) : -1;
             if (v >= 0) atomicOr(&bm[v >> 5], 1u << (v & 31));
             __builtin_amdgcn_wave_barrier();
-            int* dst = a.tile_oct + (size_t)m * a.oct_cap;
             int base = 0;
             for (int wb = 0; wb < nwords; wb += 64) {
                 const int wi = wb + lane;
