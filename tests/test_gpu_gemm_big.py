@@ -83,3 +83,34 @@ def test_big_tile_parity(torch_cuda, T, kind):
         assert np.array_equal(ys[p][none], yb[p][none])
     assert pool.device_error() == 0
     pool.close()
+
+
+@pytest.mark.parametrize("T,case", [(300, "none"), (300, "one"), (8500, "uniform")])
+def test_big_tile_edge_batches(torch_cuda, T, case):
+    """No token with an adapter (empty octet lists, every row after the
+    adapted ones), one adapter for every token, and a batch above the plan's
+    LDS token limit (8192: the plan reads ids back from HBM)."""
+    torch = torch_cuda
+    rng = np.random.default_rng(7 + T)
+    ranks = [16, 8, 32]
+    if case == "none":
+        ids = np.full(T, -1)
+    elif case == "one":
+        ids = np.full(T, 2)
+    else:
+        ids = rng.integers(-1, len(ranks), size=T)
+    projs = [wl.ProjSpec("qkv", "column", 64, (32, 16, 16)), wl.ProjSpec("o", "row", 32, (48,))]
+    spec = wl.custom_workload(f"edge-{case}-{T}", projs, T, ranks, scales=[1.5, 0.5, 2.0], ids=ids, seed=T)
+    layer = wl.draw_layer(spec, slots=range(len(ranks)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(ranks)), cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, dl.out, dl.ids)
+    torch.cuda.synchronize()
+    ys = dl.outputs()
+    refs = bdlora.layer_forward(layer)
+    for p, pi in enumerate(layer.projs):
+        e = bdlora.rel_errors(ys[p], refs[p])
+        assert e["pointwise"] <= TOL, f"{case} T={T} {pi.spec.name}: {e}"
+    assert pool.device_error() == 0
+    pool.close()
