@@ -10,7 +10,7 @@
 // fragment), kBigStages k-steps deep, with one barrier per k-step.  Eight
 // waves, 4 row quarters x 2 column halves, each own a 64 x 128 sub-tile for
 // the whole K (no cross-wave reduction): per k-step a wave reads 4 + 8
-// fragments from LDS (one k-step ahead, into a second register set) and
+// fragments from LDS (half a k-step ahead of the MFMAs that use them) and
 // issues 32 MFMAs.  The MFMAs take the weight fragment as the A operand, so a
 // lane ends up holding 4 consecutive output columns of one token and stores
 // them with one 8-byte (bf16) or 16-byte (fp32) write.  The expand runs as
@@ -19,6 +19,16 @@
 // of other adapters masked to zero), the A operand is a slice of B^T_cat, the
 // B operand the matching slice of scale * X A (a hi/lo bf16 pair, so the
 // expand sees Z to about 16 bits).
+//
+// Rows: a tile's rows are positions in the plan's row order (tokens grouped
+// by adapter, then the tokens without one), so a 64-row block carries few
+// adapters; each lane gathers its activation row through its buffer-load
+// offset, and Z and the output are addressed by token.
+//
+// Split tiles: when a batch has too few tiles for the chip, the host cuts a
+// projection's tiles into ksplit k-ranges.  Each range stores its fp32 sum as
+// a partial; a second launch of this kernel (fixup) adds a tile's partials
+// in range order, then runs the expand and the store.
 //
 // Tile order: projections heaviest first (set by the host), inside a
 // projection bands of kBigBand row tiles walked column by column.
