@@ -361,7 +361,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
 hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
     const int per = a.total_frags >= kPackWideFrags ? kPackWide : 1;
     int pack_blocks = (a.total_frags + 16 * per - 1) / (16 * per);
-    if (pack_blocks > 1024) pack_blocks = 1024;
+    if (pack_blocks > 4096) pack_blocks = 4096;
     const int nwords = (a.max_slots + 31) >> 5;
     const size_t lds = a.decode_plan ? 0 : 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
     hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), lds, s, a);
