@@ -286,7 +286,9 @@ int bdlora_adapter_elems(const bdlora_proj_desc* projs, int32_t n_projs, int32_t
 
 /* Device memory a pool with these arguments would hold: adapter slabs
  * (every slot sized for max_rank, ranks padded to multiples of 8) and the
- * per-batch workspace.  Pure host function; validates the arguments as
+ * per-batch workspace (when max_tokens is above BDLORA_DECODE_MAX_T it
+ * includes a fixed 64 MiB of fp32 partial tiles for the prefill base GEMM's
+ * split tiles).  Pure host function; validates the arguments as
  * bdlora_create_pool does (except the device). */
 int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots,
                      int32_t max_rank, int32_t max_tokens, int64_t* slab_bytes,
