@@ -388,10 +388,11 @@ def main():
     for i in range(per_pool * R):
         step(i)
     torch.cuda.synchronize()
-    sums, cnt = [0.0, 0.0, 0.0], 0
+    path = sets[0][0].last_path()
+    sums, cnt = [0.0, 0.0, 0.0, 0.0], 0
     for pool, _ in sets:
         ms, n = pool.profile_end()
-        for k in range(3):
+        for k in range(4):
             sums[k] += ms[k] * n
         cnt += n
     k_ms = [s / max(1, cnt) for s in sums]
@@ -404,19 +405,30 @@ def main():
         achieved = m_bytes / (k_ms[dom] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    elif path == "medium":
+        # medium batches: prep, shrink, base product of all rows per tile
+        # (fp32 partials), epilogue (partials + expand).  The main launch
+        # streams the base weight once; at about 240 flops per byte it sits
+        # below the MFMA/HBM ridge, so its bound is HBM: the weight and X
+        # once per projection
+        names = ("prep", "shrink", "gemm", "epilogue")
+        dom, dom_name = 2, "bdl::gemm_mid_kernel"
+        mid_bytes = sum(base_weight_bytes(spec, p) + 2 * spec.T * p.d_in for p in spec.projs)
+        achieved = mid_bytes / (k_ms[dom] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
     else:
         names = ("prep", "shrink", "gemm")
-        # the library's choice of base GEMM: the 256 x 256 LDS-staged kernel for
-        # bf16 weights above 256 tokens, the 64-row kernel otherwise
-        big = spec.T > 256 and spec.weight_format == "bf16"
-        dom, dom_name = 2, "bdl::gemm_big_kernel" if big else "bdl::gemm_kernel"
+        # the library's base GEMM: the 256 x 256 LDS-staged kernel for bf16
+        # weights above 256 tokens, the 64-row kernel otherwise
+        dom, dom_name = 2, "bdl::gemm_big_kernel" if path == "large" else "bdl::gemm_kernel"
         achieved = g_flops / (k_ms[dom] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFS,
                 "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4)}
     roof["traffic"] = committed_traffic(dom_name.split("::")[1], spec.name)
     roof["kernel"] = dom_name
     roof["kernel_ms"] = round(k_ms[dom], 5)
-    roof["algorithmic"] = m_bytes if decode else g_flops
+    roof["algorithmic"] = m_bytes if decode else (mid_bytes if path == "medium" else g_flops)
 
     out = {
         "metric": "tokens/s per layer-shard",

@@ -298,15 +298,35 @@ int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max
 int bdlora_pool_bytes(bdlora_pool_t pool, int64_t* bytes);
 
 /* Timing hooks.  bdlora_profile_begin(pool, n) makes the next n forward
- * calls record HIP events around each of their three launches on the
- * caller's stream: for a decode batch (T <= BDLORA_DECODE_MAX_T) plan and
- * packing, K-split shrink and base partials, epilogue; for a larger batch
- * plan and packing, shrink, base product with fused expand.
+ * calls record HIP events around each of their launches on the caller's
+ * stream, in four intervals: for a decode batch (BDLORA_PATH_DECODE) plan
+ * and packing, K-split shrink and base partials, epilogue, nothing; for a
+ * larger batch plan and packing, shrink, base product (with the fused
+ * expand, or for BDLORA_PATH_MEDIUM the partials), and for
+ * BDLORA_PATH_MEDIUM its epilogue (partials plus expand), else nothing.
  * bdlora_profile_end waits for them and writes the mean duration in
- * milliseconds of each launch to ms[0..2] and the number of recorded calls
- * to *n.  The calls averaged should all take the same sequence. */
+ * milliseconds of each interval to ms[0..3] (an empty interval reads about
+ * 0) and the number of recorded calls to *n.  The calls averaged should
+ * all take the same sequence. */
 int bdlora_profile_begin(bdlora_pool_t pool, int32_t n);
 int bdlora_profile_end(bdlora_pool_t pool, float* ms, int32_t* n);
+
+/* Which launch sequence served the last forward call on this pool (known
+ * when the call returns; the kernels may still be running), for tests and
+ * tuning: *path = 0 before any forward, else one of
+ *   BDLORA_PATH_DECODE  split-K decode launches (T <= BDLORA_DECODE_MAX_T)
+ *   BDLORA_PATH_TILE64  64-row tiles, base product with the fused expand
+ *   BDLORA_PATH_MEDIUM  all rows of the batch in one tile (bf16 weights,
+ *                       T <= 256, layers whose weight is large against the
+ *                       fp32 partials), then an epilogue that adds the
+ *                       partials and the expand
+ *   BDLORA_PATH_LARGE   256 x 256 tiles (bf16 weights, T > 256)
+ * INVALID_ARG for a null pool or path. */
+#define BDLORA_PATH_DECODE 1
+#define BDLORA_PATH_TILE64 2
+#define BDLORA_PATH_MEDIUM 3
+#define BDLORA_PATH_LARGE  4
+int bdlora_last_path(bdlora_pool_t pool, int32_t* path);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* bdlora_last_error(void);

@@ -70,6 +70,7 @@ _SIGS = {
     "bdlora_pool_bytes": (_I, [_P, _LP]),
     "bdlora_profile_begin": (_I, [_P, _I]),
     "bdlora_profile_end": (_I, [_P, _c.POINTER(_c.c_float), _IP]),
+    "bdlora_last_path": (_I, [_P, _IP]),
     "bdlora_last_error": (_c.c_char_p, []),
 }
 HEADER_FUNCTIONS = tuple(_SIGS)
@@ -434,7 +435,14 @@ class Pool:
         _check(lib().bdlora_profile_begin(self._h, int(n)))
 
     def profile_end(self) -> Tuple[List[float], int]:
-        ms = (_c.c_float * 3)()
+        """Mean milliseconds of the four timed intervals, and the calls recorded."""
+        ms = (_c.c_float * 4)()
         n = _c.c_int32()
         _check(lib().bdlora_profile_end(self._h, ms, _c.byref(n)))
-        return [ms[0], ms[1], ms[2]], n.value
+        return [ms[0], ms[1], ms[2], ms[3]], n.value
+
+    def last_path(self) -> str:
+        """Launch sequence of the last forward: 'decode', 'tile64', 'medium', 'large' ('' before any)."""
+        v = _c.c_int32(0)
+        _check(lib().bdlora_last_path(self._h, _c.byref(v)))
+        return {0: "", 1: "decode", 2: "tile64", 3: "medium", 4: "large"}[v.value]

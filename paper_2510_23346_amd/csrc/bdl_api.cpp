@@ -28,6 +28,7 @@ int fail(int code, const std::string& msg) {
     } while (0)
 
 constexpr long long kAlign = 128;  // elements (256 bytes)
+constexpr int kProfEvents = 8;     // timing events per profiled forward: 4 intervals
 
 long long round_up(long long v, long long m) { return (v + m - 1) / m * m; }
 int rank8(int r) { return (r + 7) / 8 * 8; }
@@ -112,7 +113,7 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
     L->slot_stride = off;
     L->slab_bytes = (long long)max_slots * off * 2;
     long long ws = 0;
-    ws += 9LL * max_tokens * 4;                                   // vid, perm, rowtok (+ slack)
+    ws += 9LL * max_tokens * 4;                                   // vid, tr8, tgrp, perm, rowtok, rowslot (+ slack)
     ws += 4LL * (max_slots + 2) * 4 + 2 * 4;                      // group tables, meta, err
     ws += ((long long)max_slots + max_tokens / 16 + 2) * 16;      // shrink items
     ws += std::max(((long long)max_tokens / 16 + 1) * (2LL * L->r8max + 64),
@@ -172,6 +173,7 @@ struct bdlora_pool {
     int4* d_items = nullptr;
     int* d_tile_oct = nullptr;
     int* d_rowtok = nullptr;
+    int* d_rowslot = nullptr;
     long long items_cap = 0, oct_elems = 0;
     int* d_meta = nullptr;
     int* d_err = nullptr;
@@ -189,7 +191,8 @@ struct bdlora_pool {
     // timing hooks
     int prof_left = 0;
     int prof_used = 0;
-    std::vector<hipEvent_t> prof_ev;      // 6 per recorded call
+    int last_path = 0;        // BDLORA_PATH_* of the last forward
+    std::vector<hipEvent_t> prof_ev;      // kProfEvents per recorded call
 };
 
 namespace {
@@ -212,6 +215,7 @@ void free_pool(bdlora_pool* P) {
     f(P->d_items);
     f(P->d_tile_oct);
     f(P->d_rowtok);
+    f(P->d_rowslot);
     f(P->d_meta);
     f(P->d_err);
     for (auto z : P->d_Z) f(z);
@@ -352,6 +356,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     if (L.bigpart_elems > 0) BDL_TRY(dev_alloc(&P->d_bigpart, L.bigpart_elems, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_rowtok, MT, &tot));
+    BDL_TRY(dev_alloc(&P->d_rowslot, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gcount, S + 1, &tot));
@@ -629,6 +634,7 @@ static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::Prep
     a->tgrp = nullptr;
     a->perm = P->d_perm;
     a->rowtok = nullptr;
+    a->rowslot = nullptr;
     a->oct_perm = 0;
     a->gslot = P->d_gslot;
     a->gstart = P->d_gstart;
@@ -767,8 +773,8 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     pa.total_frags = frags;
 
     hipEvent_t* ev = nullptr;
-    if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * 6 <= P->prof_ev.size()) {
-        ev = &P->prof_ev[(size_t)P->prof_used * 6];
+    if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * kProfEvents <= P->prof_ev.size()) {
+        ev = &P->prof_ev[(size_t)P->prof_used * kProfEvents];
         ++P->prof_used;
         --P->prof_left;
     }
@@ -781,6 +787,9 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     if (ev) BDL_HIP(hipEventRecord(ev[4], s));
     BDL_HIP(bdl::launch_dec_epi(da, s));
     if (ev) BDL_HIP(hipEventRecord(ev[5], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[6], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[7], s));
+    P->last_path = BDLORA_PATH_DECODE;
     return BDLORA_OK;
 }
 
@@ -825,6 +834,53 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         const long long xb = ((long long)T + 15) / 16 * 16 * pi.K * 2, wb = (long long)pi.N * pi.K * 2;
         big = big && pi.wfmt == BDLORA_WEIGHT_BF16 && xb < (1LL << 31) && wb < (1LL << 31);
     }
+    // bf16 weights at medium batches: all rows in one tile of the medium-batch
+    // launch (each weight fragment read once), whose partials the 64-row
+    // kernel adds to the expand.  8 waves x mid_nb column blocks per tile;
+    // long-K tiles are cut into k-ranges of about q k-steps so that the
+    // items fill the chip once, every item storing one partial tile.
+    bool mid = !big && T > bdl::kDecodeMaxT && T <= bdl::kMidMaxT && MT == 64 && P->d_bigpart != nullptr;
+    for (int i = 0; i < n; ++i) {
+        const ProjInfo& pi = L.proj[projs[i]];
+        const long long xb = ((long long)T + 15) / 16 * 16 * pi.K * 2;
+        mid = mid && pi.wfmt == BDLORA_WEIGHT_BF16 && xb < (1LL << 31);
+    }
+    const int mid_nb = 2, mid_rb = T <= 128 ? 8 : 16, mid_tn = 128 * mid_nb;
+    int mid_split[bdl::kMaxProjs];
+    int mid_items = 0;
+    if (mid) {
+        long long work = 0;
+        for (int i = 0; i < n; ++i) {
+            const ProjInfo& pi = L.proj[projs[i]];
+            work += (long long)((pi.N + mid_tn - 1) / mid_tn) * (pi.K / 32);
+        }
+        const long long units = std::min<long long>(P->n_cu, bdl::kBigPartSlots);
+        for (long long q = std::max(1LL, (work + units - 1) / units);; ++q) {
+            mid_items = 0;
+            for (int i = 0; i < n; ++i) {
+                const ProjInfo& pi = L.proj[projs[i]];
+                mid_split[i] = (int)std::max(1LL, (long long)(pi.K / 32) / q);
+                mid_items += (pi.N + mid_tn - 1) / mid_tn * mid_split[i];
+            }
+            if (mid_items <= bdl::kBigPartSlots) break;
+            // every tile unsplit and still more partials than the workspace holds
+            if (q >= 1024) {
+                mid = false;
+                break;
+            }
+        }
+        // The partials' round trip (written, then read by the epilogue) must
+        // stay well below the weight bytes the launch saves re-reading: short
+        // K ranges (small layers) make the partials as large as the weight,
+        // and then the 64-row kernel is as fast or faster.
+        long long part_bytes = 0, w_bytes = 0;
+        for (int i = 0; i < n; ++i) {
+            const ProjInfo& pi = L.proj[projs[i]];
+            part_bytes += (long long)((pi.N + mid_tn - 1) / mid_tn) * mid_split[i] * ((T + 15) / 16 * 16) * mid_tn * 4;
+            w_bytes += (long long)pi.N * pi.K * 2;
+        }
+        mid = mid && 2 * part_bytes * 10 <= 6 * w_bytes;
+    }
     const int tiles_m = (T + MT - 1) / MT;
     const int tm = big ? (T + bdl::kBigM - 1) / bdl::kBigM : tiles_m;
     const int tn = big ? bdl::kBigN : NT;
@@ -845,7 +901,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         const long long q = std::max(1LL, (work + units - 1) / units);
         for (int i = 0; i < n; ++i) ksplit[i] = (int)std::max(1LL, (long long)(L.proj[projs[i]].K / 32) / q);
     }
-    int tile = 0, cch = 1, fix = 0, pslot = 0;
+    int tile = 0, cch = 1, fix = 0, pslot = 0, mid_cols = 0;
     for (int q = 0; q < n; ++q) {
         const int i = order[q];
         const ProjInfo& pi = L.proj[projs[i]];
@@ -874,6 +930,13 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         pl.part_base = pslot;
         fix += pl.fix_count;
         pslot += pl.fix_count * pl.ksplit;
+        if (mid) {
+            pl.ksplit = mid_split[i];
+            pl.part_base = pslot;
+            pslot += (pi.N + mid_tn - 1) / mid_tn * mid_split[i];
+            pl.col_base = mid_cols;
+            mid_cols += (pi.N + 63) / 64;
+        }
         cch = std::max(cch, (pi.S * L.r8max + nts - 1) / nts);
     }
     fa.n_proj = n;
@@ -895,6 +958,11 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.bigpart = P->d_bigpart;
     fa.fixup = 0;
     fa.total_fix = fix;
+    fa.mid_rb = mid_rb;
+    fa.mid_nb = mid_nb;
+    fa.mid_items = mid ? mid_items : 0;
+    fa.mid_col_tiles = mid ? mid_cols : 0;
+    fa.max_slots = L.max_slots;
     if (pslot > bdl::kBigPartSlots) return fail(BDLORA_ERR_SHAPE, "large-tile split exceeds its partial workspace");
     if (fa.items_bound > P->items_cap || (long long)tiles_m * fa.oct_cap > P->oct_elems)
         return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
@@ -906,6 +974,13 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         pa.rowtok = P->d_rowtok;
         pa.oct_perm = 1;
         fa.rowtok = P->d_rowtok;
+    } else if (mid) {
+        // so do the medium-batch tiles (their expand needs no octet lists,
+        // only each row's slot and rank)
+        pa.rowtok = P->d_rowtok;
+        pa.rowslot = P->d_rowslot;
+        fa.rowtok = P->d_rowtok;
+        fa.rowslot = P->d_rowslot;
     }
     int frags = 0, jobs = 0;
     for (int q = 0; q < n && pack; ++q) {
@@ -921,8 +996,8 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     pa.total_frags = frags;
 
     hipEvent_t* ev = nullptr;
-    if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * 6 <= P->prof_ev.size()) {
-        ev = &P->prof_ev[(size_t)P->prof_used * 6];
+    if (P->prof_left > 0 && (size_t)(P->prof_used + 1) * kProfEvents <= P->prof_ev.size()) {
+        ev = &P->prof_ev[(size_t)P->prof_used * kProfEvents];
         ++P->prof_used;
         --P->prof_left;
     }
@@ -933,11 +1008,19 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     BDL_HIP(bdl::launch_shrink(fa, k.smb, k.snb, s));
     if (ev) BDL_HIP(hipEventRecord(ev[3], s));
     if (ev) BDL_HIP(hipEventRecord(ev[4], s));
-    if (big)
+    if (big) {
         BDL_HIP(bdl::launch_gemm_big(fa, s));
-    else
-        BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
+    } else {
+        if (mid)
+            BDL_HIP(bdl::launch_gemm_mid(fa, s));
+        else
+            BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
+    }
     if (ev) BDL_HIP(hipEventRecord(ev[5], s));
+    if (ev) BDL_HIP(hipEventRecord(ev[6], s));
+    if (mid) BDL_HIP(bdl::launch_mid_epi(fa, s));
+    if (ev) BDL_HIP(hipEventRecord(ev[7], s));
+    P->last_path = big ? BDLORA_PATH_LARGE : (mid ? BDLORA_PATH_MEDIUM : BDLORA_PATH_TILE64);
     return BDLORA_OK;
 }
 
@@ -1119,7 +1202,7 @@ int bdlora_profile_begin(bdlora_pool_t P, int32_t n) {
     if (!P || n < 0 || n > 100000) return fail(BDLORA_ERR_INVALID_ARG, "bad arguments");
     DeviceGuard guard(P->device);
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
-    while (P->prof_ev.size() < (size_t)n * 6) {
+    while (P->prof_ev.size() < (size_t)n * kProfEvents) {
         hipEvent_t e;
         BDL_HIP(hipEventCreate(&e));
         P->prof_ev.push_back(e);
@@ -1133,20 +1216,26 @@ int bdlora_profile_end(bdlora_pool_t P, float* ms, int32_t* n) {
     if (!P || !ms || !n) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
     DeviceGuard guard(P->device);
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
-    double sum[3] = {0, 0, 0};
+    double sum[kProfEvents / 2] = {};
     for (int i = 0; i < P->prof_used; ++i) {
-        hipEvent_t* ev = &P->prof_ev[(size_t)i * 6];
-        BDL_HIP(hipEventSynchronize(ev[5]));
-        for (int k = 0; k < 3; ++k) {
+        hipEvent_t* ev = &P->prof_ev[(size_t)i * kProfEvents];
+        BDL_HIP(hipEventSynchronize(ev[kProfEvents - 1]));
+        for (int k = 0; k < kProfEvents / 2; ++k) {
             float t = 0.f;
             BDL_HIP(hipEventElapsedTime(&t, ev[2 * k], ev[2 * k + 1]));
             sum[k] += t;
         }
     }
-    for (int k = 0; k < 3; ++k) ms[k] = P->prof_used ? (float)(sum[k] / P->prof_used) : 0.f;
+    for (int k = 0; k < kProfEvents / 2; ++k) ms[k] = P->prof_used ? (float)(sum[k] / P->prof_used) : 0.f;
     *n = P->prof_used;
     P->prof_left = 0;
     P->prof_used = 0;
+    return BDLORA_OK;
+}
+
+int bdlora_last_path(bdlora_pool_t P, int32_t* path) {
+    if (!P || !path) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    *path = P->last_path;
     return BDLORA_OK;
 }
 

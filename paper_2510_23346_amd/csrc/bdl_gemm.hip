@@ -360,4 +360,283 @@ hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Medium batches (kDecodeMaxT < T <= kMidMaxT, bf16 base): the base product
+// X W_s of Alg. 1 / Alg. 2 with every row of the batch in one tile, so each
+// weight fragment is read from HBM once and meets all T rows.
+//
+// Work item = (projection, 8 NB column blocks, k-range).  Per k-step the RB
+// activation fragments (all rows) go from global memory into LDS by DMA,
+// kMidStages k-steps deep, and all eight waves read them there; each wave
+// streams its own NB weight fragments straight into registers through a
+// ring of the same depth, so the weight never passes through LDS.  A wave
+// issues RB NB MFMAs per k-step (weight fragment as the A operand: a lane
+// holds 4 consecutive columns of one row).  Every item stores its fp32 sum
+// as a partial tile in lane order ((wave RB + rb) NB + cb) 64 + lane.  The
+// k-ranges split long-K tiles so that the items fill the chip once.
+//
+// mid_epi_kernel then computes each output: the sum of its partials in
+// range order plus the expand of the token's own adapter (steps "Y_adapter
+// <- Z B" and "Y <- Y + Y_adapter"), sum_j Z[t, j] B^T[n, j] in fp32 FMAs
+// over the token's own ranks only, and one bf16 (or fp32) store.
+// ---------------------------------------------------------------------------
+
+constexpr int kMidStages = 4;
+
+// copy 16 bytes per lane (byte offset vo of the buffer) to lane's slot of the
+// 1 KB fragment at dst
+__device__ __forceinline__ void mid_copy(__amdgpu_buffer_rsrc_t r, u32x4* dst, int vo) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, vo, 0, 0, 0);
+}
+
+template <int RB, int NB>
+__global__ __launch_bounds__(512) void gemm_mid_kernel(FwdArgs a) {
+    constexpr int NW = 8, CPX = RB / NW, D = kMidStages;
+    static_assert(RB % NW == 0 && D >= 3, "each wave copies RB / 8 fragments per k-step");
+    __shared__ u32x4 lds[D * RB * 64];
+    const int w = wave_id(), l = threadIdx.x & 63;
+    const int bid = blockIdx.x;
+    if (bid >= a.mid_items) return;
+    int p = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxProjs; ++q)
+        if (q < a.n_proj && bid >= a.p[q].part_base) p = q;
+    const ProjLaunch& P = a.p[p];
+    const int S = P.ksplit, item = bid - P.part_base, tile = item / S, split = item - tile * S;
+    const int T = a.T, KS = P.K >> 5, nrb = (T + 15) >> 4, ncb = P.N >> 4;
+    const int k0 = split * KS / S, NK = (split + 1) * KS / S - k0;
+
+    // activation copies of a k-step: row block w + 8 i, i < CPX, of the tile.
+    // Tile rows are positions in rowtok order (tokens grouped by adapter, so
+    // the epilogue's consecutive rows share adapters); each lane gathers its
+    // row's token through its buffer-load offset: the token's fragment, lane
+    // slot (token mod 16) + 16 (l / 16).  Rows past T repeat a valid token
+    // (their sums are never read).
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
+    int vo[CPX];
+#pragma unroll
+    for (int i = 0; i < CPX; ++i) {
+        const int pos = min((w + NW * i) * 16 + (l & 15), T - 1);
+        const int t = (int)min((unsigned)a.rowtok[pos], (unsigned)(T - 1));
+        vo[i] = ((t >> 4) * KS + k0) * 1024 + ((t & 15) + 16 * (l >> 4)) * 16;
+    }
+    // this wave's weight column blocks (clamped at the projection's edge)
+    const char* wp[NB];
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+        wp[c] = reinterpret_cast<const char*>(P.W + frag_index(min((tile * NW + w) * NB + c, ncb - 1), k0, KS)) + l * 16;
+
+    // one pipeline turn: the activations of k-step ks into LDS stage d, the
+    // weights into wr.  Past the range the last k-step is loaded again, so
+    // every turn issues the same number of loads and the wait counts below
+    // are exact.
+    auto issue = [&](int ks, int d, u32x4 (&wr)[NB]) __attribute__((always_inline)) {
+        const int kk = min(ks, NK - 1);
+        u32x4* stg = lds + d * RB * 64;
+#pragma unroll
+        for (int i = 0; i < CPX; ++i)
+            mid_copy(rx, stg + (w + NW * i) * 64, vo[i] + kk * 1024);
+#pragma unroll
+        for (int c = 0; c < NB; ++c) wr[c] = *reinterpret_cast<const u32x4*>(wp[c] + (size_t)kk * 1024);
+    };
+
+    f32x4 acc[RB][NB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int c = 0; c < NB; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    u32x4 wr[D][NB];
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) issue(d, d, wr[d]);
+
+    // k-step ks uses stage and ring slot u = ks mod D.  Its loads are complete
+    // once at most the D - 2 later turns are in flight; the barrier makes every
+    // wave's copies visible and ends every wave's reads of k-step ks - 1, whose
+    // stage and ring slot the next turn refills.
+    auto step = [&](int ks, int u) __attribute__((always_inline)) {
+        big_wait_barrier<(D - 2) * (CPX + NB)>();
+        issue(ks + D - 1, (u + D - 1) % D, wr[(u + D - 1) % D]);
+        const u32x4* stg = lds + u * RB * 64;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const u32x4 x = stg[rb * 64 + l];
+#pragma unroll
+            for (int c = 0; c < NB; ++c) acc[rb][c] = mfma(wr[u][c], x, acc[rb][c]);
+        }
+    };
+    int ks = 0;
+    for (; ks + D <= NK; ks += D) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) step(ks + u, u);
+    }
+#pragma unroll
+    for (int u = 0; u < D; ++u)
+        if (ks + u < NK) step(ks + u, u);
+    // no copy into LDS may still be in flight when the workgroup ends
+    big_wait_barrier<0>();
+
+    f32x4* dst = reinterpret_cast<f32x4*>(a.bigpart) + (size_t)(P.part_base + item) * (kBigPartElems / 4) +
+                 (size_t)w * RB * NB * 64 + l;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+        if (rb < nrb)
+#pragma unroll
+            for (int c = 0; c < NB; ++c) dst[(rb * NB + c) * 64] = acc[rb][c];
+}
+
+// Epilogue workgroups: kMidEpiTok tokens x 8 column octets of one 64-column
+// tile; thread (t, g) computes the outputs of token t in columns 8 g .. 8 g + 7.
+constexpr int kMidEpiTok = 32;
+constexpr int kMidEpiSeg = 4;     // partials per output loaded before the first sum
+
+__device__ __forceinline__ void fma8(float (&acc)[8], const u32x4 (&b)[8], const u32x4& zh, const u32x4& zl) {
+    // z_e = hi + lo of rank e (bf16 pair); acc[c] += sum_e z_e B^T[c][e]
+    const uint32_t h[4] = {zh.x, zh.y, zh.z, zh.w}, o[4] = {zl.x, zl.y, zl.z, zl.w};
+    float z[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        z[2 * e] = __uint_as_float(h[e] << 16) + __uint_as_float(o[e] << 16);
+        z[2 * e + 1] = __uint_as_float(h[e] & 0xffff0000u) + __uint_as_float(o[e] & 0xffff0000u);
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const uint32_t q[4] = {b[c].x, b[c].y, b[c].z, b[c].w};
+        float sum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sum = fmaf(z[2 * e], __uint_as_float(q[e] << 16), sum);
+            sum = fmaf(z[2 * e + 1], __uint_as_float(q[e] & 0xffff0000u), sum);
+        }
+        acc[c] += sum;
+    }
+}
+
+__global__ __launch_bounds__(kMidEpiTok * 8) void mid_epi_kernel(FwdArgs a) {
+    const int tile = blockIdx.x;
+    int p = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxProjs; ++q)
+        if (q < a.n_proj && tile >= a.p[q].col_base) p = q;
+    const ProjLaunch& P = a.p[p];
+    const int T = a.T, N = P.N;
+    // rows are positions in rowtok order (those of the main launch's tile)
+    const int pos = blockIdx.y * kMidEpiTok + (threadIdx.x >> 3);
+    const int col = (tile - P.col_base) * 64 + (threadIdx.x & 7) * 8;
+    // threads past the last row or column compute on clamped indices and
+    // store nothing (every load is issued without waiting on a branch)
+    const bool live = pos < T && col < N;
+    const int pp = min(pos, T - 1), cc = min(col, N - 8);
+    // the row's adapter (slot and rank, from the plan's row table) and token,
+    // loaded before the partials so that waiting for them leaves the
+    // partials in flight
+    const int info = a.rowslot[pp];
+    // (clamped: a bad entry can cost a wrong row, never an access past Z or out)
+    const int tt = (int)min((unsigned)a.rowtok[pp], (unsigned)(T - 1));
+
+    // partials: columns cc .. cc + 3 and cc + 4 .. cc + 7 of row pp are lanes
+    // ln and ln + 16 of block (pp / 16, cc / 16) of wave wq of column tile tc
+    const int mnb = a.mid_nb, S = P.ksplit, rbg = pp >> 4, cbg = cc >> 4;
+    const int tc = cbg / (8 * mnb), wq = (cbg - tc * 8 * mnb) / mnb, cq = cbg - tc * 8 * mnb - wq * mnb;
+    const int ln = (pp & 15) + 16 * ((cc & 15) >> 2);
+    const f32x4* src = reinterpret_cast<const f32x4*>(a.bigpart) + (size_t)(P.part_base + tc * S) * (kBigPartElems / 4) +
+                       ((size_t)(wq * a.mid_rb + rbg) * mnb + cq) * 64 + ln;
+    f32x4 y[kMidEpiSeg][2];
+#pragma unroll
+    for (int j = 0; j < kMidEpiSeg; ++j) {
+        const size_t o = (size_t)min(j, S - 1) * (kBigPartElems / 4);
+        y[j][0] = src[o];
+        y[j][1] = src[o + 16];
+    }
+
+    // the token's own adapter: ranks 0..15 of B^T and of Z, loaded without a
+    // branch (a half the rank does not have reads ranks 0..7 again, unused)
+    // (clamped: a bad entry can cost a wrong sum, never an access past the pool)
+    const int v = info >= 0 ? min(info & 0xffff, a.max_slots - 1) : -1;
+    const int r8s = info >= 0 ? min(info >> 16, a.r8max) : 0;
+    int sig = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxSlices; ++q)
+        if (q < P.n_slices && cc >= P.slice_col[q]) sig = q;
+    const uint16_t* bb = a.pool + (size_t)max(v, 0) * a.slot_stride + P.b_off + (size_t)cc * r8s;
+    const uint16_t* zp = P.Z + (size_t)tt * P.zs + sig * a.r8max;
+    u32x4 bq[2][8], zh[2], zl[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int ho = 8 * h < r8s ? 8 * h : 0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) bq[h][c] = ld16(bb + (size_t)c * r8s + ho);
+        zh[h] = ld16(zp + ho);
+        zl[h] = ld16(zp + ho + P.zplane);
+    }
+
+    float acc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMidEpiSeg; ++j)
+        if (j < S) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc[i] += y[j][0][i];
+                acc[4 + i] += y[j][1][i];
+            }
+        }
+    for (int j = kMidEpiSeg; j < S; ++j) {
+        const f32x4 u0 = src[(size_t)j * (kBigPartElems / 4)], u1 = src[(size_t)j * (kBigPartElems / 4) + 16];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            acc[i] += u0[i];
+            acc[4 + i] += u1[i];
+        }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+        if (8 * h < r8s) fma8(acc, bq[h], zh[h], zl[h]);
+    // ranks 16 and up, 8 at a time
+    for (int j0 = 16; j0 < r8s; j0 += 8) {
+        u32x4 br[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) br[c] = ld16(bb + (size_t)c * r8s + j0);
+        fma8(acc, br, ld16(zp + j0), ld16(zp + j0 + P.zplane));
+    }
+    if (!live) return;
+    if (P.out_f32) {
+        float* o = P.out_f32 + (size_t)tt * N + col;
+        *reinterpret_cast<float4*>(o) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        *reinterpret_cast<float4*>(o + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    } else {
+        u32x4 o;
+        o.x = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
+        o.y = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
+        o.z = (uint32_t)f2bf(acc[4]) | ((uint32_t)f2bf(acc[5]) << 16);
+        o.w = (uint32_t)f2bf(acc[6]) | ((uint32_t)f2bf(acc[7]) << 16);
+        *reinterpret_cast<u32x4*>(P.out + (size_t)tt * N + col) = o;
+    }
+}
+
+hipError_t launch_gemm_mid(const FwdArgs& a, hipStream_t s) {
+    if (a.mid_items <= 0) return hipSuccess;
+    if (a.T <= 0 || a.T > a.mid_rb * 16 || a.mid_rb * a.mid_nb * 2048 > kBigPartElems || !a.rowtok)
+        return hipErrorInvalidValue;
+    bool ok = false;
+#define BDL_MID_CASE(R, NN)                                                                     \
+    if (a.mid_rb == R && a.mid_nb == NN) {                                                      \
+        hipLaunchKernelGGL((gemm_mid_kernel<R, NN>), dim3(a.mid_items), dim3(512), 0, s, a);    \
+        ok = true;                                                                              \
+    }
+    BDL_MID_CASE(8, 1) BDL_MID_CASE(8, 2) BDL_MID_CASE(16, 1) BDL_MID_CASE(16, 2)
+#undef BDL_MID_CASE
+    if (!ok) return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_mid_epi(const FwdArgs& a, hipStream_t s) {
+    if (a.mid_items <= 0) return hipSuccess;
+    if (a.T <= 0 || a.mid_col_tiles <= 0 || !a.rowtok || !a.rowslot) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(mid_epi_kernel, dim3(a.mid_col_tiles, (a.T + kMidEpiTok - 1) / kMidEpiTok), dim3(kMidEpiTok * 8),
+                       0, s, a);
+    return hipGetLastError();
+}
+
 }  // namespace bdl

@@ -16,6 +16,7 @@ constexpr int kPlanLdsTokens = 8192; // plan keeps validated ids in LDS up to th
 constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base GEMM (prefill)
 constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-tile GEMM's split tiles
 constexpr int kBigPartElems = kBigM * kBigN;
+constexpr int kMidMaxT = 256;             // medium-batch base GEMM: largest batch (all rows in one tile)
 
 // One projection of a forward launch.
 struct ProjLaunch {
@@ -33,10 +34,12 @@ struct ProjLaunch {
     long long a_off, b_off;   // element offsets of packed A^T_cat and of B^T_cat in a slot
     int tiles_n;              // base GEMM: column tiles of this projection
     int tile_base;            // base GEMM: first flattened tile (large tiles: work item) of this projection
-    int ksplit;               // large-tile GEMM: k-ranges per tile (1: not split)
+    int ksplit;               // large-tile / medium-batch GEMM: k-ranges per tile (1: not split)
     int fix_base;             // large-tile GEMM: first split tile of this projection in the fix-up order
     int fix_count;            // large-tile GEMM: split tiles of this projection (0 when ksplit is 1)
-    int part_base;            // large-tile GEMM: first partial tile of this projection's split tiles
+    int part_base;            // large-tile GEMM: first partial tile of this projection's split tiles;
+                              // medium-batch GEMM: first work item (= partial tile) of this projection
+    int col_base;             // medium-batch GEMM: first 64-column epilogue tile of this projection
 };
 
 // Everything one forward launch needs (passed by value as a kernel argument).
@@ -51,6 +54,7 @@ struct FwdArgs {
     const int* vid;           // [T] validated ids
     const int* perm;          // [T] tokens grouped by adapter
     const int* rowtok;        // large-tile GEMM: token of each tile row (adapter order), or null
+    const int* rowslot;       // medium-batch GEMM: (rank8 << 16) | slot of each such row, -1 for none
     const int4* items;        // shrink items {slot, first perm index, rows, r8}
     const int* meta;          // [1] number of shrink items
     int items_bound;          // shrink: upper bound on items
@@ -62,6 +66,10 @@ struct FwdArgs {
     float* bigpart;           // large-tile GEMM: fp32 partials of split tiles (kBigPartSlots tiles)
     int fixup;                // large-tile GEMM: 0 main launch, 1 fix-up launch of the split tiles
     int total_fix;            // large-tile GEMM: split tiles over all projections
+    int mid_rb, mid_nb;       // medium-batch GEMM: 16-row blocks per tile, 16-column blocks per wave
+    int mid_items;            // medium-batch GEMM: work items (tile x k-range) over all projections
+    int mid_col_tiles;        // medium-batch GEMM: 64-column epilogue tiles over all projections
+    int max_slots;            // pool slots
 };
 
 // Activation packing job of the prep launch.
@@ -87,6 +95,7 @@ struct PrepArgs {
     int* tgrp;                // [T] group index of each token's adapter, -1 if none (optional)
     int* perm;
     int* rowtok;              // optional [T]: the adapted tokens in perm order, then the others in order
+    int* rowslot;             // optional [T], with rowtok: (rank8 << 16) | slot of each row's adapter, -1 for none
     int oct_perm;             // 1: octet lists for the 64-row blocks of rowtok order (large-tile GEMM)
     int* gslot;
     int* gstart;
@@ -164,6 +173,8 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t s);
 hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_gemm(const FwdArgs& a, int mb, int nb, hipStream_t s);
 hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s);
+hipError_t launch_gemm_mid(const FwdArgs& a, hipStream_t s);
+hipError_t launch_mid_epi(const FwdArgs& a, hipStream_t s);
 hipError_t launch_pack_adapter(uint16_t* dst_a, uint16_t* dst_b, const uint16_t* stage, int K,
                                int n_slices, const int* slice_out, int rank, int r8, hipStream_t s);
 hipError_t launch_pack_rows(const uint16_t* src, uint16_t* dst, int rows, int K, hipStream_t s);

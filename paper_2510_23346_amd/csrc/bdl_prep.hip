@@ -268,10 +268,12 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
             for (int u = 0; u < t; ++u) rank += vid_l[u] == v;
             a.perm[cnt[v] + rank] = t;
             if (a.rowtok) a.rowtok[cnt[v] + rank] = t;
+            if (a.rowslot) a.rowslot[cnt[v] + rank] = (r8l[v] << 16) | v;
         } else if (t < a.T && a.rowtok) {
             int rank = 0;
             for (int u = 0; u < t; ++u) rank += vid_l[u] < 0;
             a.rowtok[n_ad + rank] = t;
+            if (a.rowslot) a.rowslot[n_ad + rank] = -1;
         }
     } else if (wv == 0) {
         int ubase = n_ad;
@@ -281,6 +283,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
             bool ok = v >= 0;
             const unsigned long long um = __ballot(t < a.T && !ok);
             if (a.rowtok && t < a.T && !ok) a.rowtok[ubase + __popcll(um & ((1ull << lane) - 1ull))] = t;
+            if (a.rowslot && t < a.T && !ok) a.rowslot[ubase + __popcll(um & ((1ull << lane) - 1ull))] = -1;
             ubase += __popcll(um);
             unsigned long long act = __ballot(ok);
             while (act) {
@@ -294,6 +297,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
                     const int pos = b + __popcll(m & ((1ull << lane) - 1ull));
                     a.perm[pos] = t;
                     if (a.rowtok) a.rowtok[pos] = t;
+                    if (a.rowslot) a.rowslot[pos] = (r8l[s] << 16) | s;
                     ok = false;
                 }
                 act &= ~m;
