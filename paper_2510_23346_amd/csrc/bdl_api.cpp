@@ -951,6 +951,16 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.meta = P->d_meta;
     fa.items_bound = std::min(T, std::max(n_loaded, 1)) + (T + mts - 1) / mts;
     fa.cchunks = cch;
+    // Small batches over many adapters (groups of a few scattered tokens, at
+    // most 8 per loaded adapter on average) split each shrink item's K over
+    // the XCDs, partials in the split-partial workspace (which the GEMM
+    // launches reuse afterwards).  Few large groups read X about once
+    // anyway; there the split would only add the partials' traffic.
+    fa.shrink_kp = 1;
+    if (T <= 512 && T <= 8 * n_loaded && P->d_bigpart &&
+        (long long)n * fa.items_bound * cch * bdl::kShrinkKP * mts * nts <=
+            (long long)bdl::kBigPartSlots * bdl::kBigPartElems)
+        fa.shrink_kp = bdl::kShrinkKP;
     fa.tile_oct = P->d_tile_oct;
     fa.oct_cap = oct_cap(L, MT);
     fa.tiles_m = tm;

@@ -38,6 +38,14 @@ constexpr int kStages = 3;                    // k-steps of loads kept in flight
 // --------------------------------------------------------------------------
 // 2. shrink: Z[t, sigma * r8max + j] = scale_a * sum_k X[t, k] A_a,sigma[k, j]
 //    work item = (projection, shrink item, 16*NB-column chunk of A^T_cat)
+//
+//    Small batches (shrink_kp = kShrinkKP): an item's adapter group holds a
+//    few scattered tokens, and every item reads its rows out of the whole
+//    X, so each XCD would fetch most of X from HBM.  There each item's K is
+//    cut into kShrinkKP ranges, range k running on XCD k (workgroup b runs
+//    on XCD b mod 8, and the flat index keeps the range in its low bits):
+//    each XCD fetches only its range of X.  The ranges store fp32 partial
+//    tiles; shrink_reduce_kernel adds them in range order and writes Z.
 // --------------------------------------------------------------------------
 
 template <int MB, int NB>
@@ -47,10 +55,12 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
     const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15;
     const int n_items = a.meta[1];
     const int per_proj = a.items_bound * a.cchunks;
-    const int total = a.n_proj * per_proj;
+    const int KP = a.shrink_kp;
+    const int total = a.n_proj * per_proj * KP;
 
     for (int flat = blockIdx.x; flat < total; flat += gridDim.x) {
-        const int p = flat / per_proj, rem = flat - p * per_proj;
+        const int f = flat / KP, kp = flat - f * KP;
+        const int p = f / per_proj, rem = f - p * per_proj;
         const int item = rem / a.cchunks, cc = rem - item * a.cchunks;
         const int4 it = a.items[item];       // in bounds for every item < items_bound
         if (item >= n_items) continue;
@@ -79,11 +89,21 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
         for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
             for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // this range's k-steps, split over the 8 waves
+        const int ks0 = kp * KS / KP;
         int k0, nk;
-        wave_krange(KS, w, &k0, &nk);
-        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, k0, nk, kFrag, kFrag);
+        wave_krange((kp + 1) * KS / KP - ks0, w, &k0, &nk);
+        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, ks0 + k0, nk, kFrag, kFrag);
         reduce_waves<MB, NB>(acc, red);
 
+        if (KP > 1) {
+            // partial tile of range kp (row-major MT x NT), summed by shrink_reduce_kernel
+            float* dst = a.bigpart + (size_t)flat * (MT * NT);
+            for (int idx = threadIdx.x; idx < MT * NT; idx += kThreads)
+                dst[idx] = red[(idx / NT) * LD + idx % NT];
+            __syncthreads();
+            continue;
+        }
         for (int idx = threadIdx.x; idx < MT * NT; idx += kThreads) {
             const int r = idx / NT, c = idx - (idx / NT) * NT;
             const int cg = c0 + c;
@@ -101,14 +121,58 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
     }
 }
 
+// Z of the split shrink: the kShrinkKP range partials of each (projection,
+// item, chunk) tile added in range order, scaled, stored as the bf16 pair.
+template <int MB, int NB>
+__global__ __launch_bounds__(256) void shrink_reduce_kernel(FwdArgs a) {
+    constexpr int MT = MB * 16, NT = NB * 16, KP = kShrinkKP;
+    const int n_items = a.meta[1];
+    const int per_proj = a.items_bound * a.cchunks;
+    const int total = a.n_proj * per_proj;
+    for (int f = blockIdx.x; f < total; f += gridDim.x) {
+        const int p = f / per_proj, rem = f - p * per_proj;
+        const int item = rem / a.cchunks, cc = rem - item * a.cchunks;
+        const int4 it = a.items[item];
+        if (item >= n_items) continue;
+        const int slot = it.x, nrows = it.z, r8s = it.w;
+        const ProjLaunch& P = a.p[p];
+        const int ncols = P.n_slices * r8s, c0 = cc * NT;
+        if (c0 >= ncols) continue;
+        const float sc = a.scale[slot];
+        const int* prow = a.perm + it.y;
+        const float* src = a.bigpart + (size_t)f * KP * (MT * NT);
+        for (int idx = threadIdx.x; idx < MT * NT; idx += 256) {
+            const int r = idx / NT, c = idx - (idx / NT) * NT, cg = c0 + c;
+            if (r < nrows && cg < ncols) {
+                float z = 0.f;
+#pragma unroll
+                for (int k = 0; k < KP; ++k) z += src[(size_t)k * (MT * NT) + idx];
+                z *= sc;
+                const int t = prow[r];
+                const int sig = cg / r8s, j = cg - sig * r8s;
+                const uint16_t hi = f2bf(z);
+                const size_t zi = (size_t)t * P.zs + sig * a.r8max + j;
+                P.Z[zi] = hi;
+                P.Z[zi + P.zplane] = f2bf(z - bf2f(hi));
+            }
+        }
+    }
+}
+
 hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
-    const int total = a.n_proj * a.items_bound * a.cchunks;
+    const int KP = a.shrink_kp;
+    if (KP != 1 && (KP != kShrinkKP || !a.bigpart)) return hipErrorInvalidValue;
+    const int tiles = a.n_proj * a.items_bound * a.cchunks;
+    const int total = tiles * KP;
+    // a multiple of 8 (with KP = 8 each workgroup keeps one k-range)
     const int grid = total < 4096 ? total : 4096;
     if (grid <= 0) return hipSuccess;
-#define BDL_SHRINK_CASE(M, NN)                                                   \
-    if (mb == M && nb == NN) {                                                   \
-        hipLaunchKernelGGL((shrink_kernel<M, NN>), dim3(grid), dim3(kThreads), 0, s, a); \
-        return hipGetLastError();                                                \
+    const int rgrid = tiles < 2048 ? tiles : 2048;
+#define BDL_SHRINK_CASE(M, NN)                                                                          \
+    if (mb == M && nb == NN) {                                                                          \
+        hipLaunchKernelGGL((shrink_kernel<M, NN>), dim3(grid), dim3(kThreads), 0, s, a);               \
+        if (KP > 1) hipLaunchKernelGGL((shrink_reduce_kernel<M, NN>), dim3(rgrid), dim3(256), 0, s, a); \
+        return hipGetLastError();                                                                       \
     }
     BDL_SHRINK_CASE(1, 1) BDL_SHRINK_CASE(1, 2) BDL_SHRINK_CASE(1, 4)
     BDL_SHRINK_CASE(4, 1) BDL_SHRINK_CASE(4, 2) BDL_SHRINK_CASE(4, 4)

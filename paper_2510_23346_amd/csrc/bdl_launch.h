@@ -17,6 +17,7 @@ constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base 
 constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-tile GEMM's split tiles
 constexpr int kBigPartElems = kBigM * kBigN;
 constexpr int kMidMaxT = 256;             // medium-batch base GEMM: largest batch (all rows in one tile)
+constexpr int kShrinkKP = 8;              // shrink k-ranges per item when split (one per XCD)
 
 // One projection of a forward launch.
 struct ProjLaunch {
@@ -59,6 +60,8 @@ struct FwdArgs {
     const int* meta;          // [1] number of shrink items
     int items_bound;          // shrink: upper bound on items
     int cchunks;              // shrink: column chunks per item (upper bound)
+    int shrink_kp;            // shrink: k-ranges per item (1, or kShrinkKP: fp32 partials in bigpart
+                              // that a second launch sums into Z)
     const int* tile_oct;      // expand octet codes per row tile (-1 padded)
     int oct_cap;              // entries per row tile in tile_oct
     int tiles_m;              // base GEMM: row tiles
