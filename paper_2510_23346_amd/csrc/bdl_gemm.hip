@@ -485,13 +485,17 @@ __global__ __launch_bounds__(512) void gemm_mid_kernel(FwdArgs a) {
             for (int c = 0; c < NB; ++c) dst[(rb * NB + c) * 64] = acc[rb][c];
 }
 
-// Epilogue workgroups: kMidEpiTok tokens x 8 column octets of one 64-column
-// tile; thread (t, g) computes the outputs of token t in columns 8 g .. 8 g + 7.
-constexpr int kMidEpiTok = 32;
-constexpr int kMidEpiSeg = 4;     // partials per output loaded before the first sum
+// Epilogue workgroups: 256 threads over one 64-column tile; thread (t, g)
+// computes the outputs of row t in columns CPT g .. CPT g + CPT - 1, so a
+// workgroup covers 256 CPT / 64 rows.  Four columns per thread keep the
+// registers (and so the resident waves) of a thread's loads in flight low.
+constexpr int kMidEpiCols = 4;    // columns per thread
+constexpr int kMidEpiSeg = 2;     // partials per output loaded before the first sum
 
-__device__ __forceinline__ void fma8(float (&acc)[8], const u32x4 (&b)[8], const u32x4& zh, const u32x4& zl) {
-    // z_e = hi + lo of rank e (bf16 pair); acc[c] += sum_e z_e B^T[c][e]
+// acc[c] += sum_e z_e B^T[c][e] over 8 ranks, z_e = hi + lo of the bf16 pair
+template <int CPT>
+__device__ __forceinline__ void fma_ranks8(float (&acc)[CPT], const u32x4 (&b)[CPT], const u32x4& zh,
+                                           const u32x4& zl) {
     const uint32_t h[4] = {zh.x, zh.y, zh.z, zh.w}, o[4] = {zl.x, zl.y, zl.z, zl.w};
     float z[8];
 #pragma unroll
@@ -500,7 +504,7 @@ __device__ __forceinline__ void fma8(float (&acc)[8], const u32x4 (&b)[8], const
         z[2 * e + 1] = __uint_as_float(h[e] & 0xffff0000u) + __uint_as_float(o[e] & 0xffff0000u);
     }
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
+    for (int c = 0; c < CPT; ++c) {
         const uint32_t q[4] = {b[c].x, b[c].y, b[c].z, b[c].w};
         float sum = 0.f;
 #pragma unroll
@@ -512,7 +516,10 @@ __device__ __forceinline__ void fma8(float (&acc)[8], const u32x4 (&b)[8], const
     }
 }
 
-__global__ __launch_bounds__(kMidEpiTok * 8) void mid_epi_kernel(FwdArgs a) {
+template <int CPT>
+__global__ __launch_bounds__(256) void mid_epi_kernel(FwdArgs a) {
+    static_assert(CPT == 4 || CPT == 8, "one or two 4-column lanes of a partial block");
+    constexpr int TPR = 64 / CPT, RPW = 256 / TPR, NQ = CPT / 4;   // threads per row, rows per workgroup
     const int tile = blockIdx.x;
     int p = 0;
 #pragma unroll
@@ -521,12 +528,12 @@ __global__ __launch_bounds__(kMidEpiTok * 8) void mid_epi_kernel(FwdArgs a) {
     const ProjLaunch& P = a.p[p];
     const int T = a.T, N = P.N;
     // rows are positions in rowtok order (those of the main launch's tile)
-    const int pos = blockIdx.y * kMidEpiTok + (threadIdx.x >> 3);
-    const int col = (tile - P.col_base) * 64 + (threadIdx.x & 7) * 8;
+    const int pos = blockIdx.y * RPW + threadIdx.x / TPR;
+    const int col = (tile - P.col_base) * 64 + (threadIdx.x % TPR) * CPT;
     // threads past the last row or column compute on clamped indices and
     // store nothing (every load is issued without waiting on a branch)
     const bool live = pos < T && col < N;
-    const int pp = min(pos, T - 1), cc = min(col, N - 8);
+    const int pp = min(pos, T - 1), cc = min(col, N - CPT);
     // the row's adapter (slot and rank, from the plan's row table) and token,
     // loaded before the partials so that waiting for them leaves the
     // partials in flight
@@ -534,19 +541,19 @@ __global__ __launch_bounds__(kMidEpiTok * 8) void mid_epi_kernel(FwdArgs a) {
     // (clamped: a bad entry can cost a wrong row, never an access past Z or out)
     const int tt = (int)min((unsigned)a.rowtok[pp], (unsigned)(T - 1));
 
-    // partials: columns cc .. cc + 3 and cc + 4 .. cc + 7 of row pp are lanes
-    // ln and ln + 16 of block (pp / 16, cc / 16) of wave wq of column tile tc
+    // partials: columns cc + 4 q .. + 3 of row pp are lane ln + 16 q of block
+    // (pp / 16, cc / 16) of wave wq of column tile tc
     const int mnb = a.mid_nb, S = P.ksplit, rbg = pp >> 4, cbg = cc >> 4;
     const int tc = cbg / (8 * mnb), wq = (cbg - tc * 8 * mnb) / mnb, cq = cbg - tc * 8 * mnb - wq * mnb;
     const int ln = (pp & 15) + 16 * ((cc & 15) >> 2);
     const f32x4* src = reinterpret_cast<const f32x4*>(a.bigpart) + (size_t)(P.part_base + tc * S) * (kBigPartElems / 4) +
                        ((size_t)(wq * a.mid_rb + rbg) * mnb + cq) * 64 + ln;
-    f32x4 y[kMidEpiSeg][2];
+    f32x4 y[kMidEpiSeg][NQ];
 #pragma unroll
     for (int j = 0; j < kMidEpiSeg; ++j) {
         const size_t o = (size_t)min(j, S - 1) * (kBigPartElems / 4);
-        y[j][0] = src[o];
-        y[j][1] = src[o + 16];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) y[j][q] = src[o + 16 * q];
     }
 
     // the token's own adapter: ranks 0..15 of B^T and of Z, loaded without a
@@ -560,58 +567,95 @@ __global__ __launch_bounds__(kMidEpiTok * 8) void mid_epi_kernel(FwdArgs a) {
         if (q < P.n_slices && cc >= P.slice_col[q]) sig = q;
     const uint16_t* bb = a.pool + (size_t)max(v, 0) * a.slot_stride + P.b_off + (size_t)cc * r8s;
     const uint16_t* zp = P.Z + (size_t)tt * P.zs + sig * a.r8max;
-    u32x4 bq[2][8], zh[2], zl[2];
+    u32x4 zh[2], zl[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
         const int ho = 8 * h < r8s ? 8 * h : 0;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) bq[h][c] = ld16(bb + (size_t)c * r8s + ho);
         zh[h] = ld16(zp + ho);
         zl[h] = ld16(zp + ho + P.zplane);
     }
 
-    float acc[8];
+    // Ranks 0..15 of each row's B^T slice (64 columns of the tile) through
+    // LDS: the workgroup loads the RPW slices with 16-byte loads in which
+    // consecutive lanes read consecutive (column, rank half) pieces, so a wave
+    // instruction covers contiguous bytes, where each thread reading its own
+    // columns straight from HBM would touch a cache line per lane.  A slice
+    // is stored column-interleaved (column c in slot (c mod CPT) 64 / CPT +
+    // c / CPT), so the threads of a row reading one of their columns read
+    // consecutive 32-byte slots (two-way bank conflicts; a padded slot would
+    // avoid them but the extra LDS costs more in resident workgroups).
+    constexpr int SLOT = 2;                      // u32x4 per column slot: rank halves 0, 1
+    __shared__ u32x4 bl[RPW * 64 * SLOT];
+    __shared__ int rinfo[RPW];
+    const int rl = threadIdx.x / TPR;            // this thread's row in the workgroup
+    if (threadIdx.x % TPR == 0) rinfo[rl] = info;
+    __syncthreads();
+    const int tile_c0 = (tile - P.col_base) * 64;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) acc[c] = 0.f;
+    for (int k = 0; k < RPW * 128 / 256; ++k) {
+        const int idx = k * 256 + threadIdx.x, row = idx >> 7, pc = idx & 127, c = pc >> 1, h = pc & 1;
+        const int inf = rinfo[row];
+        const int vs = inf >= 0 ? min(inf & 0xffff, a.max_slots - 1) : 0;
+        const int rs = inf >= 0 ? min(inf >> 16, a.r8max) : 0;
+        // columns past N and halves past the rank read a valid piece, unused
+        const int col_c = min(tile_c0 + c, N - 1), hh = 8 * h < rs ? 8 * h : 0;
+        const u32x4 piece = ld16(a.pool + (size_t)vs * a.slot_stride + P.b_off + (size_t)col_c * rs + hh);
+        bl[(row * 64 + (c % CPT) * (64 / CPT) + c / CPT) * SLOT + h] = piece;
+    }
+    __syncthreads();
+    u32x4 bq[2][CPT];
+    {
+        const int g = (threadIdx.x % TPR) - (col - cc) / CPT;   // column group of cc in the tile
+#pragma unroll
+        for (int c = 0; c < CPT; ++c)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) bq[h][c] = bl[(rl * 64 + c * (64 / CPT) + g) * SLOT + h];
+    }
+
+    float acc[CPT];
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) acc[c] = 0.f;
 #pragma unroll
     for (int j = 0; j < kMidEpiSeg; ++j)
         if (j < S) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                acc[i] += y[j][0][i];
-                acc[4 + i] += y[j][1][i];
-            }
+            for (int q = 0; q < NQ; ++q)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[4 * q + i] += y[j][q][i];
         }
     for (int j = kMidEpiSeg; j < S; ++j) {
-        const f32x4 u0 = src[(size_t)j * (kBigPartElems / 4)], u1 = src[(size_t)j * (kBigPartElems / 4) + 16];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            acc[i] += u0[i];
-            acc[4 + i] += u1[i];
+        for (int q = 0; q < NQ; ++q) {
+            const f32x4 u = src[(size_t)j * (kBigPartElems / 4) + 16 * q];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[4 * q + i] += u[i];
         }
     }
 #pragma unroll
     for (int h = 0; h < 2; ++h)
-        if (8 * h < r8s) fma8(acc, bq[h], zh[h], zl[h]);
+        if (8 * h < r8s) fma_ranks8<CPT>(acc, bq[h], zh[h], zl[h]);
     // ranks 16 and up, 8 at a time
     for (int j0 = 16; j0 < r8s; j0 += 8) {
-        u32x4 br[8];
+        u32x4 br[CPT];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) br[c] = ld16(bb + (size_t)c * r8s + j0);
-        fma8(acc, br, ld16(zp + j0), ld16(zp + j0 + P.zplane));
+        for (int c = 0; c < CPT; ++c) br[c] = ld16(bb + (size_t)c * r8s + j0);
+        fma_ranks8<CPT>(acc, br, ld16(zp + j0), ld16(zp + j0 + P.zplane));
     }
     if (!live) return;
     if (P.out_f32) {
         float* o = P.out_f32 + (size_t)tt * N + col;
-        *reinterpret_cast<float4*>(o) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-        *reinterpret_cast<float4*>(o + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            *reinterpret_cast<float4*>(o + 4 * q) = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
     } else {
-        u32x4 o;
-        o.x = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
-        o.y = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
-        o.z = (uint32_t)f2bf(acc[4]) | ((uint32_t)f2bf(acc[5]) << 16);
-        o.w = (uint32_t)f2bf(acc[6]) | ((uint32_t)f2bf(acc[7]) << 16);
-        *reinterpret_cast<u32x4*>(P.out + (size_t)tt * N + col) = o;
+        uint32_t w[CPT / 2];
+#pragma unroll
+        for (int c = 0; c < CPT / 2; ++c) w[c] = (uint32_t)f2bf(acc[2 * c]) | ((uint32_t)f2bf(acc[2 * c + 1]) << 16);
+        uint16_t* o = P.out + (size_t)tt * N + col;
+        if constexpr (CPT == 8)
+            *reinterpret_cast<u32x4*>(o) = u32x4{w[0], w[1], w[2], w[3]};
+        else
+            *reinterpret_cast<uint2*>(o) = make_uint2(w[0], w[1]);
     }
 }
 
@@ -634,8 +678,8 @@ hipError_t launch_gemm_mid(const FwdArgs& a, hipStream_t s) {
 hipError_t launch_mid_epi(const FwdArgs& a, hipStream_t s) {
     if (a.mid_items <= 0) return hipSuccess;
     if (a.T <= 0 || a.mid_col_tiles <= 0 || !a.rowtok || !a.rowslot) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(mid_epi_kernel, dim3(a.mid_col_tiles, (a.T + kMidEpiTok - 1) / kMidEpiTok), dim3(kMidEpiTok * 8),
-                       0, s, a);
+    constexpr int rows = 256 / (64 / kMidEpiCols);   // rows per workgroup
+    hipLaunchKernelGGL(mid_epi_kernel<kMidEpiCols>, dim3(a.mid_col_tiles, (a.T + rows - 1) / rows), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
