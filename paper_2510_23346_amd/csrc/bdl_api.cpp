@@ -989,6 +989,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         // only each row's slot and rank)
         pa.rowtok = P->d_rowtok;
         pa.rowslot = P->d_rowslot;
+        pa.tile_oct = nullptr;
         fa.rowtok = P->d_rowtok;
         fa.rowslot = P->d_rowslot;
     }
