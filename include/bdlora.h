@@ -68,7 +68,8 @@ extern "C" {
 /* Batches of at most this many tokens take the decode launch sequence (plan
  * and packing, K-split shrink and base partials, epilogue); larger ones take
  * the prefill sequence (plan and packing, shrink, base product with the
- * expand fused in). */
+ * expand fused in, or for medium batches on large layers base partials and
+ * an epilogue; see bdlora_last_path). */
 #define BDLORA_DECODE_MAX_T 64
 /* Activation between the two projections of bdlora_forward_mlp. */
 #define BDLORA_ACT_NONE     0   /* H = first projection's output (Alg. 1)  */
@@ -287,8 +288,9 @@ int bdlora_adapter_elems(const bdlora_proj_desc* projs, int32_t n_projs, int32_t
 /* Device memory a pool with these arguments would hold: adapter slabs
  * (every slot sized for max_rank, ranks padded to multiples of 8) and the
  * per-batch workspace (when max_tokens is above BDLORA_DECODE_MAX_T it
- * includes a fixed 64 MiB of fp32 partial tiles for the prefill base GEMM's
- * split tiles).  Pure host function; validates the arguments as
+ * includes a fixed 64 MiB of fp32 partial tiles, used in turn by the split
+ * shrink, the medium-batch base product and the large-tile GEMM's split
+ * tiles).  Pure host function; validates the arguments as
  * bdlora_create_pool does (except the device). */
 int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots,
                      int32_t max_rank, int32_t max_tokens, int64_t* slab_bytes,
