@@ -26,6 +26,8 @@ COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
 ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections
+# BDLORA_PATH_*: launch sequence of a forward (0: none yet)
+PATHS = {0: "", 1: "decode", 2: "tile64", 3: "medium", 4: "large"}
 WEIGHT_BF16, WEIGHT_INT4_G128 = 0, 1   # BDLORA_WEIGHT_*: base weight formats
 _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_PKG, "libbdlora.so")
@@ -445,4 +447,4 @@ class Pool:
         """Launch sequence of the last forward: 'decode', 'tile64', 'medium', 'large' ('' before any)."""
         v = _c.c_int32(0)
         _check(lib().bdlora_last_path(self._h, _c.byref(v)))
-        return {0: "", 1: "decode", 2: "tile64", 3: "medium", 4: "large"}[v.value]
+        return PATHS[v.value]

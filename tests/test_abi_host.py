@@ -1,6 +1,7 @@
 """CPU checks of the C ABI library: it loads, exports every function the
 header declares, and its pure host functions (plan, sizing, element counts)
 agree with the oracle.  No GPU call is made here."""
+import ctypes
 import itertools
 import os
 import re
@@ -47,6 +48,9 @@ def test_binding_constants_match_header():
         (bd.WEIGHT_BF16, bd.WEIGHT_INT4_G128)
     for code, name in bd.STATUS.items():
         assert int(macros["BDLORA_" + ("OK" if code == 0 else "ERR_" + name)]) == code
+    for code, name in bd.PATHS.items():
+        if code:
+            assert int(macros["BDLORA_PATH_" + ("TILE64" if name == "tile64" else name.upper())]) == code
 
 
 def test_adapter_elems_reproduce_paper_counts(L):
@@ -82,6 +86,9 @@ def test_shape_errors(L, bad):
 
 
 def test_argument_errors(L):
+    # the path query validates its pointers without touching a device
+    v = ctypes.c_int32(7)
+    assert L.bdlora_last_path(None, ctypes.byref(v)) == -1 and v.value == 7
     with pytest.raises(bd.BDLoRAError) as e:
         bd.pool_size([("column", 64, (16,))], 0, 8, 16)
     assert e.value.code == -1
