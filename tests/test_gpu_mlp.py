@@ -101,6 +101,38 @@ def test_mlp_8b_shapes_decode(torch_cuda):
     pool.close()
 
 
+@pytest.mark.parametrize("T", [72, 128])
+def test_mlp_70b_shapes_medium_batch(torch_cuda, T):
+    # Llama-3.1-70B MLP shard at 1/8 tensor parallelism: gate/up 8192 -> 3584,
+    # down 3584 -> 8192.  At these batch sizes gate and up (117 MB of weight)
+    # take the medium-batch launches with fp32 outputs (the MLP's
+    # intermediate); from about 160 tokens their partials would exceed the
+    # byte rule.  Then H is packed and down runs on its own path.
+    torch = torch_cuda
+    projs = [p for p in wl.model_projs("llama-3.1-70b", 8) if p.name in ("gate", "up", "down")]
+    rng = np.random.default_rng(70 + T)
+    ranks = [16, 8, 32, 16]
+    ids = rng.integers(-1, len(ranks), size=T)
+    spec = wl.custom_workload(f"mlp-70b-{T}", projs, T, ranks, scales=[2.0, 1.0, 0.5, 1.5], ids=ids, seed=70 + T)
+    layer = wl.draw_layer(spec, slots=range(len(ranks)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(ranks)), cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    # gate and up on their own take the medium-batch path
+    g = [torch.empty((T, 3584), dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    pool.forward_layer([0, 1], [dl.X[0], dl.X[0]], [dl.W[0], dl.W[1]], g, dl.ids)
+    torch.cuda.synchronize()
+    assert pool.last_path() == "medium"
+    out = torch.empty((T, 8192), dtype=torch.bfloat16, device="cuda")
+    pool.forward_mlp(bd.ACT_SILU_MUL, [0, 1], 2, dl.X[0], [dl.W[0], dl.W[1]], dl.W[2], out, dl.ids)
+    torch.cuda.synchronize()
+    _, ref = mlp.mlp_layer_forward(layer, [0, 1], 2, "silu_mul")
+    e = bdlora.rel_errors(device_to_float(out), ref)
+    assert e["pointwise"] <= TOL, f"T={T}: {e}"
+    assert pool.device_error() == 0
+    pool.close()
+
+
 def test_mlp_argument_errors(torch_cuda):
     torch = torch_cuda
     spec, layer, pool = _setup(8, 3, "silu_mul")
