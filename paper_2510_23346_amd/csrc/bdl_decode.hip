@@ -413,7 +413,10 @@ __device__ __forceinline__ void expand8(float (&acc)[8], const float (&z)[8], co
 // the first 16 ranks' B^T and of their Z partials is issued before any sum,
 // so a thread waits for two round trips (more only for ranks above 16 or
 // groups split over many workgroups).
-__device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, int col, float (&acc)[8]) {
+// bs: this thread's columns' ranks 0..15 of B^T for token t, staged in LDS by
+// dec_epi_stage (column c of the thread at bs[16 c], rank halves at +0, +1).
+__device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, int col, const u32x4* bs,
+                                        float (&acc)[8]) {
     const DecProj& P = a.p[p];
     const int v = a.vid[t];
     const int r8s = a.tr8[t];
@@ -454,7 +457,7 @@ __device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, i
         for (int h = 0; h < 2; ++h) {
             if (8 * h < r8s) {
 #pragma unroll
-                for (int c = 0; c < 8; ++c) q[h][c] = ld16(bb + (size_t)c * r8s + 8 * h);
+                for (int c = 0; c < 8; ++c) q[h][c] = bs[16 * c + h];
                 const int vc = sig * r8s + 8 * h;
                 const int vb = P.nWb + ai * P.nbA + (vc >> 4);
                 group_wgs(pp, vb >> 2, U, G, &z0[h], &z1[h]);
@@ -529,9 +532,38 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 // projection 1 being up), stored in bf16 in the fragment layout the second
 // projection reads (rows = tokens, k = these columns).
 // Epilogue workgroups: kEpiTok tokens x 8 column octets of one 64-column tile.
-constexpr int kEpiTok = 32;
+constexpr int kEpiTok = 16;
 constexpr int kEpiThreads = kEpiTok * 8;
 
+// Ranks 0..15 of B^T for the workgroup's tokens and 64-column tile n of
+// projection p, into LDS: 16-byte pieces in which consecutive threads read
+// consecutive (column, rank half) pieces of a token's slice, so a wave's load
+// covers contiguous bytes (a thread loading its own 8 columns would touch a
+// cache line per lane).  A token's slice is stored column-interleaved: column
+// c in slot (c mod 8) 8 + c / 8, 32 bytes, so the 8 threads of a token reading
+// their k-th column read consecutive slots.  Pieces past the rank or the
+// projection's width read a valid piece, unused.  Starts and ends with a
+// barrier (every thread of the workgroup calls it).
+__device__ __forceinline__ void dec_epi_stage(const DecArgs& a, int p, int n, int t, u32x4* bst, int2* rinf) {
+    const DecProj& P = a.p[p];
+    if ((threadIdx.x & 7) == 0) {
+        const int v = a.vid[t];
+        rinf[threadIdx.x >> 3] = make_int2(max(v, 0), v >= 0 ? min(a.tr8[t], kMaxRank8) : 0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kEpiTok * 128 / kEpiThreads; ++k) {
+        const int idx = k * kEpiThreads + threadIdx.x, row = idx >> 7, pc = idx & 127, c = pc >> 1, h = pc & 1;
+        const int2 inf = rinf[row];
+        const int colc = min(n * 64 + c, P.N - 1), hh = 8 * h < inf.y ? 8 * h : 0;
+        bst[(row * 64 + (c & 7) * 8 + (c >> 3)) * 2 + h] =
+            ld16(a.pool + (size_t)inf.x * a.slot_stride + P.b_off + (size_t)colc * inf.y + hh);
+    }
+    __syncthreads();
+}
+
+// SILU: the MLP's gated mode (gate and up summed, H = silu(gate) * up).
+template <bool SILU>
 __global__ __launch_bounds__(kEpiThreads) void dec_epi_kernel(DecArgs a) {
     const int tile = blockIdx.x;
     int p = 0;
@@ -546,18 +578,25 @@ __global__ __launch_bounds__(kEpiThreads) void dec_epi_kernel(DecArgs a) {
     // store nothing (no early exit: every load is issued without waiting on
     // a branch)
     const bool live = t < a.T && col < P.N;
+    const int tt = min(t, a.T - 1), cc = min(col, P.N - 8);
+    __shared__ u32x4 bst[kEpiTok * 64 * 2];
+    __shared__ int2 rinf[kEpiTok];
+    const u32x4* bs = bst + ((threadIdx.x >> 3) * 64 + (cc - n * 64) / 8) * 2;
     float acc[8];
-    epi_acc(a, p, n, min(t, a.T - 1), min(col, P.N - 8), acc);
+    dec_epi_stage(a, p, n, tt, bst, rinf);
+    epi_acc(a, p, n, tt, cc, bs, acc);
+    if constexpr (SILU) {
+        // every thread stages and sums up as well (the barriers are uniform)
+        float up[8];
+        dec_epi_stage(a, 1, n, tt, bst, rinf);
+        epi_acc(a, 1, n, tt, cc, bs, up);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[c] = acc[c] / (1.f + __expf(-acc[c])) * up[c];
+    }
     if (!live) return;
     if (a.mlp_act < 0) {
         *reinterpret_cast<u32x4*>(P.out + (size_t)t * P.N + col) = pack_bf16x8(acc);
         return;
-    }
-    if (a.mlp_act == BDLORA_ACT_SILU_MUL) {
-        float up[8];
-        epi_acc(a, 1, n, t, col, up);
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[c] = acc[c] / (1.f + __expf(-acc[c])) * up[c];
     }
     // H[t][col .. col + 7] -> fragment (t / 16, col / 32), lane (t % 16) + 16 ((col % 32) / 8)
     const size_t f = ((size_t)(t >> 4) * a.h_KS + (col >> 5)) * kFrag + ((t & 15) + 16 * ((col & 31) >> 3)) * 8;
@@ -570,7 +609,11 @@ hipError_t launch_dec_epi(const DecArgs& a, hipStream_t s) {
     if (a.T > kDecodeMaxT || a.main_grid <= 0) return hipErrorInvalidValue;
     if (a.mlp_act >= 0 && (!a.h_dst || (a.mlp_act == BDLORA_ACT_SILU_MUL && (a.n_proj != 2 || a.p[1].N != a.p[0].N))))
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL(dec_epi_kernel, dim3(grid, (a.T + kEpiTok - 1) / kEpiTok), dim3(kEpiThreads), 0, s, a);
+    const dim3 g(grid, (a.T + kEpiTok - 1) / kEpiTok);
+    if (a.mlp_act == BDLORA_ACT_SILU_MUL)
+        hipLaunchKernelGGL(dec_epi_kernel<true>, g, dim3(kEpiThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(dec_epi_kernel<false>, g, dim3(kEpiThreads), 0, s, a);
     return hipGetLastError();
 }
 
