@@ -532,7 +532,7 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 // projection 1 being up), stored in bf16 in the fragment layout the second
 // projection reads (rows = tokens, k = these columns).
 // Epilogue workgroups: kEpiTok tokens x 8 column octets of one 64-column tile.
-constexpr int kEpiTok = 16;
+constexpr int kEpiTok = 8;
 constexpr int kEpiThreads = kEpiTok * 8;
 
 // Ranks 0..15 of B^T for the workgroup's tokens and 64-column tile n of
