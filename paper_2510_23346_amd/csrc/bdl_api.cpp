@@ -607,10 +607,12 @@ struct Shapes {
 
 // Column blocks per base-GEMM tile: the widest tile (least re-reading of the
 // activations) that still leaves enough workgroups to occupy the chip.
-static Shapes pick_shapes(int T, long long col_blocks = 0) {
+static Shapes pick_shapes(int T, long long col_blocks = 0, int r8max = bdl::kMaxRank8) {
     Shapes k;
     k.smb = T <= 512 ? 1 : 4;
-    k.snb = T <= 512 ? 1 : 4;
+    // prefill shrink items: 64 rank columns, or 32 when no adapter is wider
+    // (a rank-32 adapter's slice then fills its chunk instead of half of it)
+    k.snb = T <= 512 ? 1 : (r8max <= 32 ? 2 : 4);
     k.gmb = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
     const long long row_tiles = (T + 16 * k.gmb - 1) / (16 * k.gmb);
     const long long blocks = col_blocks * row_tiles;
@@ -807,7 +809,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     const Layout& L = P->L;
     long long col_blocks = 0;
     for (int i = 0; i < n; ++i) col_blocks += L.proj[projs[i]].N / 16;
-    const Shapes k = pick_shapes(T, col_blocks);
+    const Shapes k = pick_shapes(T, col_blocks, L.r8max);
     const int mts = 16 * k.smb, nts = 16 * k.snb;
     const int MT = 16 * k.gmb, NT = 16 * k.gnb;
 
