@@ -288,9 +288,9 @@ int bdlora_adapter_elems(const bdlora_proj_desc* projs, int32_t n_projs, int32_t
 /* Device memory a pool with these arguments would hold: adapter slabs
  * (every slot sized for max_rank, ranks padded to multiples of 8) and the
  * per-batch workspace (when max_tokens is above BDLORA_DECODE_MAX_T it
- * includes a fixed 64 MiB of fp32 partial tiles, used in turn by the split
- * shrink, the medium-batch base product and the large-tile GEMM's split
- * tiles).  Pure host function; validates the arguments as
+ * includes a fixed 64 MiB of fp32 partial tiles for the medium-batch base
+ * product and the large-tile GEMM's split tiles, and 32 MiB for the split
+ * shrink's partials).  Pure host function; validates the arguments as
  * bdlora_create_pool does (except the device). */
 int bdlora_pool_size(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots,
                      int32_t max_rank, int32_t max_tokens, int64_t* slab_bytes,
@@ -321,7 +321,10 @@ int bdlora_profile_end(bdlora_pool_t pool, float* ms, int32_t* n);
  *   BDLORA_PATH_MEDIUM  all rows of the batch in one tile (bf16 weights,
  *                       T <= 256, layers whose weight is large against the
  *                       fp32 partials), then an epilogue that adds the
- *                       partials and the expand
+ *                       partials and the expand; the shrink runs beside the
+ *                       base product on a stream the pool owns, forked from
+ *                       the caller's stream after the plan and joined back
+ *                       before the epilogue (graph capture follows the fork)
  *   BDLORA_PATH_LARGE   256 x 256 tiles (bf16 weights, T > 256)
  * INVALID_ARG for a null pool or path. */
 #define BDLORA_PATH_DECODE 1

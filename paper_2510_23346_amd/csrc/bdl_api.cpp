@@ -52,6 +52,7 @@ struct Layout {
     long long part_slots = 0;          // decode partial tiles
     long long mlp_elems = 0;           // prefill MLP: gate and up outputs, fp32
     long long bigpart_elems = 0;       // large-tile GEMM: fp32 partials of split tiles
+    long long shrinkpart_elems = 0;    // split shrink: fp32 partials
 };
 
 // Validates the pool arguments and computes the memory layout.
@@ -137,6 +138,9 @@ int make_layout(const bdlora_proj_desc* projs, int n_projs, int max_slots, int m
     // above the decode size)
     L->bigpart_elems = max_tokens > bdl::kDecodeMaxT ? (long long)bdl::kBigPartSlots * bdl::kBigPartElems : 0;
     ws += L->bigpart_elems * 4;
+    // and of the split shrink (which can run beside the base product)
+    L->shrinkpart_elems = max_tokens > bdl::kDecodeMaxT ? bdl::kShrinkPartElems : 0;
+    ws += L->shrinkpart_elems * 4;
     ws += max_slots * 12LL;                                       // slot tables
     L->ws_bytes = ws;
     return BDLORA_OK;
@@ -182,6 +186,12 @@ struct bdlora_pool {
     float* d_part = nullptr;
     float* d_mlp = nullptr;
     float* d_bigpart = nullptr;
+    float* d_shrinkpart = nullptr;
+    // medium batches: the shrink runs on side_stream, forked from the
+    // caller's stream after the prep launch and joined back before the
+    // epilogue
+    hipStream_t side_stream = nullptr;
+    hipEvent_t fork_ev = nullptr, join_ev = nullptr;
     int n_cu = 0;
     uint16_t* d_Xp[bdl::kMaxProjs] = {};
     uint16_t* d_stage = nullptr;
@@ -223,10 +233,14 @@ void free_pool(bdlora_pool* P) {
     f(P->d_part);
     f(P->d_mlp);
     f(P->d_bigpart);
+    f(P->d_shrinkpart);
     for (auto x : P->d_Xp) f(x);
     f(P->d_stage);
     for (auto e : P->prof_ev) (void)hipEventDestroy(e);
     if (P->load_stream) (void)hipStreamDestroy(P->load_stream);
+    if (P->side_stream) (void)hipStreamDestroy(P->side_stream);
+    if (P->fork_ev) (void)hipEventDestroy(P->fork_ev);
+    if (P->join_ev) (void)hipEventDestroy(P->join_ev);
     delete P;
 }
 
@@ -354,6 +368,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_part, L.part_slots * bdl::kPartElems, &tot));
     BDL_TRY(dev_alloc(&P->d_mlp, L.mlp_elems, &tot));
     if (L.bigpart_elems > 0) BDL_TRY(dev_alloc(&P->d_bigpart, L.bigpart_elems, &tot));
+    if (L.shrinkpart_elems > 0) BDL_TRY(dev_alloc(&P->d_shrinkpart, L.shrinkpart_elems, &tot));
     BDL_TRY(dev_alloc(&P->d_perm, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_rowtok, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_rowslot, MT, &tot));
@@ -395,6 +410,9 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     for (int p = 0; p < n_projs; ++p)
         if (int r = hipz(P->d_Z[p], (size_t)std::max(1LL, L.z_elems[p]) * 2)) return r;
     hipError_t e = hipStreamCreateWithFlags(&P->load_stream, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&P->side_stream, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&P->fork_ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&P->join_ev, hipEventDisableTiming);
     if (e != hipSuccess) {
         free_pool(P);
         return fail(BDLORA_ERR_HIP, std::string("hipStreamCreate: ") + hipGetErrorString(e));
@@ -955,13 +973,13 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.cchunks = cch;
     // Small batches over many adapters (groups of a few scattered tokens, at
     // most 8 per loaded adapter on average) split each shrink item's K over
-    // the XCDs, partials in the split-partial workspace (which the GEMM
-    // launches reuse afterwards).  Few large groups read X about once
-    // anyway; there the split would only add the partials' traffic.
+    // the XCDs, partials in their own workspace.  Few large groups read X
+    // about once anyway; there the split would only add the partials'
+    // traffic.
     fa.shrink_kp = 1;
-    if (T <= 512 && T <= 8 * n_loaded && P->d_bigpart &&
-        (long long)n * fa.items_bound * cch * bdl::kShrinkKP * mts * nts <=
-            (long long)bdl::kBigPartSlots * bdl::kBigPartElems)
+    fa.shrinkpart = P->d_shrinkpart;
+    if (T <= 512 && T <= 8 * n_loaded && P->d_shrinkpart &&
+        (long long)n * fa.items_bound * cch * bdl::kShrinkKP * mts * nts <= L.shrinkpart_elems)
         fa.shrink_kp = bdl::kShrinkKP;
     fa.tile_oct = P->d_tile_oct;
     fa.oct_cap = oct_cap(L, MT);
@@ -1017,9 +1035,21 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     if (ev) BDL_HIP(hipEventRecord(ev[0], s));
     BDL_HIP(bdl::launch_prep(pa, s));
     if (ev) BDL_HIP(hipEventRecord(ev[1], s));
-    if (ev) BDL_HIP(hipEventRecord(ev[2], s));
-    BDL_HIP(bdl::launch_shrink(fa, k.smb, k.snb, s));
-    if (ev) BDL_HIP(hipEventRecord(ev[3], s));
+    // Medium batches: the shrink (Z for the epilogue) and the base product
+    // are independent, and both stream HBM; the shrink runs on the pool's
+    // side stream beside the base product and is joined back before the
+    // epilogue.  (Under graph capture the side stream joins the capture
+    // through the fork event.)
+    hipStream_t ss = s;
+    if (mid) {
+        BDL_HIP(hipEventRecord(P->fork_ev, s));
+        BDL_HIP(hipStreamWaitEvent(P->side_stream, P->fork_ev, 0));
+        ss = P->side_stream;
+    }
+    if (ev) BDL_HIP(hipEventRecord(ev[2], ss));
+    BDL_HIP(bdl::launch_shrink(fa, k.smb, k.snb, ss));
+    if (ev) BDL_HIP(hipEventRecord(ev[3], ss));
+    if (mid) BDL_HIP(hipEventRecord(P->join_ev, ss));
     if (ev) BDL_HIP(hipEventRecord(ev[4], s));
     if (big) {
         BDL_HIP(bdl::launch_gemm_big(fa, s));
@@ -1030,6 +1060,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
             BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
     }
     if (ev) BDL_HIP(hipEventRecord(ev[5], s));
+    if (mid) BDL_HIP(hipStreamWaitEvent(s, P->join_ev, 0));
     if (ev) BDL_HIP(hipEventRecord(ev[6], s));
     if (mid) BDL_HIP(bdl::launch_mid_epi(fa, s));
     if (ev) BDL_HIP(hipEventRecord(ev[7], s));

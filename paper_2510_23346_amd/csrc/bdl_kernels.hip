@@ -45,7 +45,8 @@ constexpr int kStages = 3;                    // k-steps of loads kept in flight
 //    cut into kShrinkKP ranges, range k running on XCD k (workgroup b runs
 //    on XCD b mod 8, and the flat index keeps the range in its low bits):
 //    each XCD fetches only its range of X.  The ranges store fp32 partial
-//    tiles; shrink_reduce_kernel adds them in range order and writes Z.
+//    tiles (their own workspace); shrink_reduce_kernel adds them in range
+//    order and writes Z.
 // --------------------------------------------------------------------------
 
 template <int MB, int NB>
@@ -98,7 +99,7 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
 
         if (KP > 1) {
             // partial tile of range kp (row-major MT x NT), summed by shrink_reduce_kernel
-            float* dst = a.bigpart + (size_t)flat * (MT * NT);
+            float* dst = a.shrinkpart + (size_t)flat * (MT * NT);
             for (int idx = threadIdx.x; idx < MT * NT; idx += kThreads)
                 dst[idx] = red[(idx / NT) * LD + idx % NT];
             __syncthreads();
@@ -140,7 +141,7 @@ __global__ __launch_bounds__(256) void shrink_reduce_kernel(FwdArgs a) {
         if (c0 >= ncols) continue;
         const float sc = a.scale[slot];
         const int* prow = a.perm + it.y;
-        const float* src = a.bigpart + (size_t)f * KP * (MT * NT);
+        const float* src = a.shrinkpart + (size_t)f * KP * (MT * NT);
         for (int idx = threadIdx.x; idx < MT * NT; idx += 256) {
             const int r = idx / NT, c = idx - (idx / NT) * NT, cg = c0 + c;
             if (r < nrows && cg < ncols) {
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(256) void shrink_reduce_kernel(FwdArgs a) {
 
 hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
     const int KP = a.shrink_kp;
-    if (KP != 1 && (KP != kShrinkKP || !a.bigpart)) return hipErrorInvalidValue;
+    if (KP != 1 && (KP != kShrinkKP || !a.shrinkpart)) return hipErrorInvalidValue;
     const int tiles = a.n_proj * a.items_bound * a.cchunks;
     const int total = tiles * KP;
     // a multiple of 8 (with KP = 8 each workgroup keeps one k-range)

@@ -18,6 +18,7 @@ constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-til
 constexpr int kBigPartElems = kBigM * kBigN;
 constexpr int kMidMaxT = 256;             // medium-batch base GEMM: largest batch (all rows in one tile)
 constexpr int kShrinkKP = 8;              // shrink k-ranges per item when split (one per XCD)
+constexpr long long kShrinkPartElems = 8LL << 20;   // fp32 partials of the split shrink (32 MiB)
 
 // One projection of a forward launch.
 struct ProjLaunch {
@@ -60,8 +61,9 @@ struct FwdArgs {
     const int* meta;          // [1] number of shrink items
     int items_bound;          // shrink: upper bound on items
     int cchunks;              // shrink: column chunks per item (upper bound)
-    int shrink_kp;            // shrink: k-ranges per item (1, or kShrinkKP: fp32 partials in bigpart
-                              // that a second launch sums into Z)
+    int shrink_kp;            // shrink: k-ranges per item (1, or kShrinkKP: fp32 partials in
+                              // shrinkpart that a second launch sums into Z)
+    float* shrinkpart;        // split shrink: fp32 partials (kShrinkPartElems)
     const int* tile_oct;      // expand octet codes per row tile (-1 padded)
     int oct_cap;              // entries per row tile in tile_oct
     int tiles_m;              // base GEMM: row tiles
