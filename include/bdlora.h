@@ -320,7 +320,8 @@ int bdlora_profile_end(bdlora_pool_t pool, float* ms, int32_t* n);
  *   BDLORA_PATH_TILE64  64-row tiles, base product with the fused expand
  *   BDLORA_PATH_MEDIUM  all rows of the batch in one tile (bf16 weights,
  *                       T <= 256, layers whose weight is large against the
- *                       fp32 partials), then an epilogue that adds the
+ *                       fp32 partials or batches of at most 8 tokens per
+ *                       loaded adapter), then an epilogue that adds the
  *                       partials and the expand; the shrink runs beside the
  *                       base product on a stream the pool owns, forked from
  *                       the caller's stream after the plan and joined back

@@ -892,14 +892,17 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         // The partials' round trip (written, then read by the epilogue) must
         // stay well below the weight bytes the launch saves re-reading: short
         // K ranges (small layers) make the partials as large as the weight,
-        // and then the 64-row kernel is as fast or faster.
+        // and then the 64-row kernel is as fast or faster -- unless the batch
+        // spreads over many adapters (at most 8 tokens per loaded adapter):
+        // its shrink is then long, and this path runs it beside the base
+        // product instead of before it.
         long long part_bytes = 0, w_bytes = 0;
         for (int i = 0; i < n; ++i) {
             const ProjInfo& pi = L.proj[projs[i]];
             part_bytes += (long long)((pi.N + mid_tn - 1) / mid_tn) * mid_split[i] * ((T + 15) / 16 * 16) * mid_tn * 4;
             w_bytes += (long long)pi.N * pi.K * 2;
         }
-        mid = mid && 2 * part_bytes * 10 <= 6 * w_bytes;
+        mid = mid && (2 * part_bytes * 10 <= 6 * w_bytes || T <= 8 * n_loaded);
     }
     const int tiles_m = (T + MT - 1) / MT;
     const int tm = big ? (T + bdl::kBigM - 1) / bdl::kBigM : tiles_m;

@@ -18,8 +18,8 @@ Covered here:
   256-column tiles, with ranks from 1 to 64 (the expand's loop past 16
   ranks);
 - edge batches: no adapted token, and one rank-64 adapter for every token;
-- the path each shape takes (the byte rule that keeps small layers on the
-  64-row kernel).
+- the path each shape takes (the rule that keeps small layers with few
+  adapters on the 64-row kernel).
 Every case checks that the path ran (pool.last_path()).  The error rule is
 as in test_gpu_parity.
 """
@@ -94,6 +94,20 @@ def test_medium_parity_70b_shard(torch_cuda, T):
     _check_all(layer, ids, ys, yb, f"T={T}")
 
 
+@pytest.mark.parametrize("T", [100, 256])
+def test_medium_parity_8b_shard_many_adapters(torch_cuda, T):
+    """The 8B layer shard with 32 resident rank-16 adapters and Zipf ids:
+    too small for the byte rule, but at most 8 tokens per loaded adapter,
+    so the medium path runs its long shrink beside the base product."""
+    spec = dataclasses.replace(wl.workload(1), name=f"8b-layer-T{T}", T=T, seed=800 + T)
+    ids = wl.draw_ids(spec)
+    active = sorted(int(s) for s in np.unique(ids) if s >= 0)
+    layer, ys, yb, path = _run(torch_cuda, spec, list(range(spec.n_slots)))
+    assert path == "medium", f"T={T}: the batch took the {path} path"
+    _check_all(layer, ids, ys, yb, f"8b T={T}")
+    assert len(active) > 8
+
+
 def _ragged_projs():
     return [
         wl.ProjSpec("qkv", "column", 8192, (1008, 144, 128)),   # slice boundaries inside 256-column tiles
@@ -131,24 +145,27 @@ def test_medium_edge_batches(torch_cuda, T, case):
     _check_all(layer, ids, ys, yb, f"{case} T={T}")
 
 
-@pytest.mark.parametrize("model,T,path", [("llama-3.1-8b", 64, "decode"), ("llama-3.1-70b", 65, "medium"),
-                                          ("llama-3.1-70b", 256, "medium"), ("llama-3.1-70b", 257, "large"),
-                                          ("llama-3.1-8b", 100, "tile64"), ("llama-3.1-8b", 256, "tile64")])
-def test_path_choice(torch_cuda, model, T, path):
+@pytest.mark.parametrize("model,T,n_slots,path", [
+    ("llama-3.1-8b", 64, 2, "decode"), ("llama-3.1-70b", 65, 2, "medium"), ("llama-3.1-70b", 256, 2, "medium"),
+    ("llama-3.1-70b", 257, 2, "large"), ("llama-3.1-8b", 100, 2, "tile64"), ("llama-3.1-8b", 256, 2, "tile64"),
+    ("llama-3.1-8b", 128, 32, "medium"), ("llama-3.1-8b", 256, 32, "medium")])
+def test_path_choice(torch_cuda, model, T, n_slots, path):
     """The launch sequence each batch takes: decode up to 64 tokens, the
-    medium-batch launches for the 70B shard up to 256, the 64-row kernel for
-    the 8B shard (whose weight is too small against the partials of a
-    chip-filling split), the large tiles above 256.  Outputs are checked on
-    a few rows against the oracle."""
+    medium-batch launches for the 70B shard up to 256; for the 8B shard
+    (whose weight is too small against the partials of a chip-filling split)
+    the 64-row kernel, unless the batch spreads over many adapters (at most
+    8 tokens per loaded adapter), whose long shrink the medium path runs
+    beside the base product; the large tiles above 256.  Outputs are checked
+    on a few rows against the oracle."""
     torch = torch_cuda
-    ranks = [16, 8]
+    ranks = [16, 8] * (n_slots // 2)
     rng = np.random.default_rng(T)
     ids = rng.integers(-1, len(ranks), size=T)
-    spec = wl.custom_workload(f"path-{model}-{T}", wl.model_projs(model, 8), T, ranks, scales=[2.0, 1.0],
-                              ids=ids, seed=T)
-    layer = wl.draw_layer(spec, slots=[0, 1])
+    spec = wl.custom_workload(f"path-{model}-{T}-{n_slots}", wl.model_projs(model, 8), T, ranks,
+                              scales=[2.0, 1.0] * (n_slots // 2), ids=ids, seed=T)
+    layer = wl.draw_layer(spec, slots=range(n_slots))
     pool = make_pool(spec, max_tokens=T)
-    load_adapters(pool, spec, [0, 1], cache=layer.adapters)
+    load_adapters(pool, spec, range(n_slots), cache=layer.adapters)
     dl = DeviceLayer(layer)
     pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, dl.out, dl.ids)
     torch.cuda.synchronize()
