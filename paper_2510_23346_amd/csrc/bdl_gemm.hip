@@ -1,5 +1,8 @@
-// Large-tile base GEMM with the fused BD-LoRA expand, for prefill batches.
+// Base GEMMs of batches above the decode size, bf16 weights: the large-tile
+// GEMM with the fused BD-LoRA expand (prefill batches, below), and the
+// medium-batch GEMM with its epilogue (further down).
 //
+// Large-tile GEMM.
 // One workgroup computes a 256 x 256 output tile (tokens x columns) of one
 // projection: out = X W_s + Zhat B, the base product, the adapter expand and
 // their sum of Alg. 1 / Alg. 2 in one pass over the tile.  The operands are

@@ -1,7 +1,9 @@
 // HIP kernels of the BD-LoRA shard forward for gfx950 (MI355X).
 //
 // A forward launch of one token batch over P projections (all sharing the
-// tokens' adapter ids) runs three kernels on the caller's stream:
+// tokens' adapter ids) above the decode size runs these kernels on the
+// caller's stream (medium batches swap step 3 for the medium-batch GEMM and
+// its epilogue in bdl_gemm.hip, large ones for the large-tile GEMM there):
 //
 //  1. prep_kernel   -- workgroup 0 plans the batch: validates ids and groups
 //                      tokens by adapter (counting sort over slots), and
