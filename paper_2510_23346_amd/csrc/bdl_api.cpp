@@ -1041,11 +1041,16 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     // Medium batches: the shrink (Z for the epilogue) and the base product
     // are independent, and both stream HBM; the shrink runs on the pool's
     // side stream beside the base product and is joined back before the
-    // epilogue.  (Under graph capture the side stream joins the capture
-    // through the fork event.)
+    // epilogue.  The base product is enqueued first, so that its workgroups
+    // (one per CU) take the CUs before the shrink's many small ones fill
+    // them.  (Under graph capture the side stream joins the capture through
+    // the fork event.)
     hipStream_t ss = s;
     if (mid) {
         BDL_HIP(hipEventRecord(P->fork_ev, s));
+        if (ev) BDL_HIP(hipEventRecord(ev[4], s));
+        BDL_HIP(bdl::launch_gemm_mid(fa, s));
+        if (ev) BDL_HIP(hipEventRecord(ev[5], s));
         BDL_HIP(hipStreamWaitEvent(P->side_stream, P->fork_ev, 0));
         ss = P->side_stream;
     }
@@ -1053,16 +1058,15 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     BDL_HIP(bdl::launch_shrink(fa, k.smb, k.snb, ss));
     if (ev) BDL_HIP(hipEventRecord(ev[3], ss));
     if (mid) BDL_HIP(hipEventRecord(P->join_ev, ss));
-    if (ev) BDL_HIP(hipEventRecord(ev[4], s));
-    if (big) {
-        BDL_HIP(bdl::launch_gemm_big(fa, s));
-    } else {
-        if (mid)
-            BDL_HIP(bdl::launch_gemm_mid(fa, s));
+    if (!mid) {
+        // the fused expand of the 64-row and large tiles reads Z: after the shrink
+        if (ev) BDL_HIP(hipEventRecord(ev[4], s));
+        if (big)
+            BDL_HIP(bdl::launch_gemm_big(fa, s));
         else
             BDL_HIP(bdl::launch_gemm(fa, k.gmb, k.gnb, s));
+        if (ev) BDL_HIP(hipEventRecord(ev[5], s));
     }
-    if (ev) BDL_HIP(hipEventRecord(ev[5], s));
     if (mid) BDL_HIP(hipStreamWaitEvent(s, P->join_ev, 0));
     if (ev) BDL_HIP(hipEventRecord(ev[6], s));
     if (mid) BDL_HIP(bdl::launch_mid_epi(fa, s));
