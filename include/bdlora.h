@@ -71,6 +71,9 @@ extern "C" {
  * expand fused in, or for medium batches on large layers base partials and
  * an epilogue; see bdlora_last_path). */
 #define BDLORA_DECODE_MAX_T 64
+/* Largest number of segments a bdlora_segments batch may have (the segments
+ * travel with the launch, by value). */
+#define BDLORA_MAX_SEGMENTS 256
 /* Activation between the two projections of bdlora_forward_mlp. */
 #define BDLORA_ACT_NONE     0   /* H = first projection's output (Alg. 1)  */
 #define BDLORA_ACT_SILU_MUL 1   /* H = silu(gate) * up (gated MLP)         */
@@ -89,6 +92,25 @@ extern "C" {
 
 typedef struct bdlora_pool* bdlora_pool_t;
 
+/* A batch given as segments instead of per-token ids (heterogeneous
+ * batching, Sec. 2 on S-LoRA: the requests of a batch each name one
+ * adapter, and a prefill request is a contiguous run of tokens).  Host
+ * arrays of n_seg entries: segment i covers tokens start[i] ..
+ * start[i] + len[i] - 1 and uses adapter slot[i] (-1 = no adapter).  The
+ * segments must tile 0 .. T-1 in order: start[0] = 0, len[i] >= 1,
+ * start[i+1] = start[i] + len[i], start[n_seg-1] + len[n_seg-1] = T.
+ * 1 <= n_seg <= BDLORA_MAX_SEGMENTS.  Adjacent segments may name the same
+ * slot.  The forward validates them on the host before anything is
+ * enqueued and copies them into the launch, so the arrays may be freed or
+ * reused as soon as the call returns (also under graph capture: a captured
+ * forward replays the segments it was given). */
+typedef struct {
+    int32_t n_seg;
+    const int32_t* start;
+    const int32_t* len;
+    const int32_t* slot;
+} bdlora_segments;
+
 /* One projection on one shard.  d_in: local input width (K), a multiple of
  * 32.  slice_out[i]: local output width of slice i, a multiple of 16.
  * kind only documents the sharding (BDLORA_COLUMN / BDLORA_ROW); both kinds
@@ -105,16 +127,27 @@ typedef struct {
 
 /* Create an adapter pool on HIP device `device` for the `n_projs`
  * projections described by `projs` (1..BDLORA_MAX_PROJS).  The pool has
- * `max_slots` adapter slots (1..BDLORA_MAX_SLOTS), each sized for rank
- * `max_rank` (0..BDLORA_MAX_RANK) on every projection, plus a workspace for
+ * adapter slots each sized for rank `max_rank` (0..BDLORA_MAX_RANK) on every
+ * projection (bdlora_layout_slot_bytes bytes per slot), plus a workspace for
  * batches of up to `max_tokens` tokens.  Paper: the GPU-side adapter cache
  * of App. C.2 / App. F (adapters loaded once, reused by every batch).
+ * Slot count and adapter memory:
+ *   pool_bytes = 0:  max_slots slots (1..BDLORA_MAX_SLOTS);
+ *   pool_bytes > 0, max_slots = 0: as many slots as pool_bytes holds
+ *                    (at most BDLORA_MAX_SLOTS; OOM if not even one);
+ *   pool_bytes > 0, max_slots > 0: max_slots slots, which must fit in
+ *                    pool_bytes (else OOM, nothing allocated).
+ * pool_bytes bounds the adapter slabs only; the workspace comes on top
+ * (bdlora_pool_size reports both).  bdlora_pool_slots gives the count.
  * All memory is allocated here; forward calls allocate nothing.
  * On success *out receives the handle.  Errors: INVALID_ARG, SHAPE, OOM, HIP,
  * UNSUPPORTED (device is not gfx950). */
 int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots,
-                       int32_t max_rank, int32_t max_tokens, int32_t device,
+                       int32_t max_rank, int32_t max_tokens, int64_t pool_bytes, int32_t device,
                        bdlora_pool_t* out);
+
+/* Number of adapter slots of the pool.  Errors: INVALID_ARG. */
+int bdlora_pool_slots(bdlora_pool_t pool, int32_t* slots);
 
 /* Free every device and host resource of the pool (waits for its work). */
 int bdlora_destroy_pool(bdlora_pool_t pool);
@@ -144,6 +177,21 @@ int bdlora_load_adapter(bdlora_pool_t pool, int32_t slot, int32_t rank, float sc
 
 /* Bytes of one adapter slot of the pool (0 for a null pool). */
 int64_t bdlora_slot_bytes(bdlora_pool_t pool);
+
+/* Bytes of one adapter slot of any pool created with these projections and
+ * max_rank (pure host function; App. C.2 compact storage, ranks padded to
+ * multiples of 8).  Errors: INVALID_ARG, SHAPE. */
+int bdlora_layout_slot_bytes(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_rank,
+                             int64_t* bytes);
+
+/* bdlora_pack_adapter_host without a pool (pure host code, no device
+ * needed): packs one adapter for every pool created with these projections
+ * and max_rank, into slab_host (bdlora_layout_slot_bytes bytes).  Lets a
+ * process without a GPU prepare a host-side adapter cache.  Errors:
+ * INVALID_ARG (bad rank, null pointer, non-finite value), SHAPE. */
+int bdlora_pack_adapter_layout(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_rank,
+                               int32_t rank, const uint16_t* const* A_host,
+                               const uint16_t* const* B_host, void* slab_host);
 
 /* Pack one adapter on the host into the pool's slot layout (for a host-side
  * cache): slab_host receives bdlora_slot_bytes(pool) bytes (padding zeroed).
@@ -209,21 +257,41 @@ int bdlora_pack_weight_int4(const void* q, const void* scales, void* W_packed, i
  * projection): out = X W_s^T + scale_a (X A_a) B_a per token.
  * proj: index into the pool's projection list.  X: device [T x d_in];
  * W: device, the base weight [d_out_s x d_in] packed by bdlora_pack_weight
- * (or bdlora_pack_weight_int4 for an INT4 projection);
- * ids: device int32 [T]; out: device [T x d_out_s].
- * T: 0..max_tokens (T = 0 enqueues nothing).  Errors: INVALID_ARG, SHAPE, HIP. */
+ * (or bdlora_pack_weight_int4 for an INT4 projection); out: device
+ * [T x d_out_s].  The batch's adapters come either as ids (device int32
+ * [T], one per token; segs = NULL) or as segs (host segments, see
+ * bdlora_segments; ids = NULL); exactly one of the two.  With segs an id
+ * that names no loaded slot fails the call with BAD_ADAPTER before anything
+ * is enqueued; with ids it is treated as -1 on the device and raises the
+ * sticky device error flag.  Both forms give bit-identical outputs for the
+ * same batch.  T: 0..max_tokens (T = 0 enqueues nothing).
+ *
+ * Graph capture.  A forward may be captured in a HIP graph; the replay
+ * repeats the launches with the arguments of the capture.  The launch
+ * geometry of a decode batch (T <= BDLORA_DECODE_MAX_T) given as ids covers
+ * at most min(T, adapters loaded when the call is made) distinct adapters:
+ * if a replay's ids use more distinct adapters than that (adapters loaded
+ * after the capture), the tokens of the adapters past the bound (in
+ * ascending slot order) get the base output only and the device error flag
+ * is raised.  Recapture after loading adapters.  Larger batches have no such
+ * bound, and segments, checked against the adapters loaded when the call is
+ * made, stay within it.
+ * Errors: INVALID_ARG, BAD_ADAPTER (segs only), SHAPE, HIP. */
 int bdlora_forward_shard(bdlora_pool_t pool, int32_t proj, const void* X, const void* W,
-                         const int32_t* ids, int32_t T, void* out, void* stream);
+                         const int32_t* ids, const bdlora_segments* segs, int32_t T, void* out,
+                         void* stream);
 
-/* Several projection calls that share the token batch and its ids (the
- * projections of one decoder layer), enqueued as one plan, one shrink and
- * one base-plus-expand launch.  projs[i] indexes the pool's projection
- * list; X[i], W[i], out[i] are device pointers as for bdlora_forward_shard
- * (host arrays of n pointers).  n: 1..BDLORA_MAX_PROJS; the same projection
- * may not appear twice.  Errors: as bdlora_forward_shard. */
+/* Several projection calls that share the token batch and its ids or
+ * segments (the projections of one decoder layer), enqueued as one plan,
+ * one shrink and one base-plus-expand launch.  projs[i] indexes the pool's
+ * projection list; X[i], W[i], out[i] are device pointers as for
+ * bdlora_forward_shard (host arrays of n pointers).  n: 1..BDLORA_MAX_PROJS;
+ * the same projection may not appear twice.  Errors: as
+ * bdlora_forward_shard. */
 int bdlora_forward_layer(bdlora_pool_t pool, int32_t n, const int32_t* projs,
                          const void* const* X, const void* const* W, void* const* out,
-                         const int32_t* ids, int32_t T, void* stream);
+                         const int32_t* ids, const bdlora_segments* segs, int32_t T,
+                         void* stream);
 
 /* One device's share of a BD-LoRA MLP (Alg. 1, App. B): the first
  * (column-parallel) projection(s), the intermediate H, then the
@@ -239,14 +307,15 @@ int bdlora_forward_layer(bdlora_pool_t pool, int32_t n, const int32_t* projs,
  * projections' width must equal down's d_in.
  * X: device [T x d_in] bf16, shared by the first projections; W_first:
  * host array of 1 or 2 device pointers to packed weights; W_down: packed
- * weight of down; out: device [T x d_out of down]; ids: device int32 [T].
+ * weight of down; out: device [T x d_out of down]; ids (device int32 [T])
+ * or segs (host segments), exactly one, as for bdlora_forward_shard.
  * T: 0..max_tokens.  Enqueued on `stream`; uses the pool's workspace, so
  * calls on one pool must share one stream.
- * Errors: INVALID_ARG (bad act, indices, kinds or null pointers), SHAPE
- * (widths do not chain), HIP. */
+ * Errors: INVALID_ARG (bad act, indices, kinds or null pointers),
+ * BAD_ADAPTER (segs only), SHAPE (widths do not chain), HIP. */
 int bdlora_forward_mlp(bdlora_pool_t pool, int32_t act, const int32_t* first, int32_t down,
                        const void* X, const void* const* W_first, const void* W_down, void* out,
-                       const int32_t* ids, int32_t T, void* stream);
+                       const int32_t* ids, const bdlora_segments* segs, int32_t T, void* stream);
 
 /* Host-side plan of a batch (the integer bookkeeping of heterogeneous
  * batching, Sec. 2 on S-LoRA), a pure host function: validates host ids

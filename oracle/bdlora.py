@@ -1,5 +1,10 @@
 """BD-LoRA shard forward in float64 -- TEST INFRASTRUCTURE ONLY (see package doc).
 
+The parity reference is the float64 evaluation.  ``shard_forward`` and the
+layer helpers also take ``dtype=np.float32``: the same steps in single
+precision, the plain fp32 CPU implementation whose speed the benchmark
+reports as its CPU baseline.
+
 Notation follows the paper.  ``X`` is ``[S, d_in]`` (S tokens), base weights
 are in the paper's orientation ``W [d_in, d_out]`` so the base product is
 ``X W``; a LoRA adapter is ``A [d_in, r]``, ``B [r, d_out]`` with scale
@@ -51,18 +56,19 @@ def _f64(a) -> np.ndarray:
 # --------------------------------------------------------------------------
 
 def shard_forward(X: np.ndarray, W: np.ndarray, ids: Sequence[int],
-                  adapters: Dict[int, ProjAdapter], slices: Sequence[int]) -> np.ndarray:
+                  adapters: Dict[int, ProjAdapter], slices: Sequence[int],
+                  dtype=np.float64) -> np.ndarray:
     """One projection on one shard for a heterogeneous batch (Alg. 2 / Alg. 1).
 
     ``X [S, d_in]``; ``W [d_in, sum(slices)]`` (paper orientation); ``ids[S]``
     are adapter ids (-1: none); ``adapters[slot] = (gamma, A_list, B_list)``
     where slice ``j`` has ``A_j [d_in, r]`` and ``B_j [r, slices[j]]``.  The
     output of slice ``j`` occupies columns ``sum(slices[:j]) ...`` (for the
-    attention input projection: ``[q_s | k_s | v_s]``).  Returns float64
-    ``[S, sum(slices)]``.
+    attention input projection: ``[q_s | k_s | v_s]``).  Returns
+    ``[S, sum(slices)]`` in ``dtype`` (float64 unless asked otherwise).
     """
-    X = _f64(X)
-    W = _f64(W)
+    X = np.asarray(X, dtype=dtype)
+    W = np.asarray(W, dtype=dtype)
     ids = np.asarray(ids, dtype=np.int64)
     S, d_in = X.shape
     if W.shape != (d_in, int(sum(slices))):
@@ -79,39 +85,39 @@ def shard_forward(X: np.ndarray, W: np.ndarray, ids: Sequence[int],
         Xg = X[rows]
         col = 0
         for j, n_out in enumerate(slices):
-            A = _f64(A_list[j])
-            B = _f64(B_list[j])
+            A = np.asarray(A_list[j], dtype=dtype)
+            B = np.asarray(B_list[j], dtype=dtype)
             if A.shape[0] != d_in or B.shape[1] != n_out or A.shape[1] != B.shape[0]:
                 raise ValueError(f"adapter {slot} slice {j}: bad shapes {A.shape} {B.shape}")
             Z = Xg @ A                                 # local adapter projection
             Y_adapter = Z @ B                          # expand
-            Y[rows, col:col + n_out] += float(gamma) * Y_adapter
+            Y[rows, col:col + n_out] += dtype(gamma) * Y_adapter
             col += n_out
     return Y
 
 
-def layer_forward(layer) -> List[np.ndarray]:
+def layer_forward(layer, dtype=np.float64) -> List[np.ndarray]:
     """All projection calls of a drawn layer (``workloads.LayerInputs``).
 
     Each projection uses its own ``X`` and ``W`` (the inputs are independent
     synthetic tensors), the shared per-token ids and the shared adapters.
-    Returns float64 outputs in the paper orientation ``[S, d_out_s]``.
+    Returns outputs (in ``dtype``) in the paper orientation ``[S, d_out_s]``.
     """
     outs = []
     for p, pi in enumerate(layer.projs):
         ad = {s: (a.scale, a.A[p], a.B[p]) for s, a in layer.adapters.items()}
-        outs.append(shard_forward(pi.X, pi.W, layer.ids, ad, pi.spec.slices))
+        outs.append(shard_forward(pi.X, pi.W, layer.ids, ad, pi.spec.slices, dtype))
     return outs
 
 
-def layer_forward_rows(layer, rows: Sequence[int]) -> List[np.ndarray]:
+def layer_forward_rows(layer, rows: Sequence[int], dtype=np.float64) -> List[np.ndarray]:
     """Like :func:`layer_forward` but only for the token rows ``rows``
     (each output row depends on its own token only)."""
     rows = np.asarray(rows, dtype=np.int64)
     outs = []
     for p, pi in enumerate(layer.projs):
         ad = {s: (a.scale, a.A[p], a.B[p]) for s, a in layer.adapters.items()}
-        outs.append(shard_forward(pi.X[rows], pi.W, layer.ids[rows], ad, pi.spec.slices))
+        outs.append(shard_forward(pi.X[rows], pi.W, layer.ids[rows], ad, pi.spec.slices, dtype))
     return outs
 
 

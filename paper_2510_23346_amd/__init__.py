@@ -19,12 +19,13 @@ __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
     "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T",
     "ACT_NONE", "ACT_SILU_MUL", "WEIGHT_BF16", "WEIGHT_INT4_G128", "pack_weight_int4",
-    "packed_weight_bytes",
+    "packed_weight_bytes", "MAX_SEGMENTS", "Segments", "layout_slot_bytes", "pack_adapter_layout",
 ]
 
 COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
+MAX_SEGMENTS = 256      # BDLORA_MAX_SEGMENTS: most segments of a batch given as segments
 ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections
 # BDLORA_PATH_*: launch sequence of a forward (0: none yet)
 PATHS = {0: "", 1: "decode", 2: "tile64", 3: "medium", 4: "large"}
@@ -49,8 +50,17 @@ class ProjDesc(ctypes.Structure):
                 ("slice_out", _c.c_int32 * MAX_SLICES), ("weight_format", _c.c_int32)]
 
 
+class _Segs(ctypes.Structure):
+    _fields_ = [("n_seg", _c.c_int32), ("start", _IP), ("len", _IP), ("slot", _IP)]
+
+
+_SP = _c.POINTER(_Segs)
+
 _SIGS = {
-    "bdlora_create_pool": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _I, _I, _c.POINTER(_P)]),
+    "bdlora_create_pool": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _I, _c.c_int64, _I, _c.POINTER(_P)]),
+    "bdlora_pool_slots": (_I, [_P, _IP]),
+    "bdlora_layout_slot_bytes": (_I, [_c.POINTER(ProjDesc), _I, _I, _LP]),
+    "bdlora_pack_adapter_layout": (_I, [_c.POINTER(ProjDesc), _I, _I, _I, _c.POINTER(_P), _c.POINTER(_P), _P]),
     "bdlora_destroy_pool": (_I, [_P]),
     "bdlora_load_adapter": (_I, [_P, _I, _I, _c.c_float, _c.POINTER(_P), _c.POINTER(_P)]),
     "bdlora_unload_adapter": (_I, [_P, _I]),
@@ -58,9 +68,9 @@ _SIGS = {
     "bdlora_pack_adapter_host": (_I, [_P, _I, _c.POINTER(_P), _c.POINTER(_P), _P]),
     "bdlora_load_adapter_packed": (_I, [_P, _I, _I, _c.c_float, _P, _P]),
     "bdlora_load_adapters_packed": (_I, [_P, _I, _I, _IP, _c.POINTER(_c.c_float), _P, _P]),
-    "bdlora_forward_shard": (_I, [_P, _I, _P, _P, _P, _I, _P, _P]),
-    "bdlora_forward_layer": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _I, _P]),
-    "bdlora_forward_mlp": (_I, [_P, _I, _IP, _I, _P, _c.POINTER(_P), _P, _P, _P, _I, _P]),
+    "bdlora_forward_shard": (_I, [_P, _I, _P, _P, _P, _SP, _I, _P, _P]),
+    "bdlora_forward_layer": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _SP, _I, _P]),
+    "bdlora_forward_mlp": (_I, [_P, _I, _IP, _I, _P, _c.POINTER(_P), _P, _P, _P, _SP, _I, _P]),
     "bdlora_build_plan": (_I, [_IP, _I, _IP, _I, _IP, _IP, _IP, _IP, _IP, _IP]),
     "bdlora_plan_device": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P]),
     "bdlora_get_device_error": (_I, [_P, _P, _IP]),
@@ -196,6 +206,98 @@ def _i32p(a: np.ndarray):
     return a.ctypes.data_as(_IP)
 
 
+class Segments:
+    """A batch in run-length form (``bdlora_segments``): segment ``i``
+    covers tokens ``start[i] .. start[i] + len[i] - 1`` and uses adapter
+    ``slot[i]`` (-1: none).  ``Segments.from_ids(ids)`` makes the maximal
+    runs of a per-token id vector."""
+
+    def __init__(self, start, length, slot):
+        self.start = np.ascontiguousarray(np.asarray(start, dtype=np.int32))
+        self.len = np.ascontiguousarray(np.asarray(length, dtype=np.int32))
+        self.slot = np.ascontiguousarray(np.asarray(slot, dtype=np.int32))
+        if not (self.start.shape == self.len.shape == self.slot.shape) or self.start.ndim != 1:
+            raise ValueError("start, len and slot must be 1-D arrays of one length")
+        self._c = _Segs(int(self.start.size), _i32p(self.start), _i32p(self.len), _i32p(self.slot))
+
+    @classmethod
+    def from_ids(cls, ids) -> "Segments":
+        ids = np.asarray(ids, dtype=np.int64).reshape(-1)
+        if ids.size == 0:
+            return cls([], [], [])
+        cut = np.flatnonzero(np.diff(ids) != 0) + 1
+        start = np.concatenate([[0], cut])
+        length = np.diff(np.concatenate([start, [ids.size]]))
+        return cls(start, length, ids[start])
+
+    @property
+    def n_seg(self) -> int:
+        return int(self.start.size)
+
+    @property
+    def T(self) -> int:
+        return int(self.len.sum())
+
+    def ref(self):
+        return _c.byref(self._c)
+
+
+def _batch(ids, segs):
+    """(ids pointer, segments pointer, T) for a forward call: exactly one of
+    device ``ids`` and host ``segs``."""
+    if (ids is None) == (segs is None):
+        raise ValueError("give exactly one of ids and segs")
+    if segs is not None:
+        if not isinstance(segs, Segments):
+            segs = Segments.from_ids(segs)
+        return 0, segs.ref(), segs.T, segs
+    return _ptr(ids), None, int(ids.shape[0]), None
+
+
+def layout_slot_bytes(projs, max_rank: int) -> int:
+    """Bytes of one adapter slot of any pool with these projections and
+    max_rank (pure host)."""
+    arr, norm = _descs(projs)
+    out = _c.c_int64()
+    _check(lib().bdlora_layout_slot_bytes(arr, len(norm), int(max_rank), _c.byref(out)))
+    return out.value
+
+
+def _flat_factors(projs, rank: int, A, B):
+    flatA, flatB, keep = [], [], []
+    for p, (_, d_in, slices) in enumerate(projs):
+        for s, n in enumerate(slices):
+            a = np.ascontiguousarray(np.asarray(A[p][s]).view(np.uint16) if rank else np.zeros((d_in, 0), np.uint16))
+            b = np.ascontiguousarray(np.asarray(B[p][s]).view(np.uint16) if rank else np.zeros((0, n), np.uint16))
+            if a.shape != (d_in, rank) or b.shape != (rank, n):
+                raise ValueError(f"adapter factor shapes {a.shape}, {b.shape} do not match "
+                                 f"({d_in}, {rank}), ({rank}, {n})")
+            keep += [a, b]
+            flatA.append(a.ctypes.data)
+            flatB.append(b.ctypes.data)
+    pa = (_c.c_void_p * max(1, len(flatA)))(*flatA)
+    pb = (_c.c_void_p * max(1, len(flatB)))(*flatB)
+    return pa, pb, keep
+
+
+def pack_adapter_layout(projs, max_rank: int, rank: int, A, B, out=None):
+    """Pack one adapter into the slot layout of pools with these projections
+    and max_rank, on the host without a pool or GPU; returns the uint8
+    slab (``out`` if given)."""
+    arr, norm = _descs(projs)
+    nbytes = layout_slot_bytes(projs, max_rank)
+    if out is None:
+        out = np.empty(nbytes, dtype=np.uint8)
+    n = out.numel() * out.element_size() if hasattr(out, "numel") else out.nbytes
+    if n < nbytes:
+        raise ValueError(f"out must hold {nbytes} bytes")
+    ptr = out.data_ptr() if hasattr(out, "data_ptr") else out.ctypes.data
+    pa, pb, keep = _flat_factors(norm, int(rank), A, B)
+    _check(lib().bdlora_pack_adapter_layout(arr, len(norm), int(max_rank), int(rank), pa, pb, ptr))
+    del keep
+    return out
+
+
 def build_plan(loaded: Sequence[int], ids: Sequence[int]):
     """Host plan (see ``bdlora_build_plan``).  Returns ``(status, vid,
     groups, perm)`` with ``groups`` a list of ``(slot, start, count)``."""
@@ -244,15 +346,18 @@ class Pool:
     """
 
     def __init__(self, projs, max_slots: int, max_rank: int, max_tokens: int, device: int = 0,
-                 weight_formats=None):
+                 weight_formats=None, pool_bytes: int = 0):
         self._arr, self.projs = _descs(projs, weight_formats)
         self.weight_formats = [int(self._arr[i].weight_format) for i in range(len(self.projs))]
-        self.max_slots, self.max_rank, self.max_tokens = int(max_slots), int(max_rank), int(max_tokens)
+        self.max_rank, self.max_tokens = int(max_rank), int(max_tokens)
         self.device = int(device)
         h = _c.c_void_p()
-        _check(lib().bdlora_create_pool(self._arr, len(self.projs), self.max_slots, self.max_rank,
-                                        self.max_tokens, self.device, _c.byref(h)))
+        _check(lib().bdlora_create_pool(self._arr, len(self.projs), int(max_slots), self.max_rank,
+                                        self.max_tokens, int(pool_bytes), self.device, _c.byref(h)))
         self._h = h
+        n = _c.c_int32()
+        _check(lib().bdlora_pool_slots(h, _c.byref(n)))
+        self.max_slots = n.value
         self.loaded = np.zeros(self.max_slots, np.int32)
 
     # -- lifetime ---------------------------------------------------------
@@ -284,22 +389,6 @@ class Pool:
         return out.value
 
     # -- adapters ---------------------------------------------------------
-    def _flat_factors(self, rank: int, A, B):
-        flatA, flatB, keep = [], [], []
-        for p, (_, d_in, slices) in enumerate(self.projs):
-            for s, n in enumerate(slices):
-                a = np.ascontiguousarray(np.asarray(A[p][s]).view(np.uint16) if rank else np.zeros((d_in, 0), np.uint16))
-                b = np.ascontiguousarray(np.asarray(B[p][s]).view(np.uint16) if rank else np.zeros((0, n), np.uint16))
-                if a.shape != (d_in, rank) or b.shape != (rank, n):
-                    raise ValueError(f"adapter factor shapes {a.shape}, {b.shape} do not match "
-                                     f"({d_in}, {rank}), ({rank}, {n})")
-                keep += [a, b]
-                flatA.append(a.ctypes.data)
-                flatB.append(b.ctypes.data)
-        pa = (_c.c_void_p * max(1, len(flatA)))(*flatA)
-        pb = (_c.c_void_p * max(1, len(flatB)))(*flatB)
-        return pa, pb, keep
-
     @property
     def slot_bytes(self) -> int:
         return int(lib().bdlora_slot_bytes(self._h))
@@ -315,7 +404,7 @@ class Pool:
         if n < self.slot_bytes:
             raise ValueError(f"out must hold {self.slot_bytes} bytes")
         ptr = out.data_ptr() if hasattr(out, "data_ptr") else out.ctypes.data
-        pa, pb, keep = self._flat_factors(int(rank), A, B)
+        pa, pb, keep = _flat_factors(self.projs, int(rank), A, B)
         _check(lib().bdlora_pack_adapter_host(self._h, int(rank), pa, pb, ptr))
         del keep
         return out
@@ -349,19 +438,7 @@ class Pool:
         """``A[p][s]``: uint16 bf16 bits ``[d_in, rank]``; ``B[p][s]``:
         ``[rank, slice_out]`` (paper layout), for every projection p and
         slice s of the pool."""
-        flatA, flatB, keep = [], [], []
-        for p, (_, d_in, slices) in enumerate(self.projs):
-            for s, n in enumerate(slices):
-                a = np.ascontiguousarray(np.asarray(A[p][s]).view(np.uint16) if rank else np.zeros((d_in, 0), np.uint16))
-                b = np.ascontiguousarray(np.asarray(B[p][s]).view(np.uint16) if rank else np.zeros((0, n), np.uint16))
-                if a.shape != (d_in, rank) or b.shape != (rank, n):
-                    raise ValueError(f"adapter factor shapes {a.shape}, {b.shape} do not match "
-                                     f"({d_in}, {rank}), ({rank}, {n})")
-                keep += [a, b]
-                flatA.append(a.ctypes.data)
-                flatB.append(b.ctypes.data)
-        pa = (_c.c_void_p * max(1, len(flatA)))(*flatA)
-        pb = (_c.c_void_p * max(1, len(flatB)))(*flatB)
+        pa, pb, keep = _flat_factors(self.projs, int(rank), A, B)
         _check(lib().bdlora_load_adapter(self._h, int(slot), int(rank), float(scale), pa, pb))
         self.loaded[int(slot)] = 1
         del keep
@@ -388,16 +465,23 @@ class Pool:
                 if t.element_size() != 2 or not t.is_contiguous():
                     raise ValueError(f"{name} must be a contiguous 2-byte (bf16) tensor")
 
-    def forward_shard(self, proj: int, X, W, ids, out, T: Optional[int] = None, stream=None):
-        """One projection: ``out = X W^T + scale (X A) B`` per token."""
-        T = int(ids.shape[0]) if T is None else int(T)
+    def forward_shard(self, proj: int, X, W, ids, out, T: Optional[int] = None, stream=None, segs=None):
+        """One projection: ``out = X W^T + scale (X A) B`` per token.  The
+        adapters come as device ``ids`` or as host ``segs`` (a
+        :class:`Segments` or a per-token id sequence turned into runs); pass
+        ``ids=None`` with ``segs``."""
+        ip, sp, T0, keep = _batch(ids, segs)
+        T = T0 if T is None else int(T)
         self._check_io(proj, X, W, out, T)
-        _check(lib().bdlora_forward_shard(self._h, int(proj), _ptr(X), _ptr(W), _ptr(ids), T, _ptr(out),
+        _check(lib().bdlora_forward_shard(self._h, int(proj), _ptr(X), _ptr(W), ip or None, sp, T, _ptr(out),
                                           _stream_handle(stream)))
+        del keep
 
-    def forward_layer(self, projs: Sequence[int], Xs, Ws, outs, ids, T: Optional[int] = None, stream=None):
+    def forward_layer(self, projs: Sequence[int], Xs, Ws, outs, ids, T: Optional[int] = None, stream=None,
+                      segs=None):
         """Several projections sharing the token batch, in one launch set."""
-        T = int(ids.shape[0]) if T is None else int(T)
+        ip, sp, T0, keep = _batch(ids, segs)
+        T = T0 if T is None else int(T)
         n = len(projs)
         for i, p in enumerate(projs):
             self._check_io(p, Xs[i], Ws[i], outs[i], T)
@@ -405,14 +489,16 @@ class Pool:
         xs = (_c.c_void_p * n)(*[_ptr(x) for x in Xs])
         ws = (_c.c_void_p * n)(*[_ptr(w) for w in Ws])
         os_ = (_c.c_void_p * n)(*[_ptr(o) for o in outs])
-        _check(lib().bdlora_forward_layer(self._h, n, pr, xs, ws, os_, _ptr(ids), T, _stream_handle(stream)))
+        _check(lib().bdlora_forward_layer(self._h, n, pr, xs, ws, os_, ip or None, sp, T, _stream_handle(stream)))
+        del keep
 
     def forward_mlp(self, act: int, first: Sequence[int], down: int, X, W_first, W_down, out, ids,
-                    T: Optional[int] = None, stream=None):
+                    T: Optional[int] = None, stream=None, segs=None):
         """One device's share of a BD-LoRA MLP (Alg. 1): ``first`` = [proj]
         (act ACT_NONE) or [gate, up] (ACT_SILU_MUL), then the row projection
         ``down``; ``out`` is down's partial output."""
-        T = int(ids.shape[0]) if T is None else int(T)
+        ip, sp, T0, keep = _batch(ids, segs)
+        T = T0 if T is None else int(T)
         n = len(first)
         for i, p in enumerate(first):
             self._check_io(p, X, W_first[i], None, T)
@@ -420,7 +506,8 @@ class Pool:
         pr = (_c.c_int32 * max(n, 1))(*[int(p) for p in first])
         ws = (_c.c_void_p * max(n, 1))(*[_ptr(w) for w in W_first])
         _check(lib().bdlora_forward_mlp(self._h, int(act), pr, int(down), _ptr(X), ws, _ptr(W_down), _ptr(out),
-                                        _ptr(ids), T, _stream_handle(stream)))
+                                        ip or None, sp, T, _stream_handle(stream)))
+        del keep
 
     def plan_device(self, ids, vid, gslot, gstart, gcount, perm, n_groups, T: Optional[int] = None, stream=None):
         T = int(ids.shape[0]) if T is None else int(T)

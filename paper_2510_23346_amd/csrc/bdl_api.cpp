@@ -157,6 +157,15 @@ struct DeviceGuard {
     }
 };
 
+// The adapters of a batch as the forward got them: device ids, or host
+// segments validated and copied here (they travel with the prep launch).
+struct Batch {
+    const int32_t* ids = nullptr;     // device [T], or null
+    int n_seg = 0;
+    int seg_start[bdl::kMaxSeg];
+    int seg_slot[bdl::kMaxSeg];
+};
+
 }  // namespace
 
 struct bdlora_pool {
@@ -262,9 +271,83 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 }  // namespace
 
+namespace {
+
+// Pack one adapter into the slot layout of L (host memory, slot_stride
+// elements, padding zeroed): the work of bdlora_pack_adapter_host.
+int pack_adapter_slab(const Layout& L, int rank, const uint16_t* const* A_host, const uint16_t* const* B_host,
+                      uint16_t* slab) {
+    if (rank < 0 || rank > L.max_rank) return fail(BDLORA_ERR_INVALID_ARG, "rank out of range 0..max_rank");
+    if (rank > 0 && (!A_host || !B_host)) return fail(BDLORA_ERR_INVALID_ARG, "null factor arrays");
+    const int r8 = rank8(rank);
+    std::memset(slab, 0, (size_t)L.slot_stride * 2);
+    int k = 0;
+    for (int p = 0; p < L.n_projs; ++p) {
+        const ProjInfo& pi = L.proj[p];
+        if (rank == 0) {
+            k += pi.S;
+            continue;
+        }
+        for (int s = 0; s < pi.S; ++s) {
+            if (!A_host[k + s] || !B_host[k + s]) return fail(BDLORA_ERR_INVALID_ARG, "null factor pointer");
+        }
+        // A^T_cat in the fragment layout: row s*r8 + j is column j of A_s
+        // (zero for j >= rank), rows padded to 16; element
+        // [(rb KS + ks) 512 + lane 8 + i] = A^T_cat[16 rb + lane%16][32 ks + 8 (lane/16) + i]
+        const int KS = pi.K / 32, arows = pi.S * r8;
+        uint16_t* da = slab + pi.a_off;
+        for (int row = 0; row < arows; ++row) {
+            const int s = row / r8, j = row - s * r8;
+            if (j >= rank) continue;
+            const uint16_t* a = A_host[k + s];
+            const int rb = row / 16, lr = row % 16;
+            for (int kk = 0; kk < pi.K; ++kk) {
+                const uint16_t v = a[(size_t)kk * rank + j];
+                if ((v & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in A");
+                const int ks = kk / 32, w = kk % 32, lane = lr + 16 * (w / 8), i = w % 8;
+                da[((size_t)rb * KS + ks) * 512 + lane * 8 + i] = v;
+            }
+        }
+        // B^T_cat [N x r8] row-major: row n is column n of its slice's B
+        uint16_t* db = slab + pi.b_off;
+        for (int s = 0; s < pi.S; ++s) {
+            const uint16_t* b = B_host[k + s];
+            const int n_s = pi.slice_out[s];
+            for (int j = 0; j < rank; ++j)
+                for (int n = 0; n < n_s; ++n) {
+                    const uint16_t v = b[(size_t)j * n_s + n];
+                    if ((v & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in B");
+                    db[(size_t)(pi.slice_col[s] + n) * r8 + j] = v;
+                }
+        }
+        k += pi.S;
+    }
+    return BDLORA_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* bdlora_last_error(void) { return g_err.c_str(); }
+
+int bdlora_layout_slot_bytes(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_rank, int64_t* bytes) {
+    if (!bytes) return fail(BDLORA_ERR_INVALID_ARG, "null output");
+    Layout L;
+    int rc = make_layout(projs, n_projs, 1, max_rank, 1, &L);
+    if (rc) return rc;
+    *bytes = L.slot_stride * 2;
+    return BDLORA_OK;
+}
+
+int bdlora_pack_adapter_layout(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_rank, int32_t rank,
+                               const uint16_t* const* A_host, const uint16_t* const* B_host, void* slab_host) {
+    if (!slab_host) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    Layout L;
+    int rc = make_layout(projs, n_projs, 1, max_rank, 1, &L);
+    if (rc) return rc;
+    return pack_adapter_slab(L, rank, A_host, B_host, static_cast<uint16_t*>(slab_host));
+}
 
 int bdlora_adapter_elems(const bdlora_proj_desc* projs, int32_t n_projs, int32_t rank, int64_t* elems) {
     if (!elems) return fail(BDLORA_ERR_INVALID_ARG, "null output");
@@ -325,12 +408,28 @@ int bdlora_build_plan(const int32_t* loaded, int32_t max_slots, const int32_t* i
 }
 
 int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t max_slots, int32_t max_rank,
-                       int32_t max_tokens, int32_t device, bdlora_pool_t* out) {
+                       int32_t max_tokens, int64_t pool_bytes, int32_t device, bdlora_pool_t* out) {
     if (!out) return fail(BDLORA_ERR_INVALID_ARG, "null output handle");
     *out = nullptr;
+    if (pool_bytes < 0) return fail(BDLORA_ERR_INVALID_ARG, "pool_bytes must be >= 0");
+    if (max_slots == 0 && pool_bytes > 0) {
+        // as many slots as the adapter budget holds
+        Layout L1;
+        int rc = make_layout(projs, n_projs, 1, max_rank, max_tokens, &L1);
+        if (rc) return rc;
+        const long long per = L1.slot_stride * 2;
+        const long long n = std::min<long long>(pool_bytes / per, BDLORA_MAX_SLOTS);
+        if (n < 1)
+            return fail(BDLORA_ERR_OOM, "pool_bytes " + std::to_string(pool_bytes) + " holds no adapter slot of " +
+                                            std::to_string(per) + " bytes");
+        max_slots = (int32_t)n;
+    }
     Layout L;
     int rc = make_layout(projs, n_projs, max_slots, max_rank, max_tokens, &L);
     if (rc) return rc;
+    if (pool_bytes > 0 && L.slab_bytes > pool_bytes)
+        return fail(BDLORA_ERR_OOM, std::to_string(max_slots) + " adapter slots need " + std::to_string(L.slab_bytes) +
+                                        " bytes, more than pool_bytes " + std::to_string(pool_bytes));
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || ndev <= 0) {
         (void)hipGetLastError();
@@ -407,6 +506,11 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     if (int r = hipz(P->d_loaded, (size_t)S * 4)) return r;
     if (int r = hipz(P->d_err, 4)) return r;
     if (int r = hipz(P->d_meta, 16)) return r;
+    // plan tables: entries past a batch's counts are never written by the
+    // plan; zero (slot 0) rather than whatever the allocation held
+    if (int r = hipz(P->d_gslot, (size_t)(S + 1) * 4)) return r;
+    if (int r = hipz(P->d_gstart, (size_t)(S + 1) * 4)) return r;
+    if (int r = hipz(P->d_gcount, (size_t)(S + 1) * 4)) return r;
     for (int p = 0; p < n_projs; ++p)
         if (int r = hipz(P->d_Z[p], (size_t)std::max(1LL, L.z_elems[p]) * 2)) return r;
     hipError_t e = hipStreamCreateWithFlags(&P->load_stream, hipStreamNonBlocking);
@@ -436,6 +540,12 @@ int bdlora_destroy_pool(bdlora_pool_t P) {
     DeviceGuard guard(P->device);
     (void)hipDeviceSynchronize();
     free_pool(P);
+    return BDLORA_OK;
+}
+
+int bdlora_pool_slots(bdlora_pool_t P, int32_t* slots) {
+    if (!P || !slots) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
+    *slots = P->L.max_slots;
     return BDLORA_OK;
 }
 
@@ -519,54 +629,7 @@ int64_t bdlora_slot_bytes(bdlora_pool_t P) {
 int bdlora_pack_adapter_host(bdlora_pool_t P, int32_t rank, const uint16_t* const* A_host,
                              const uint16_t* const* B_host, void* slab_host) {
     if (!P || !slab_host) return fail(BDLORA_ERR_INVALID_ARG, "null argument");
-    const Layout& L = P->L;
-    if (rank < 0 || rank > L.max_rank) return fail(BDLORA_ERR_INVALID_ARG, "rank out of range 0..max_rank");
-    if (rank > 0 && (!A_host || !B_host)) return fail(BDLORA_ERR_INVALID_ARG, "null factor arrays");
-    const int r8 = rank8(rank);
-    uint16_t* slab = static_cast<uint16_t*>(slab_host);
-    std::memset(slab, 0, (size_t)L.slot_stride * 2);
-    int k = 0;
-    for (int p = 0; p < L.n_projs; ++p) {
-        const ProjInfo& pi = L.proj[p];
-        if (rank == 0) {
-            k += pi.S;
-            continue;
-        }
-        for (int s = 0; s < pi.S; ++s) {
-            if (!A_host[k + s] || !B_host[k + s]) return fail(BDLORA_ERR_INVALID_ARG, "null factor pointer");
-        }
-        // A^T_cat in the fragment layout: row s*r8 + j is column j of A_s
-        // (zero for j >= rank), rows padded to 16; element
-        // [(rb KS + ks) 512 + lane 8 + i] = A^T_cat[16 rb + lane%16][32 ks + 8 (lane/16) + i]
-        const int KS = pi.K / 32, arows = pi.S * r8;
-        uint16_t* da = slab + pi.a_off;
-        for (int row = 0; row < arows; ++row) {
-            const int s = row / r8, j = row - s * r8;
-            if (j >= rank) continue;
-            const uint16_t* a = A_host[k + s];
-            const int rb = row / 16, lr = row % 16;
-            for (int kk = 0; kk < pi.K; ++kk) {
-                const uint16_t v = a[(size_t)kk * rank + j];
-                if ((v & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in A");
-                const int ks = kk / 32, w = kk % 32, lane = lr + 16 * (w / 8), i = w % 8;
-                da[((size_t)rb * KS + ks) * 512 + lane * 8 + i] = v;
-            }
-        }
-        // B^T_cat [N x r8] row-major: row n is column n of its slice's B
-        uint16_t* db = slab + pi.b_off;
-        for (int s = 0; s < pi.S; ++s) {
-            const uint16_t* b = B_host[k + s];
-            const int n_s = pi.slice_out[s];
-            for (int j = 0; j < rank; ++j)
-                for (int n = 0; n < n_s; ++n) {
-                    const uint16_t v = b[(size_t)j * n_s + n];
-                    if ((v & 0x7f80u) == 0x7f80u) return fail(BDLORA_ERR_INVALID_ARG, "non-finite value in B");
-                    db[(size_t)(pi.slice_col[s] + n) * r8 + j] = v;
-                }
-        }
-        k += pi.S;
-    }
-    return BDLORA_OK;
+    return pack_adapter_slab(P->L, rank, A_host, B_host, static_cast<uint16_t*>(slab_host));
 }
 
 int bdlora_load_adapters_packed(bdlora_pool_t P, int32_t first_slot, int32_t n, const int32_t* ranks,
@@ -640,9 +703,15 @@ static Shapes pick_shapes(int T, long long col_blocks = 0, int r8max = bdl::kMax
 
 static int oct_cap(const Layout& L, int gemm_mt) { return gemm_mt * L.r8max / 8 + 64; }
 
-static void fill_plan_args(bdlora_pool_t P, const int32_t* ids, int T, bdl::PrepArgs* a, const Shapes& k) {
-    a->ids = ids;
+static void fill_plan_args(bdlora_pool_t P, const Batch& B, int T, bdl::PrepArgs* a, const Shapes& k) {
+    a->ids = B.ids;
     a->T = T;
+    a->n_seg = B.ids ? 0 : B.n_seg;
+    for (int i = 0; i < a->n_seg; ++i) {
+        a->seg_start[i] = B.seg_start[i];
+        a->seg_slot[i] = B.seg_slot[i];
+    }
+    a->act_max = -1;
     a->loaded = P->d_loaded;
     a->r8 = P->d_r8;
     a->max_slots = P->L.max_slots;
@@ -687,12 +756,16 @@ static const uint16_t* int4_scales(const ProjInfo& pi, const void* W) {
 }
 
 static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
-                          const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s,
+                          const void* const* W, void* const* out, const Batch& B, int T, hipStream_t s,
                           const DecMode& mode = DecMode()) {
     const Layout& L = P->L;
+    // adapter positions of the launches: the loaded adapters bound the
+    // distinct ones a batch can use (the plan treats any past that bound as
+    // none and raises the error flag).  Both forms of the batch (ids,
+    // segments) take the same launch geometry, so they give the same bits.
     int n_loaded = 0;
     for (int v : P->h_loaded) n_loaded += v != 0;
-    const int act_max = std::min(T, n_loaded);
+    const int act_max = std::min({T, n_loaded, bdl::kDecodeMaxT});
 
     bdl::DecArgs da;
     std::memset(&da, 0, sizeof(da));
@@ -722,9 +795,11 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     // two workgroups per CU, each with at least 4 units (one k-step of a
     // full group) whatever the number of adapters in use; the kernels' 32-bit
     // schedule arithmetic needs units * workgroups < 2^32
+    // (at least one workgroup: one that owns every unit needs no minimum)
     const int grid = (int)std::min<long long>(
-        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, units_min / 4, 0xffffffffLL / std::max(1LL, units_max)});
-    if (grid < 1) return fail(BDLORA_ERR_SHAPE, "projection too small for the decode launch");
+        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, std::max(1LL, units_min / 4),
+         0xffffffffLL / std::max(1LL, units_max)});
+    if (grid < 1) return fail(BDLORA_ERR_SHAPE, "batch too large for the decode launch's schedule");
     if (groups_max + grid > L.part_slots) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
     da.n_proj = n;
     da.T = T;
@@ -767,10 +842,11 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     k.gmb = (T + 15) / 16;
     k.gnb = 4;
     bdl::PrepArgs pa;
-    fill_plan_args(P, ids, T, &pa, k);
+    fill_plan_args(P, B, T, &pa, k);
     pa.tile_oct = nullptr;                        // the epilogue needs no octet lists
     pa.tgrp = P->d_tgrp;
     pa.decode_plan = 1;
+    pa.act_max = act_max;
     // projections given the same X (gate and up) share one packed copy
     int frags = 0, jobs = 0;
     for (int q = 0; q < n && mode.prep; ++q) {
@@ -822,7 +898,7 @@ static bool use_decode(const Layout& L, int T) {
 // packed activations are already in place), shrink, base product with the
 // expand fused in.
 static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
-                           const void* const* W, void* const* out, const int32_t* ids, int T, hipStream_t s,
+                           const void* const* W, void* const* out, const Batch& B, int T, hipStream_t s,
                            bool pack = true, float* const* out_f32 = nullptr) {
     const Layout& L = P->L;
     long long col_blocks = 0;
@@ -839,6 +915,9 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
         return (long long)L.proj[projs[x]].K * L.proj[projs[x]].N > (long long)L.proj[projs[y]].K * L.proj[projs[y]].N;
     });
+    // the loaded adapters bound the distinct ones the batch can use; the
+    // path choices below take that bound (the host does not see device ids,
+    // and both forms of the batch must take the same launches)
     int n_loaded = 0;
     for (int v : P->h_loaded) n_loaded += v != 0;
     // bf16 weights above one 256-row tile: the 256 x 256 LDS-staged kernel
@@ -972,7 +1051,10 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.perm = P->d_perm;
     fa.items = P->d_items;
     fa.meta = P->d_meta;
-    fa.items_bound = std::min(T, std::max(n_loaded, 1)) + (T + mts - 1) / mts;
+    // every group gives at most ceil(count / mts) items: at most
+    // (groups + T / mts) in all, groups bounded by the slots (device ids: a
+    // bound that holds whatever is loaded when a captured forward replays)
+    fa.items_bound = std::min(T, L.max_slots) + (T + mts - 1) / mts;
     fa.cchunks = cch;
     // Small batches over many adapters (groups of a few scattered tokens, at
     // most 8 per loaded adapter on average) split each shrink item's K over
@@ -1001,7 +1083,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
 
     bdl::PrepArgs pa;
-    fill_plan_args(P, ids, T, &pa, k);
+    fill_plan_args(P, B, T, &pa, k);
     if (big) {
         // the large tiles take their rows in adapter order
         pa.rowtok = P->d_rowtok;
@@ -1075,8 +1157,38 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     return BDLORA_OK;
 }
 
+// The batch's adapters: device ids, or host segments checked here (tiling
+// 0..T-1 in order, every slot loaded or -1) and copied into *B.
+static int read_batch(bdlora_pool_t P, const int32_t* ids, const bdlora_segments* sg, int T, Batch* B) {
+    if ((ids != nullptr) == (sg != nullptr)) return fail(BDLORA_ERR_INVALID_ARG, "give exactly one of ids and segs");
+    if (ids) {
+        B->ids = ids;
+        return BDLORA_OK;
+    }
+    const int n = sg->n_seg;
+    if (n < 1 || n > bdl::kMaxSeg) return fail(BDLORA_ERR_INVALID_ARG, "n_seg must be 1..BDLORA_MAX_SEGMENTS");
+    if (!sg->start || !sg->len || !sg->slot) return fail(BDLORA_ERR_INVALID_ARG, "null segment array");
+    long long next = 0;
+    bool bad = false;
+    for (int i = 0; i < n; ++i) {
+        if (sg->start[i] != next || sg->len[i] < 1)
+            return fail(BDLORA_ERR_INVALID_ARG, "segments must tile 0..T-1 in order (segment " + std::to_string(i) + ")");
+        next += sg->len[i];
+        const int a = sg->slot[i];
+        if (a != -1 && (a < 0 || a >= P->L.max_slots || !P->h_loaded[a])) bad = true;
+        B->seg_start[i] = sg->start[i];
+        B->seg_slot[i] = a;
+    }
+    if (next != T) return fail(BDLORA_ERR_INVALID_ARG, "segment lengths do not add up to T");
+    if (bad) return fail(BDLORA_ERR_BAD_ADAPTER, "a segment names no loaded adapter slot");
+    B->ids = nullptr;
+    B->n_seg = n;
+    return BDLORA_OK;
+}
+
 int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
-                         const void* const* W, void* const* out, const int32_t* ids, int32_t T, void* stream) {
+                         const void* const* W, void* const* out, const int32_t* ids, const bdlora_segments* segs,
+                         int32_t T, void* stream) {
     if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
     const Layout& L = P->L;
     if (n < 1 || n > BDLORA_MAX_PROJS) return fail(BDLORA_ERR_INVALID_ARG, "n must be 1..8");
@@ -1092,27 +1204,28 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
             return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
     }
     if (T == 0) return BDLORA_OK;
-    if (!ids) return fail(BDLORA_ERR_INVALID_ARG, "null ids");
+    Batch B;
+    if (int rc = read_batch(P, ids, segs, T, &B)) return rc;
     DeviceGuard guard(P->device);
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
 
-    if (use_decode(L, T)) return forward_decode(P, n, projs, X, W, out, ids, T, s);
-    return forward_prefill(P, n, projs, X, W, out, ids, T, s);
+    if (use_decode(L, T)) return forward_decode(P, n, projs, X, W, out, B, T, s);
+    return forward_prefill(P, n, projs, X, W, out, B, T, s);
 }
 
-int bdlora_forward_shard(bdlora_pool_t P, int32_t proj, const void* X, const void* W, const int32_t* ids, int32_t T,
-                         void* out, void* stream) {
+int bdlora_forward_shard(bdlora_pool_t P, int32_t proj, const void* X, const void* W, const int32_t* ids,
+                         const bdlora_segments* segs, int32_t T, void* out, void* stream) {
     const void* xs[1] = {X};
     const void* ws[1] = {W};
     void* os[1] = {out};
     int32_t pr[1] = {proj};
-    return bdlora_forward_layer(P, 1, pr, xs, ws, os, ids, T, stream);
+    return bdlora_forward_layer(P, 1, pr, xs, ws, os, ids, segs, T, stream);
 }
 
 int bdlora_forward_mlp(bdlora_pool_t P, int32_t act, const int32_t* first, int32_t down, const void* X,
-                       const void* const* W_first, const void* W_down, void* out, const int32_t* ids, int32_t T,
-                       void* stream) {
+                       const void* const* W_first, const void* W_down, void* out, const int32_t* ids,
+                       const bdlora_segments* segs, int32_t T, void* stream) {
     if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
     const Layout& L = P->L;
     if (act != BDLORA_ACT_NONE && act != BDLORA_ACT_SILU_MUL) return fail(BDLORA_ERR_INVALID_ARG, "unknown act");
@@ -1131,11 +1244,13 @@ int bdlora_forward_mlp(bdlora_pool_t P, int32_t act, const int32_t* first, int32
     }
     if (L.proj[down].kind != BDLORA_ROW) return fail(BDLORA_ERR_INVALID_ARG, "down must be a row projection");
     if (T == 0) return BDLORA_OK;
-    if (!ids || !X || !W_down || !out) return fail(BDLORA_ERR_INVALID_ARG, "null tensor pointer");
+    if (!X || !W_down || !out) return fail(BDLORA_ERR_INVALID_ARG, "null tensor pointer");
     for (int j = 0; j < nf; ++j)
         if (!W_first[j] || !aligned16(W_first[j])) return fail(BDLORA_ERR_INVALID_ARG, "W must be 16-byte aligned");
     if (!aligned16(X) || !aligned16(W_down) || !aligned16(out))
         return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
+    Batch B;
+    if (int rc = read_batch(P, ids, segs, T, &B)) return rc;
     DeviceGuard guard(P->device);
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
@@ -1152,20 +1267,20 @@ int bdlora_forward_mlp(bdlora_pool_t P, int32_t act, const int32_t* first, int32
         m1.h_dst = h;
         m1.h_KS = Ni / 32;
         void* none[2] = {nullptr, nullptr};
-        int rc = forward_decode(P, nf, first, xs, W_first, none, ids, T, s, m1);
+        int rc = forward_decode(P, nf, first, xs, W_first, none, B, T, s, m1);
         if (rc) return rc;
         DecMode m2;
         m2.prep = false;
-        return forward_decode(P, 1, dn, xs, wd, od, ids, T, s, m2);
+        return forward_decode(P, 1, dn, xs, wd, od, B, T, s, m2);
     }
     // prefill: gate/up outputs in fp32 to the pool's workspace, H packed,
     // then down
     float* g_u[2] = {P->d_mlp, P->d_mlp + (size_t)T * Ni};
     void* none[2] = {nullptr, nullptr};
-    int rc = forward_prefill(P, nf, first, xs, W_first, none, ids, T, s, true, g_u);
+    int rc = forward_prefill(P, nf, first, xs, W_first, none, B, T, s, true, g_u);
     if (rc) return rc;
     BDL_HIP(bdl::launch_mlp_pack(g_u[0], act == BDLORA_ACT_SILU_MUL ? g_u[1] : nullptr, h, T, Ni, s));
-    return forward_prefill(P, 1, dn, xs, wd, od, ids, T, s, false);
+    return forward_prefill(P, 1, dn, xs, wd, od, B, T, s, false);
 }
 
 int bdlora_plan_device(bdlora_pool_t P, const int32_t* ids, int32_t T, int32_t* vid, int32_t* gslot, int32_t* gstart,
@@ -1178,7 +1293,9 @@ int bdlora_plan_device(bdlora_pool_t P, const int32_t* ids, int32_t T, int32_t* 
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
     bdl::PrepArgs pa;
-    fill_plan_args(P, ids, T, &pa, pick_shapes(T));
+    Batch B;
+    B.ids = ids;
+    fill_plan_args(P, B, T, &pa, pick_shapes(T));
     BDL_HIP(bdl::launch_prep(pa, s));
     const int G = std::min(T, P->L.max_slots);
     if (T > 0) {

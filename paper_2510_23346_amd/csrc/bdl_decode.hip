@@ -127,13 +127,16 @@ __device__ __forceinline__ int dec_items(const DecSeg& g, int kq, int* kw) {
 }
 
 // element pointer of k-step 0 of virtual block vb of projection P; lane i of
-// gs holds the slot of the i-th adapter in use.  Positions at or past n_act
-// (in a group with a used one) read the first adapter's factor, unused.
+// gs holds the slot of the i-th adapter in use (entries at or past n_act are
+// not written by the plan).  Positions at or past n_act (in a group with a
+// weight block or a used adapter) read slot 0's factor, unused: that slot
+// always exists, whatever the table holds.
 __device__ __forceinline__ const uint16_t* dec_block(const DecArgs& a, const DecProj& P, int vb, int KS, int gs,
                                                      int n_act_v) {
     if (vb < P.nWb) return P.W + frag_index(vb, 0, KS);
     const int ai = (vb - P.nWb) / P.nbA, c = vb - P.nWb - ai * P.nbA;
-    const int slot = __builtin_amdgcn_readlane(gs, ai < __builtin_amdgcn_readfirstlane(n_act_v) ? ai : 0);
+    const bool used = ai < __builtin_amdgcn_readfirstlane(n_act_v);
+    const int slot = used ? __builtin_amdgcn_readlane(gs, used ? ai : 0) : 0;
     return a.pool + (size_t)slot * a.slot_stride + P.a_off + frag_index(c, 0, KS);
 }
 

@@ -13,6 +13,7 @@ constexpr int kMaxSlices = 4;
 constexpr int kMaxSlots = 8192;
 constexpr int kMaxRank8 = 128;       // largest supported rank, rounded up to 8
 constexpr int kPlanLdsTokens = 8192; // plan keeps validated ids in LDS up to this batch size
+constexpr int kMaxSeg = BDLORA_MAX_SEGMENTS;   // segments of a batch given in run-length form
 constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base GEMM (prefill)
 constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-tile GEMM's split tiles
 constexpr int kBigPartElems = kBigM * kBigN;
@@ -87,8 +88,13 @@ struct PackJob {
 
 // Prep launch: workgroup 0 plans the batch, the others pack activations.
 struct PrepArgs {
-    const int* ids;
+    const int* ids;           // [T] per-token ids, or null: the batch is given by the segments below
     int T;
+    int n_seg;                // segments (ids null): token t takes seg_slot[i] of the last i with
+    int seg_start[kMaxSeg];   // seg_start[i] <= t (the host checked that they tile 0..T-1)
+    int seg_slot[kMaxSeg];
+    int act_max;              // decode plan: adapters past this many (slot order) are treated as
+                              // none and raise *err (the decode launches' bound); -1: no bound
     const int* loaded;
     const int* r8;            // [max_slots]
     int max_slots;

@@ -55,19 +55,33 @@ __device__ __forceinline__ unsigned wave_or(unsigned v) {
     return (unsigned)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Segments form: lane i < n_seg writes the id of segment i into ids_lds for
+// its tokens (the host checked that the segments tile 0..T-1), and lane t
+// reads token t's id back.
+__device__ __forceinline__ int decode_seg_id(const PrepArgs& a, int* ids_lds) {
+    const int l = threadIdx.x & 63;
+    if (l < a.n_seg) {
+        const int s0 = a.seg_start[l], s1 = l + 1 < a.n_seg ? a.seg_start[l + 1] : a.T, v = a.seg_slot[l];
+        for (int t = s0; t < s1 && t < kDecodeMaxT; ++t) ids_lds[t] = v;
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);        // lgkmcnt(0): this wave's LDS stores are done
+    __builtin_amdgcn_wave_barrier();
+    return l < a.T ? ids_lds[l] : -1;
+}
+
 // Plan of a decode batch (T <= 64) by one wave: validated ids, ranks, the
 // adapters in use in ascending slot order (groups) and each token's group.
 // Lane t holds token t.  Pools of at most 64 slots keep the slot tables in
 // lanes (one load round trip) and find the groups from the bit mask of slots
 // in use; larger pools look the tables up per token and take the smallest
 // remaining slot per pass.
-__device__ void decode_plan(const PrepArgs& a) {
+__device__ void decode_plan(const PrepArgs& a, int* ids_lds) {
     const int l = threadIdx.x & 63;
     const bool in = l < a.T;
     const bool small = a.max_slots <= 64;
     const int lt = small && l < a.max_slots ? a.loaded[l] : 0;
     const int rt = small && l < a.max_slots ? a.r8[l] : 0;
-    const int id = in ? a.ids[l] : -1;
+    const int id = a.ids ? (in ? a.ids[l] : -1) : decode_seg_id(a, ids_lds);
     const bool in_range = id >= 0 && id < a.max_slots;
     int ld, r8v;
     if (small) {
@@ -78,10 +92,10 @@ __device__ void decode_plan(const PrepArgs& a) {
         ld = in_range ? a.loaded[id] : 0;
         r8v = in_range ? a.r8[id] : 0;
     }
-    const bool ok = in_range && ld != 0;
-    const int v = ok ? id : -1;
-    const bool bad = __ballot(in && !ok && id != -1) != 0ull;
+    bool ok = in_range && ld != 0;
+    bool bad = __ballot(in && !ok && id != -1) != 0ull;
     int g = 0, mine = -1;
+    const int v = ok ? id : -1;
     if (small) {
         const unsigned long long bit = ok ? 1ull << v : 0ull;
         const unsigned long long used =
@@ -101,8 +115,19 @@ __device__ void decode_plan(const PrepArgs& a) {
             rem &= ~__ballot(eq);
         }
     }
+    // adapters past the launches' bound (possible only when a captured
+    // forward replays after more adapters were loaded): base only, flagged
+    if (a.act_max >= 0 && g > a.act_max) {
+        const bool over = ok && mine >= a.act_max;
+        bad = bad || __ballot(over) != 0ull;
+        if (over) {
+            ok = false;
+            mine = -1;
+        }
+        g = a.act_max;
+    }
     if (in) {
-        a.vid[l] = v;
+        a.vid[l] = ok ? v : -1;
         a.tr8[l] = ok ? r8v : 0;
         if (a.tgrp) a.tgrp[l] = mine;
     }
@@ -154,8 +179,9 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
             pack_activations<1>(a, blockIdx.x - 1, gridDim.x - 1);
         return;
     }
+    __shared__ int vid_l[kPlanLdsTokens];
     if (a.decode_plan) {
-        if (threadIdx.x < 64) decode_plan(a);
+        if (threadIdx.x < 64) decode_plan(a, vid_l);
         return;
     }
     extern __shared__ int tabs[];             // cnt | r8 | loaded | 15 tile bitmaps
@@ -164,8 +190,8 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     int* r8l = tabs + a.max_slots;
     int* ldl = tabs + 2 * a.max_slots;
     unsigned* bits = reinterpret_cast<unsigned*>(tabs + 3 * a.max_slots);
-    __shared__ int vid_l[kPlanLdsTokens];
     __shared__ int s_err;
+    __shared__ int seg_s[kMaxSeg], seg_v[kMaxSeg];
     __shared__ int wsum[16][3];
     __shared__ int wpre[16][3];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -177,7 +203,24 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
         ldl[s] = a.loaded[s];
     }
     if (tid == 0) s_err = 0;
+    if (!a.ids && tid < a.n_seg) {
+        seg_s[tid] = a.seg_start[tid];
+        seg_v[tid] = a.seg_slot[tid];
+    }
     __syncthreads();
+    // id of token t from the segments: the last segment starting at or
+    // before t (binary search; seg_s[0] = 0)
+    auto seg_id = [&](int t) {
+        int lo = 0, hi = a.n_seg - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (seg_s[mid] <= t)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        return seg_v[lo];
+    };
     // ids in batches of 8 per thread: all loads of a batch are issued before
     // any of its stores, so a batch costs one round trip
     for (int t0 = 0; t0 < a.T; t0 += 8 * 1024) {
@@ -185,7 +228,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int t = t0 + j * 1024 + tid;
-            idv[j] = t < a.T ? a.ids[t] : -1;
+            idv[j] = t < a.T ? (a.ids ? a.ids[t] : seg_id(t)) : -1;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {

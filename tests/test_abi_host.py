@@ -161,3 +161,99 @@ def test_int4_descriptor_validation(L):
         assert L.bdlora_pool_size(arr, 1, 4, 8, 16, ctypes.byref(a), ctypes.byref(b)) == -4
     arr, _ = bd._descs(ok, 5)
     assert L.bdlora_pool_size(arr, 1, 4, 8, 16, ctypes.byref(a), ctypes.byref(b)) == -1
+
+
+def test_segment_constant_matches_header():
+    text = open(os.path.join(ROOT, "include", "bdlora.h")).read()
+    macros = dict(re.findall(r"^#define (BDLORA_\w+)\s+\(?(-?\d+)\)?", text, re.M))
+    assert int(macros["BDLORA_MAX_SEGMENTS"]) == bd.MAX_SEGMENTS
+
+
+@pytest.mark.parametrize("T", [0, 1, 7, 40])
+def test_segments_from_ids_are_the_oracle_runs(L, T):
+    rng = np.random.default_rng(T)
+    ids = np.repeat(rng.integers(-1, 5, size=T), rng.integers(1, 4, size=T))[:T]
+    sg = bd.Segments.from_ids(ids)
+    runs = oplan.segments(ids)
+    assert sg.n_seg == len(runs) and sg.T == T
+    assert list(zip(sg.start.tolist(), sg.len.tolist(), sg.slot.tolist())) == [tuple(r) for r in runs]
+
+
+def _slot_layout_reference(projs, max_rank, rank, A, B):
+    """The pool's documented slot layout, written out element by element:
+    per projection, A^T_cat (row s*r8 + j = column j of slice s's A, rows
+    padded to 16) in 1 KB fragments, element [(rb*KS + ks)*512 + lane*8 + i]
+    = A^T_cat[16 rb + lane%16][32 ks + 8 (lane//16) + i], then B^T_cat
+    [N x r8] row-major (row n = column n of its slice's B), each region
+    starting at a multiple of 128 elements."""
+    r8max = max(8, (max_rank + 7) // 8 * 8)
+    r8 = (rank + 7) // 8 * 8
+    regions, off = [], 0
+    up = lambda v, m: (v + m - 1) // m * m
+    for kind, d_in, slices in projs:
+        S, N, KS = len(slices), sum(slices), d_in // 32
+        a_off = off
+        off = up(off + up(S * r8max, 16) * d_in, 128)
+        b_off = off
+        off = up(off + N * r8max, 128)
+        regions.append((a_off, b_off))
+    out = np.zeros(off, np.uint16)
+    for p, (kind, d_in, slices) in enumerate(projs):
+        a_off, b_off = regions[p]
+        KS = d_in // 32
+        for s, n_s in enumerate(slices):
+            for j in range(rank):
+                row = s * r8 + j
+                rb, lr = divmod(row, 16)
+                for k in range(d_in):
+                    ks, w = divmod(k, 32)
+                    lane = lr + 16 * (w // 8)
+                    out[a_off + (rb * KS + ks) * 512 + lane * 8 + w % 8] = A[p][s][k, j]
+            col0 = sum(slices[:s])
+            for j in range(rank):
+                for n in range(n_s):
+                    out[b_off + (col0 + n) * r8 + j] = B[p][s][j, n]
+    return out
+
+
+@pytest.mark.parametrize("max_rank,rank", [(8, 3), (16, 16), (24, 9), (16, 0)])
+def test_host_packer_writes_the_documented_slot_layout(L, max_rank, rank):
+    projs = [("column", 64, (32, 16, 16)), ("row", 32, (48,))]
+    rng = np.random.default_rng(max_rank * 10 + rank)
+    A = [[rng.integers(1, 1 << 14, size=(d, rank), dtype=np.uint16) for _ in sl] for _, d, sl in projs]
+    B = [[rng.integers(1, 1 << 14, size=(rank, n), dtype=np.uint16) for n in sl] for _, _, sl in projs]
+    nbytes = bd.layout_slot_bytes(projs, max_rank)
+    assert nbytes == bd.pool_size(projs, 3, max_rank, 16)[0] // 3
+    slab = bd.pack_adapter_layout(projs, max_rank, rank, A, B)
+    assert slab.nbytes == nbytes
+    ref = _slot_layout_reference(projs, max_rank, rank, A, B)
+    assert np.array_equal(slab.view(np.uint16), ref)
+
+
+def test_host_packer_errors(L):
+    projs = [("column", 64, (16,))]
+    A = [[np.zeros((64, 4), np.uint16)]]
+    B = [[np.zeros((4, 16), np.uint16)]]
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.pack_adapter_layout(projs, 2, 4, A, B)                 # rank > max_rank
+    assert e.value.code == -1
+    A[0][0][3, 1] = 0x7F80                                        # +inf
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.pack_adapter_layout(projs, 8, 4, A, B)
+    assert e.value.code == -1 and "non-finite" in str(e.value)
+
+
+def test_pool_byte_budget_is_checked_before_any_device_work(L):
+    # a budget that holds no slot, or fewer slots than asked for, is OOM;
+    # both are decided on the host (no device is needed to fail)
+    projs = [("column", 256, (64,))]
+    per = bd.layout_slot_bytes(projs, 16)
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.Pool(projs, 0, 16, 32, pool_bytes=per - 1)
+    assert e.value.code == -2
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.Pool(projs, 8, 16, 32, pool_bytes=8 * per - 1)
+    assert e.value.code == -2 and "pool_bytes" in str(e.value)
+    with pytest.raises(bd.BDLoRAError) as e:
+        bd.Pool(projs, 8, 16, 32, pool_bytes=-5)
+    assert e.value.code == -1

@@ -139,16 +139,26 @@ def test_int4_8b_layer_decode(torch_cuda):
     s1 = wl.workload(1)
     spec = wl.WorkloadSpec(s1.name + "-int4", s1.model, s1.tp, s1.projs, s1.T, s1.n_slots, s1.ranks,
                            s1.scales, s1.ids_kind, s1.seed, weight_format="int4_g128")
-    ids = wl.draw_ids(spec)
-    active = sorted(int(s) for s in np.unique(ids) if s >= 0)
-    layer = wl.draw_layer(spec, slots=active)
+    # every slot loaded, as the benchmark does (same launch geometry)
+    slots = list(range(spec.n_slots))
+    layer = wl.draw_layer(spec, slots=slots)
     pool = make_pool(spec)
-    load_adapters(pool, spec, active, cache=layer.adapters)
+    load_adapters(pool, spec, slots, cache=layer.adapters)
     dl, ys = _run(torch, spec, layer, pool)
     refs = quant.layer_forward_w4(layer)
+    # the LoRA term alone: the base-only forward (every id -1) against the
+    # oracle's product with the decoded INT4 weight
+    base = [torch.full_like(o, float("nan")) for o in dl.out]
+    pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, base, torch.full_like(dl.ids, -1))
+    torch.cuda.synchronize()
     for p, pi in enumerate(layer.projs):
         e = bdlora.rel_errors(ys[p], refs[p])
         assert e["pointwise"] <= TOL, f"{pi.spec.name}: {e}"
+        Wd = quant.dequantize(pi.Wq, pi.Ws_bits, pi.spec.d_in)
+        rbase = pi.X.astype(np.float64) @ Wd
+        d = bdlora.delta_errors(ys[p], device_to_float(base[p]), refs[p], rbase)
+        assert d <= TOL, f"{pi.spec.name}: LoRA-term error {d}"
+    assert pool.device_error() == 0
     pool.close()
 
 

@@ -145,7 +145,7 @@ def test_mlp_argument_errors(torch_cuda):
     def call(act, first, down):
         pr = (ctypes.c_int32 * 2)(*first, *([0] * (2 - len(first))))
         return L.bdlora_forward_mlp(pool._h, act, pr, down, dl.X[0].data_ptr(), ws, dl.W[2].data_ptr(),
-                                    out.data_ptr(), dl.ids.data_ptr(), 8, None)
+                                    out.data_ptr(), dl.ids.data_ptr(), None, 8, None)
     assert call(bd.ACT_SILU_MUL, [0, 1], 2) == 0
     torch.cuda.synchronize()
     assert call(7, [0, 1], 2) == -1                  # unknown act

@@ -36,7 +36,7 @@ def _run_layer(torch, spec, layer, pool, T=None):
 
 def _base_only(torch, spec, dl, pool):
     ids_none = torch.full_like(dl.ids, -1)
-    outs = [torch.empty_like(o) for o in dl.out]
+    outs = [torch.full_like(o, float("nan")) for o in dl.out]
     pool.forward_layer(list(range(len(spec.projs))), dl.X, dl.W, outs, ids_none)
     torch.cuda.synchronize()
     return [device_to_float(o) for o in outs]
@@ -350,37 +350,23 @@ def test_all_shards_reassemble_the_unsharded_layer(torch_cuda):
 # the five benchmark workloads at full size
 # ---------------------------------------------------------------------------
 
-def _sample_rows(ids, k, seed):
-    T = ids.size
-    rng = np.random.default_rng(seed)
-    rows = set(rng.choice(T, size=min(k, T), replace=False).tolist())
-    rows |= {0, T - 1}
-    change = np.nonzero(np.diff(ids) != 0)[0]
-    rows |= set(change.tolist()) | set((change + 1).tolist())
-    return np.array(sorted(rows))
-
-
 @pytest.mark.parametrize("index", [0, 1, 2, 3, 4])
 def test_workload_parity(torch_cuda, index):
+    # the resident set bench.py loads (every slot of the pool, config 4's 512
+    # included), so the launch geometry checked here is the one it times;
+    # every row of every output is compared with the oracle
     torch = torch_cuda
     spec = wl.workload(index)
     ids = wl.draw_ids(spec)
-    active = sorted(int(s) for s in np.unique(ids) if s >= 0)
-    layer = wl.draw_layer(spec, slots=active)
+    slots = list(range(spec.n_slots))
+    layer = wl.draw_layer(spec, slots=slots)
     pool = make_pool(spec)
-    load_adapters(pool, spec, active, cache=layer.adapters)
+    load_adapters(pool, spec, slots, cache=layer.adapters)
     dl, ys = _run_layer(torch, spec, layer, pool)
     yb = _base_only(torch, spec, dl, pool)
-    if spec.T <= 512:
-        rows = np.arange(spec.T)
-        refs = bdlora.layer_forward(layer)
-    else:
-        rows = _sample_rows(ids, 96, index)
-        refs = bdlora.layer_forward_rows(layer, rows)
-    rbase = _oracle_base(layer, rows)
+    refs = bdlora.layer_forward(layer)
+    rbase = _oracle_base(layer)
     for p in range(len(spec.projs)):
-        _check(ys[p][rows], refs[p], yb[p][rows], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
-        # every output is finite and the unsampled rows were written
-        assert np.all(np.isfinite(ys[p]))
+        _check(ys[p], refs[p], yb[p], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
     assert pool.device_error() == 0
     pool.close()

@@ -40,6 +40,19 @@ def test_matches_brute_force(seed):
     np.testing.assert_allclose(y, yb, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("seed", [0, 1])
+def test_float32_evaluation_matches_brute_force_to_single_precision(seed):
+    # the single-precision evaluation (the CPU baseline's) computes the same
+    # steps: against the float64 brute force it may differ only by float32
+    # rounding of sums over at most d_in + r terms
+    X, W, ids, ad, sl = _tiny_case(seed, T=9, d_in=40)
+    y = bdlora.shard_forward(X, W, ids, ad, sl, dtype=np.float32)
+    assert y.dtype == np.float32
+    yb = bdlora.brute_force(X, W, ids, ad, sl)
+    scale = np.abs(yb).max()
+    assert np.max(np.abs(y - yb)) <= 64 * np.finfo(np.float32).eps * scale
+
+
 def test_empty_batch():
     X, W, ids, ad, sl = _tiny_case(0)
     y = bdlora.shard_forward(X[:0], W, ids[:0], ad, sl)

@@ -27,6 +27,7 @@ float) and the GPU path (as raw 16-bit patterns).
 """
 from __future__ import annotations
 
+import os
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence, Tuple
 
@@ -52,10 +53,15 @@ def bf16_round(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
     Inputs are finite; NaN/Inf are never generated here.
     """
     f = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
-    u = f.view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = ((u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)).astype(np.uint16)
-    return r, bf16_bits_to_float(r)
+    u = f.view(np.uint32)
+    # u + 0x7FFF + lsb stays below 2**32 for every finite input
+    r = (u >> np.uint32(16)) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    bits = r.astype(np.uint16)
+    r <<= np.uint32(16)
+    return bits, r.view(np.float32)
 
 
 def bf16_bits_to_float(bits: np.ndarray) -> np.ndarray:
@@ -348,6 +354,19 @@ def draw_adapter(spec: WorkloadSpec, slot: int) -> Adapter:
     return Adapter(slot, r, float(spec.scales[slot]), Ab, Bb, A, B)
 
 
+def draw_adapters(spec: WorkloadSpec, slots: Sequence[int]) -> Dict[int, Adapter]:
+    """The adapters of ``slots``, drawn on a few threads (each slot has its
+    own random stream, so the result does not depend on the order)."""
+    slots = [int(s) for s in slots]
+    if len(slots) <= 4:
+        return {s: draw_adapter(spec, s) for s in slots}
+    from concurrent.futures import ThreadPoolExecutor
+    workers = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        drawn = list(ex.map(lambda s: draw_adapter(spec, s), slots))
+    return dict(zip(slots, drawn))
+
+
 def draw_layer(spec: WorkloadSpec, slots: Optional[Sequence[int]] = None) -> LayerInputs:
     """Draw ids, per-projection X and W, and the adapters of ``slots``
     (default: every slot that some token uses)."""
@@ -355,8 +374,7 @@ def draw_layer(spec: WorkloadSpec, slots: Optional[Sequence[int]] = None) -> Lay
     projs = [draw_proj(spec, p) for p in range(len(spec.projs))]
     if slots is None:
         slots = sorted(int(s) for s in np.unique(ids) if s >= 0)
-    adapters = {int(s): draw_adapter(spec, int(s)) for s in slots}
-    return LayerInputs(spec, ids, projs, adapters)
+    return LayerInputs(spec, ids, projs, draw_adapters(spec, slots))
 
 
 def custom_workload(name: str, projs: List[ProjSpec], T: int, ranks: Sequence[int],
@@ -373,5 +391,6 @@ def custom_workload(name: str, projs: List[ProjSpec], T: int, ranks: Sequence[in
 
 
 __all__.append("custom_workload")
+__all__.append("draw_adapters")
 __all__.append("quantize_int4_g128")
 __all__.append("tiny_mlp_projs")

@@ -57,7 +57,8 @@ class DeviceLayer:
                 self.W.append(pack_weight_int4(q, bits_to_device(pi.Ws_bits, device)))
             else:
                 self.W.append(pack_weight(bits_to_device(np.ascontiguousarray(pi.W_bits.T), device)))
-            self.out.append(torch.empty((T, pi.spec.d_out), dtype=torch.bfloat16, device=device))
+            # NaN-filled, so an output the kernels never write cannot pass a check
+            self.out.append(torch.full((T, pi.spec.d_out), float("nan"), dtype=torch.bfloat16, device=device))
 
     def outputs(self) -> List[np.ndarray]:
         return [device_to_float(o) for o in self.out]
