@@ -293,6 +293,30 @@ int bdlora_forward_layer(bdlora_pool_t pool, int32_t n, const int32_t* projs,
                          const int32_t* ids, const bdlora_segments* segs, int32_t T,
                          void* stream);
 
+/* For callers that cannot allocate device memory during the call (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * bdlora_forward_layer for decode batches (1 <= T <= BDLORA_DECODE_MAX_T;
+ * T = 0 enqueues nothing) whose per-batch scratch -- the plan's tables, the
+ * packed activations and the fp32 partial tiles -- lives in a static device
+ * array of BDLORA_STATIC_SCRATCH_BYTES that the library holds on every GPU it
+ * runs on until the process ends, instead of in the pool's workspace.  The
+ * call allocates nothing (no hipMalloc, no allocating library routine); the
+ * pool still holds the adapters, their tables and the error flag.  Same
+ * arguments, kernels, launch geometry and results (bit for bit) as
+ * bdlora_forward_layer.  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams, other pools, other threads)
+ * race and must be serialized by the caller.  Nothing in the array has to
+ * start at zero: every word a call reads was written earlier in that call.
+ * Errors: as bdlora_forward_layer; SHAPE for T above BDLORA_DECODE_MAX_T or a
+ * call whose scratch exceeds BDLORA_STATIC_SCRATCH_BYTES (the message gives
+ * the sizes); HIP if the array's address could not be taken when the pool
+ * was created. */
+#define BDLORA_STATIC_SCRATCH_BYTES (32 << 20)
+int bdlora_forward_layer_static(bdlora_pool_t pool, int32_t n, const int32_t* projs,
+                                const void* const* X, const void* const* W, void* const* out,
+                                const int32_t* ids, const bdlora_segments* segs, int32_t T,
+                                void* stream);
+
 /* One device's share of a BD-LoRA MLP (Alg. 1, App. B): the first
  * (column-parallel) projection(s), the intermediate H, then the
  * row-parallel projection `down`, whose output is the device's partial that

@@ -26,6 +26,7 @@ COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
 MAX_SEGMENTS = 256      # BDLORA_MAX_SEGMENTS: most segments of a batch given as segments
+STATIC_SCRATCH_BYTES = 32 << 20   # BDLORA_STATIC_SCRATCH_BYTES: static scratch of forward_layer_static
 ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections
 # BDLORA_PATH_*: launch sequence of a forward (0: none yet)
 PATHS = {0: "", 1: "decode", 2: "tile64", 3: "medium", 4: "large"}
@@ -71,6 +72,8 @@ _SIGS = {
     "bdlora_forward_shard": (_I, [_P, _I, _P, _P, _P, _SP, _I, _P, _P]),
     "bdlora_forward_layer": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _SP, _I, _P]),
     "bdlora_forward_mlp": (_I, [_P, _I, _IP, _I, _P, _c.POINTER(_P), _P, _P, _P, _SP, _I, _P]),
+    "bdlora_forward_layer_static": (_I, [_P, _I, _IP, _c.POINTER(_P), _c.POINTER(_P), _c.POINTER(_P), _P, _SP, _I,
+                                         _P]),
     "bdlora_build_plan": (_I, [_IP, _I, _IP, _I, _IP, _IP, _IP, _IP, _IP, _IP]),
     "bdlora_plan_device": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P]),
     "bdlora_get_device_error": (_I, [_P, _P, _IP]),
@@ -490,6 +493,25 @@ class Pool:
         ws = (_c.c_void_p * n)(*[_ptr(w) for w in Ws])
         os_ = (_c.c_void_p * n)(*[_ptr(o) for o in outs])
         _check(lib().bdlora_forward_layer(self._h, n, pr, xs, ws, os_, ip or None, sp, T, _stream_handle(stream)))
+        del keep
+
+    def forward_layer_static(self, projs: Sequence[int], Xs, Ws, outs, ids, T: Optional[int] = None,
+                             stream=None, segs=None):
+        """``forward_layer`` for decode batches (T <= DECODE_MAX_T) with its
+        per-batch scratch in the library's static device array: the call
+        allocates nothing.  Calls on one GPU share that array (serialize
+        them)."""
+        ip, sp, T0, keep = _batch(ids, segs)
+        T = T0 if T is None else int(T)
+        n = len(projs)
+        for i, p in enumerate(projs):
+            self._check_io(p, Xs[i], Ws[i], outs[i], T)
+        pr = (_c.c_int32 * n)(*[int(p) for p in projs])
+        xs = (_c.c_void_p * n)(*[_ptr(x) for x in Xs])
+        ws = (_c.c_void_p * n)(*[_ptr(w) for w in Ws])
+        os_ = (_c.c_void_p * n)(*[_ptr(o) for o in outs])
+        _check(lib().bdlora_forward_layer_static(self._h, n, pr, xs, ws, os_, ip or None, sp, T,
+                                                 _stream_handle(stream)))
         del keep
 
     def forward_mlp(self, act: int, first: Sequence[int], down: int, X, W_first, W_down, out, ids,

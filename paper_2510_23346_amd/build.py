@@ -20,7 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libbdlora.so")
 
-SOURCES = ["bdl_prep.hip", "bdl_decode.hip", "bdl_kernels.hip", "bdl_gemm.hip", "bdl_api.cpp"]
+SOURCES = ["bdl_prep.hip", "bdl_decode.hip", "bdl_kernels.hip", "bdl_gemm.hip", "bdl_static.hip", "bdl_api.cpp"]
 ARCH = "gfx950"
 
 

@@ -211,6 +211,7 @@ struct bdlora_pool {
     int prof_left = 0;
     int prof_used = 0;
     int last_path = 0;        // BDLORA_PATH_* of the last forward
+    hipError_t static_err = hipSuccess;   // taking the static scratch's address at creation
     std::vector<hipEvent_t> prof_ev;      // kProfEvents per recorded call
 };
 
@@ -526,6 +527,10 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
         free_pool(P);
         return fail(BDLORA_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(e));
     }
+    // set-up of the allocation-free entry point on this device (its failure
+    // only disables that entry point)
+    P->static_err = bdl::static_scratch_init(device);
+    if (P->static_err != hipSuccess) (void)hipGetLastError();
 #undef BDL_TRY
     P->h_rank.assign(S, 0);
     P->h_r8.assign(S, 0);
@@ -755,9 +760,37 @@ static const uint16_t* int4_scales(const ProjInfo& pi, const void* W) {
     return reinterpret_cast<const uint16_t*>(static_cast<const char*>(W) + (size_t)pi.N * pi.K / 2);
 }
 
+// Where a decode call keeps its per-batch scratch: the pool's workspace, or
+// (the allocation-free entry point) the library's static device array.
+struct DecWs {
+    int* vid = nullptr;               // [T] validated ids
+    int* tr8 = nullptr;               // [T] padded rank of each token's adapter
+    int* tgrp = nullptr;              // [T] group of each token's adapter
+    int* gslot = nullptr;             // [<= 64] slots of the adapters in use
+    int* meta = nullptr;              // [4] plan counts
+    uint16_t* Xp[bdl::kMaxProjs] = {};   // packed activations of the call's i-th projection
+    float* part = nullptr;            // fp32 partial tiles; null: carved from arena
+    long long part_slots = 0;
+    char* arena = nullptr;            // static scratch left for the partial tiles
+    long long arena_bytes = 0;
+};
+
+static DecWs pool_dec_ws(bdlora_pool_t P, int n, const int32_t* projs) {
+    DecWs w;
+    w.vid = P->d_vid;
+    w.tr8 = P->d_tr8;
+    w.tgrp = P->d_tgrp;
+    w.gslot = P->d_gslot;
+    w.meta = P->d_meta;
+    for (int i = 0; i < n; ++i) w.Xp[i] = P->d_Xp[projs[i]];
+    w.part = P->d_part;
+    w.part_slots = P->L.part_slots;
+    return w;
+}
+
 static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
                           const void* const* W, void* const* out, const Batch& B, int T, hipStream_t s,
-                          const DecMode& mode = DecMode()) {
+                          const DecWs& ws, const DecMode& mode = DecMode()) {
     const Layout& L = P->L;
     // adapter positions of the launches: the loaded adapters bound the
     // distinct ones a batch can use (the plan treats any past that bound as
@@ -774,7 +807,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     for (int i = 0; i < n; ++i) {
         const ProjInfo& pi = L.proj[projs[i]];
         bdl::DecProj& d = da.p[i];
-        d.Xp = P->d_Xp[projs[i]];
+        d.Xp = ws.Xp[i];
         d.W = (const uint16_t*)W[i];
         d.Ws = int4_scales(pi, W[i]);
         d.out = (uint16_t*)out[i];
@@ -800,7 +833,19 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, std::max(1LL, units_min / 4),
          0xffffffffLL / std::max(1LL, units_max)});
     if (grid < 1) return fail(BDLORA_ERR_SHAPE, "batch too large for the decode launch's schedule");
-    if (groups_max + grid > L.part_slots) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
+    float* part = ws.part;
+    long long part_slots = ws.part_slots;
+    if (!part) {
+        // the partial tiles this call needs, from the rest of the static scratch
+        part_slots = groups_max + grid;
+        if (part_slots * bdl::kPartElems * 4 > ws.arena_bytes)
+            return fail(BDLORA_ERR_SHAPE, "the call's partial tiles need " +
+                                              std::to_string(part_slots * bdl::kPartElems * 4) +
+                                              " bytes, the static scratch has " + std::to_string(ws.arena_bytes) +
+                                              " left after the plan and the packed activations");
+        part = reinterpret_cast<float*>(ws.arena);
+    }
+    if (groups_max + grid > part_slots) return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
     da.n_proj = n;
     da.T = T;
     {
@@ -821,14 +866,14 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     da.pool = P->d_slabs;
     da.slot_stride = L.slot_stride;
     da.scale = P->d_scale;
-    da.vid = P->d_vid;
-    da.tr8 = P->d_tr8;
-    da.tgrp = P->d_tgrp;
-    da.gslot = P->d_gslot;
-    da.meta = P->d_meta;
+    da.vid = ws.vid;
+    da.tr8 = ws.tr8;
+    da.tgrp = ws.tgrp;
+    da.gslot = ws.gslot;
+    da.meta = ws.meta;
     da.act_max = act_max;
-    da.part = P->d_part;
-    da.part_slots = (int)L.part_slots;
+    da.part = part;
+    da.part_slots = (int)part_slots;
     da.main_grid = grid;
     da.tiles = tiles;
     da.err = P->d_err;
@@ -844,8 +889,15 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     bdl::PrepArgs pa;
     fill_plan_args(P, B, T, &pa, k);
     pa.tile_oct = nullptr;                        // the epilogue needs no octet lists
-    pa.tgrp = P->d_tgrp;
-    pa.decode_plan = 1;
+    pa.decode_plan = 1;                           // writes vid, tr8, tgrp, gslot, meta (and err) only
+    pa.vid = ws.vid;
+    pa.tr8 = ws.tr8;
+    pa.tgrp = ws.tgrp;
+    pa.gslot = ws.gslot;
+    pa.meta = ws.meta;
+    pa.perm = nullptr;
+    pa.gstart = pa.gcount = nullptr;
+    pa.items = nullptr;
     pa.act_max = act_max;
     // projections given the same X (gate and up) share one packed copy
     int frags = 0, jobs = 0;
@@ -859,7 +911,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         }
         bdl::PackJob& J = pa.jobs[jobs++];
         J.src = (const uint16_t*)X[q];
-        J.dst = P->d_Xp[projs[q]];
+        J.dst = ws.Xp[q];
         J.rows = T;
         J.K = da.p[q].K;
         J.frag_base = frags;
@@ -1186,9 +1238,9 @@ static int read_batch(bdlora_pool_t P, const int32_t* ids, const bdlora_segments
     return BDLORA_OK;
 }
 
-int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
-                         const void* const* W, void* const* out, const int32_t* ids, const bdlora_segments* segs,
-                         int32_t T, void* stream) {
+// Argument checks shared by the layer entry points.
+static int check_layer_args(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
+                            const void* const* W, void* const* out, int T) {
     if (!P) return fail(BDLORA_ERR_INVALID_ARG, "null pool");
     const Layout& L = P->L;
     if (n < 1 || n > BDLORA_MAX_PROJS) return fail(BDLORA_ERR_INVALID_ARG, "n must be 1..8");
@@ -1203,6 +1255,14 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
         if (T > 0 && (!aligned16(X[i]) || !aligned16(W[i]) || !aligned16(out[i])))
             return fail(BDLORA_ERR_INVALID_ARG, "X, W and out must be 16-byte aligned");
     }
+    return BDLORA_OK;
+}
+
+int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
+                         const void* const* W, void* const* out, const int32_t* ids, const bdlora_segments* segs,
+                         int32_t T, void* stream) {
+    if (int rc = check_layer_args(P, n, projs, X, W, out, T)) return rc;
+    const Layout& L = P->L;
     if (T == 0) return BDLORA_OK;
     Batch B;
     if (int rc = read_batch(P, ids, segs, T, &B)) return rc;
@@ -1210,8 +1270,47 @@ int bdlora_forward_layer(bdlora_pool_t P, int32_t n, const int32_t* projs, const
     if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
     hipStream_t s = (hipStream_t)stream;
 
-    if (use_decode(L, T)) return forward_decode(P, n, projs, X, W, out, B, T, s);
+    if (use_decode(L, T)) return forward_decode(P, n, projs, X, W, out, B, T, s, pool_dec_ws(P, n, projs));
     return forward_prefill(P, n, projs, X, W, out, B, T, s);
+}
+
+int bdlora_forward_layer_static(bdlora_pool_t P, int32_t n, const int32_t* projs, const void* const* X,
+                                const void* const* W, void* const* out, const int32_t* ids,
+                                const bdlora_segments* segs, int32_t T, void* stream) {
+    if (int rc = check_layer_args(P, n, projs, X, W, out, T)) return rc;
+    if (T == 0) return BDLORA_OK;
+    if (T > bdl::kDecodeMaxT)
+        return fail(BDLORA_ERR_SHAPE, "the static-scratch forward takes decode batches (T <= BDLORA_DECODE_MAX_T)");
+    Batch B;
+    if (int rc = read_batch(P, ids, segs, T, &B)) return rc;
+    char* base = static_cast<char*>(bdl::static_scratch(P->device));
+    if (!base)
+        return fail(BDLORA_ERR_HIP, std::string("static scratch address not available on this device: ") +
+                                        hipGetErrorString(P->static_err));
+    // the array carved in 256-byte aligned pieces: plan tables, packed
+    // activations per projection of the call, then the partial tiles
+    long long off = 0;
+    auto take = [&](long long bytes) {
+        char* p = base + off;
+        off = round_up(off + bytes, 256);
+        return p;
+    };
+    DecWs w;
+    w.meta = reinterpret_cast<int*>(take(16));
+    w.vid = reinterpret_cast<int*>(take(4LL * bdl::kDecodeMaxT));
+    w.tr8 = reinterpret_cast<int*>(take(4LL * bdl::kDecodeMaxT));
+    w.tgrp = reinterpret_cast<int*>(take(4LL * bdl::kDecodeMaxT));
+    w.gslot = reinterpret_cast<int*>(take(4LL * (bdl::kDecodeMaxT + 1)));
+    for (int i = 0; i < n; ++i) w.Xp[i] = reinterpret_cast<uint16_t*>(take(round_up(T, 16) * P->L.proj[projs[i]].K * 2LL));
+    if (off > bdl::kStaticScratchBytes)
+        return fail(BDLORA_ERR_SHAPE, "the call's packed activations need " + std::to_string(off) +
+                                          " bytes, more than BDLORA_STATIC_SCRATCH_BYTES");
+    w.part = nullptr;
+    w.arena = base + off;
+    w.arena_bytes = bdl::kStaticScratchBytes - off;
+    DeviceGuard guard(P->device);
+    if (!guard.ok) return fail(BDLORA_ERR_HIP, "hipSetDevice failed");
+    return forward_decode(P, n, projs, X, W, out, B, T, (hipStream_t)stream, w);
 }
 
 int bdlora_forward_shard(bdlora_pool_t P, int32_t proj, const void* X, const void* W, const int32_t* ids,
@@ -1267,11 +1366,11 @@ int bdlora_forward_mlp(bdlora_pool_t P, int32_t act, const int32_t* first, int32
         m1.h_dst = h;
         m1.h_KS = Ni / 32;
         void* none[2] = {nullptr, nullptr};
-        int rc = forward_decode(P, nf, first, xs, W_first, none, B, T, s, m1);
+        int rc = forward_decode(P, nf, first, xs, W_first, none, B, T, s, pool_dec_ws(P, nf, first), m1);
         if (rc) return rc;
         DecMode m2;
         m2.prep = false;
-        return forward_decode(P, 1, dn, xs, wd, od, B, T, s, m2);
+        return forward_decode(P, 1, dn, xs, wd, od, B, T, s, pool_dec_ws(P, 1, dn), m2);
     }
     // prefill: gate/up outputs in fp32 to the pool's workspace, H packed,
     // then down

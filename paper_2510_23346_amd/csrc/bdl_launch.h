@@ -201,4 +201,13 @@ hipError_t launch_pack_int4(const uint8_t* q, const uint16_t* scales, uint32_t* 
                             int K, hipStream_t s);
 hipError_t launch_mlp_pack(const float* G, const float* U, uint16_t* dst, int T, int N, hipStream_t s);
 
+// Static scratch of the allocation-free decode entry point (bdl_static.hip).
+constexpr long long kStaticScratchBytes = BDLORA_STATIC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+// Take the address of the current device's copy (call once per device, with
+// it current; later calls return at once).
+hipError_t static_scratch_init(int device);
+// That address (null before static_scratch_init succeeded on the device).
+void* static_scratch(int device);
+
 }  // namespace bdl

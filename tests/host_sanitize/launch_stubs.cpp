@@ -26,5 +26,7 @@ hipError_t launch_pack_int4(const uint8_t*, const uint16_t*, uint32_t*, uint16_t
 hipError_t launch_mlp_pack(const float*, const float*, uint16_t*, int, int, hipStream_t) {
     return hipErrorNotSupported;
 }
+hipError_t static_scratch_init(int) { return hipErrorNotSupported; }
+void* static_scratch(int) { return nullptr; }
 
 }  // namespace bdl
