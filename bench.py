@@ -345,6 +345,58 @@ def attainable():
     return {"copy_GBps": round(copy_gbs, 1), "hipblaslt_bf16_8192cube_TFLOPs": round(gemm_tfs, 1)}
 
 
+def time_steps(step, R, K, warmup, eager=False):
+    """Run ``warmup`` steps, then time exactly K: captured into HIP graphs of
+    one pass over the R rotated input copies (plus one for a remainder), the
+    wall clock between torch.cuda.synchronize() calls; HIP events around each
+    replay give the per-step distribution.  ``step(i, stream)`` enqueues step
+    i on ``stream``.  Returns (ms per step, percentiles or None)."""
+    import numpy as np
+    import torch
+
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        step(i, stream)
+    torch.cuda.synchronize()
+    replays = []
+    if not eager:
+        def capture(n):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+                cs = torch.cuda.current_stream()
+                for i in range(n):
+                    step(i, cs)
+            return g
+        full, rem = divmod(K, R)
+        g_full = capture(R) if full else None
+        g_rem = capture(rem) if rem else None
+        for _ in range(2):
+            if g_full:
+                g_full.replay()
+        torch.cuda.synchronize()
+        replays = [(g_full, R)] * full + ([(g_rem, rem)] if g_rem else [])
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(replays) + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    if eager:
+        for i in range(K):
+            step(i, stream)
+    else:
+        evs[0].record(stream)
+        for j, (g, _) in enumerate(replays):
+            g.replay()
+            evs[j + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pct = None
+    if replays:
+        per = np.array([evs[j].elapsed_time(evs[j + 1]) / n for j, (_, n) in enumerate(replays)])
+        pct = {"p10": round(float(np.percentile(per, 10)), 5), "p50": round(float(np.percentile(per, 50)), 5),
+               "p90": round(float(np.percentile(per, 90)), 5), "samples": int(per.size),
+               "steps_per_sample": R}
+    return (t1 - t0) * 1e3 / K, pct
+
+
 def measure(index, K, warmup, rotate=0, eager=False):
     """Time K steps of workload ``index``; returns its part of the JSON line
     and the drawn layer (for the CPU baseline)."""
@@ -379,48 +431,7 @@ def measure(index, K, warmup, rotate=0, eager=False):
         pool, dl = sets[i % R]
         pool.forward_layer(projs, dl.X, dl.W, dl.out, dl.ids, stream=s)
 
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    # graphs: one per pass over the R copies, plus one for a remainder
-    replays = []
-    if not eager:
-        def capture(n):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=torch.cuda.Stream()):
-                cs = torch.cuda.current_stream()
-                for i in range(n):
-                    step(i, cs)
-            return g
-        full, rem = divmod(K, R)
-        g_full = capture(R) if full else None
-        g_rem = capture(rem) if rem else None
-        for _ in range(2):
-            if g_full:
-                g_full.replay()
-        torch.cuda.synchronize()
-        replays = [(g_full, R)] * full + ([(g_rem, rem)] if g_rem else [])
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(replays) + 1)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    if eager:
-        for i in range(K):
-            step(i)
-    else:
-        evs[0].record(stream)
-        for j, (g, _) in enumerate(replays):
-            g.replay()
-            evs[j + 1].record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / K
-    pct = None
-    if replays:
-        per = np.array([evs[j].elapsed_time(evs[j + 1]) / n for j, (_, n) in enumerate(replays)])
-        pct = {"p10": round(float(np.percentile(per, 10)), 5), "p50": round(float(np.percentile(per, 50)), 5),
-               "p90": round(float(np.percentile(per, 90)), 5), "samples": int(per.size),
-               "steps_per_sample": R}
+    ms_per_step, pct = time_steps(step, R, K, warmup, eager)
 
     # per-kernel durations with HIP events on the launch stream (eager)
     n_prof = max(R, min(K, 400))
@@ -514,6 +525,68 @@ def measure(index, K, warmup, rotate=0, eager=False):
     return res, spec, layer
 
 
+def measure_mlp(index, K, warmup, eager=False):
+    """The MLP shard of Alg. 1 on the Llama-3.1-8B layer shard of workload
+    ``index`` (1: 64 decode tokens; 2: 8 x 512 prefill): gate and up, H =
+    silu(gate) * up held in bf16, then down, through bdlora_forward_mlp, timed
+    like the layer steps."""
+    import numpy as np
+    import torch
+
+    import paper_2510_23346_amd as bd
+    import workloads as wl
+    from workloads.gpu import DeviceLayer, load_adapters, make_pool
+
+    spec = wl.workload(index)
+    names = [p.name for p in spec.projs]
+    gi, ui, di = names.index("gate"), names.index("up"), names.index("down")
+    ids_np = wl.draw_ids(spec)
+    resident = list(range(spec.n_slots))
+    layer = wl.draw_layer(spec, slots=resident)
+    T = spec.T
+    g, d = spec.projs[gi], spec.projs[di]
+    Ni = g.d_out
+    active = sorted({int(a) for a in ids_np if a >= 0})
+    w_bytes = 2 * (2 * g.d_in * Ni + d.d_in * d.d_out)
+    io_bytes = 2 * T * g.d_in + 2 * 2 * T * Ni + 2 * T * d.d_out      # X, H written and read, out
+    ad_bytes = sum(2 * spec.ranks[a] * (2 * (g.d_in + Ni) + d.d_in + d.d_out) for a in active)
+    step_bytes = w_bytes + io_bytes + ad_bytes
+    flops = 2 * T * (2 * g.d_in * Ni + d.d_in * d.d_out) + sum(
+        2 * spec.ranks[a] * (2 * (g.d_in + Ni) + d.d_in + d.d_out) for a in ids_np if a >= 0)
+    R = max(2, math.ceil(2 * MALL_BYTES / step_bytes))
+    sets = []
+    for i in range(R):
+        pool = make_pool(spec)
+        load_adapters(pool, spec, resident, cache=layer.adapters)
+        sets.append((pool, DeviceLayer(layer)))
+
+    def step(i, s=None):
+        pool, dl = sets[i % R]
+        pool.forward_mlp(bd.ACT_SILU_MUL, [gi, ui], di, dl.X[gi], [dl.W[gi], dl.W[ui]], dl.W[di], dl.out[di],
+                         dl.ids, stream=s)
+
+    ms, pct = time_steps(step, R, max(K, 20 * R), warmup, eager)
+    step(0)
+    torch.cuda.synchronize()
+    path = sets[0][0].last_path()
+    for pool, _ in sets:
+        pool.close()
+    del sets
+    torch.cuda.synchronize()
+    return {
+        "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s", "ms_per_step": round(ms, 5),
+        "step_ms_events": pct,
+        "config": {"workload": spec.name.replace("layer", "mlp"), "tokens": T,
+                   "projections": ["gate", "up", "down"], "act": "silu(gate) * up",
+                   "adapters_resident": len(resident), "adapters_active": len(active),
+                   "down_path": path, "timing": f"HIP graphs over {R} rotated input copies"},
+        "step_hbm": {"algorithmic_bytes": step_bytes,
+                     "frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "step_mfma": {"algorithmic_flops": flops,
+                      "frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)},
+    }
+
+
 HEADLINE = 4                     # the largest single-GPU configuration
 OTHERS = (0, 1, 2, 3, 5)         # reported beside it in the same line
 
@@ -572,6 +645,11 @@ def main():
             r, sp, _ = measure(i, max(args.steps, 400), args.warmup, 0, args.eager)
             print(f"bench: {sp.name} {r['ms_per_step']} ms/step", file=sys.stderr, flush=True)
             others[sp.name] = r
+        mlps = {}
+        for i in (1, 2):
+            r = measure_mlp(i, args.steps, args.warmup, args.eager)
+            print(f"bench: {r['config']['workload']} {r['ms_per_step']} ms/step", file=sys.stderr, flush=True)
+            mlps[r["config"]["workload"]] = r
     out = {
         "metric": "tokens/s per layer-shard",
         "value": head["value"],
@@ -598,6 +676,7 @@ def main():
     if not args.only:
         out["attainable"] = attainable()
         out["workloads"] = others
+        out["mlp"] = mlps
     print(json.dumps(out), flush=True)
 
 

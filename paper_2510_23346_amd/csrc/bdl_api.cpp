@@ -949,9 +949,18 @@ static bool use_decode(const Layout& L, int T) {
 // Batches above the decode size: prep (plan + packing; with pack = false the
 // packed activations are already in place), shrink, base product with the
 // expand fused in.
+// The MLP's first projections (bdlora_forward_mlp, batches above the decode
+// size): where H goes and how it is formed.
+struct MlpOut {
+    int act;                 // BDLORA_ACT_*
+    uint16_t* h;             // H in the fragment layout of down's input
+    int h_KS;                // its k-steps (down's d_in / 32)
+    float* f32[2];           // 64-row path: the projections' fp32 outputs (formed into H afterwards)
+};
+
 static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const void* const* X,
                            const void* const* W, void* const* out, const Batch& B, int T, hipStream_t s,
-                           bool pack = true, float* const* out_f32 = nullptr) {
+                           bool pack = true, const MlpOut* mlp = nullptr) {
     const Layout& L = P->L;
     long long col_blocks = 0;
     for (int i = 0; i < n; ++i) col_blocks += L.proj[projs[i]].N / 16;
@@ -964,9 +973,11 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     // heavy projections first so the long-running tiles start early
     std::vector<int> order(n);
     for (int i = 0; i < n; ++i) order[i] = i;
-    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-        return (long long)L.proj[projs[x]].K * L.proj[projs[x]].N > (long long)L.proj[projs[y]].K * L.proj[projs[y]].N;
-    });
+    if (!mlp)        // (the MLP's gate stays first: it leads the paired tiles)
+        std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+            return (long long)L.proj[projs[x]].K * L.proj[projs[x]].N >
+                   (long long)L.proj[projs[y]].K * L.proj[projs[y]].N;
+        });
     // the loaded adapters bound the distinct ones the batch can use; the
     // path choices below take that bound (the host does not see device ids,
     // and both forms of the batch must take the same launches)
@@ -1035,9 +1046,14 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         }
         mid = mid && (2 * part_bytes * 10 <= 6 * w_bytes || T <= 8 * n_loaded);
     }
+    // MLP on the large-tile and medium-batch paths: their epilogues form H
+    // and write it once, in bf16 (gate and up in paired tiles); on the
+    // 64-row path the projections write fp32 and a pack launch forms H
+    const bool h_fused = mlp && (big || mid);
+    const bool paired = h_fused && mlp->act == BDLORA_ACT_SILU_MUL;
     const int tiles_m = (T + MT - 1) / MT;
     const int tm = big ? (T + bdl::kBigM - 1) / bdl::kBigM : tiles_m;
-    const int tn = big ? bdl::kBigN : NT;
+    const int tn = big ? (paired ? bdl::kBigN / 2 : bdl::kBigN) : NT;
     // Large tiles: a projection's tiles are cut into ksplit k-ranges of about
     // q k-steps, q = (all tile k-steps) / (compute units), so that the work
     // items fill the chip once; ksplit = 1 when its K is at most q.  The
@@ -1047,7 +1063,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     for (int i = 0; i < n; ++i) ksplit[i] = 1;
     if (big) {
         long long work = 0;
-        for (int i = 0; i < n; ++i) {
+        for (int i = 0; i < (paired ? 1 : n); ++i) {        // paired: the gate's tiles carry up's columns
             const ProjInfo& pi = L.proj[projs[i]];
             work += (long long)tm * ((pi.N + tn - 1) / tn) * (pi.K / 32);
         }
@@ -1065,7 +1081,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         pl.W = (const uint16_t*)W[i];
         pl.Ws = int4_scales(pi, W[i]);
         pl.out = (uint16_t*)out[i];
-        pl.out_f32 = out_f32 ? out_f32[i] : nullptr;
+        pl.out_f32 = mlp && !h_fused ? mlp->f32[i] : nullptr;
         pl.Z = P->d_Z[projs[i]];
         pl.zplane = (long long)L.max_tokens * pi.zs;
         pl.K = pi.K;
@@ -1078,18 +1094,25 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         pl.tiles_n = (pi.N + tn - 1) / tn;
         pl.tile_base = tile;
         pl.ksplit = ksplit[i];
-        tile += tm * pl.tiles_n * pl.ksplit;
         pl.fix_base = fix;
-        pl.fix_count = pl.ksplit > 1 ? tm * pl.tiles_n : 0;
         pl.part_base = pslot;
-        fix += pl.fix_count;
-        pslot += pl.fix_count * pl.ksplit;
+        if (paired && q == 1) {
+            // up has no tiles of its own (gate's tiles hold its columns): its
+            // bases sit past every item so that none maps to it
+            pl.ksplit = ksplit[0];
+            pl.fix_count = 0;
+        } else {
+            tile += tm * pl.tiles_n * pl.ksplit;
+            pl.fix_count = pl.ksplit > 1 ? tm * pl.tiles_n : 0;
+            fix += pl.fix_count;
+            pslot += pl.fix_count * pl.ksplit;
+        }
         if (mid) {
             pl.ksplit = mid_split[i];
             pl.part_base = pslot;
             pslot += (pi.N + mid_tn - 1) / mid_tn * mid_split[i];
             pl.col_base = mid_cols;
-            mid_cols += (pi.N + 63) / 64;
+            if (!(paired && q == 1)) mid_cols += (pi.N + 63) / 64;
         }
         cch = std::max(cch, (pi.S * L.r8max + nts - 1) / nts);
     }
@@ -1130,6 +1153,15 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     fa.mid_items = mid ? mid_items : 0;
     fa.mid_col_tiles = mid ? mid_cols : 0;
     fa.max_slots = L.max_slots;
+    fa.mlp_act = h_fused ? mlp->act : -1;
+    fa.h_dst = h_fused ? mlp->h : nullptr;
+    fa.h_KS = h_fused ? mlp->h_KS : 0;
+    if (paired) {
+        // up's bases past gate's items (and past the epilogue's column tiles)
+        fa.p[1].tile_base = tile;
+        fa.p[1].fix_base = fix;
+        fa.p[1].col_base = mid_cols;
+    }
     if (pslot > bdl::kBigPartSlots) return fail(BDLORA_ERR_SHAPE, "large-tile split exceeds its partial workspace");
     if (fa.items_bound > P->items_cap || (long long)tiles_m * fa.oct_cap > P->oct_elems)
         return fail(BDLORA_ERR_SHAPE, "batch exceeds the pool workspace");
@@ -1372,13 +1404,21 @@ int bdlora_forward_mlp(bdlora_pool_t P, int32_t act, const int32_t* first, int32
         m2.prep = false;
         return forward_decode(P, 1, dn, xs, wd, od, B, T, s, pool_dec_ws(P, 1, dn), m2);
     }
-    // prefill: gate/up outputs in fp32 to the pool's workspace, H packed,
-    // then down
-    float* g_u[2] = {P->d_mlp, P->d_mlp + (size_t)T * Ni};
+    // larger batches: the first projections' epilogue writes H (bf16,
+    // packed as down's input) on the large-tile and medium-batch paths; on
+    // the 64-row path they write fp32 to the pool's workspace and a pack
+    // launch forms H.  Then down reads H in place.
+    MlpOut mo;
+    mo.act = act;
+    mo.h = h;
+    mo.h_KS = Ni / 32;
+    mo.f32[0] = P->d_mlp;
+    mo.f32[1] = P->d_mlp + (size_t)T * Ni;
     void* none[2] = {nullptr, nullptr};
-    int rc = forward_prefill(P, nf, first, xs, W_first, none, B, T, s, true, g_u);
+    int rc = forward_prefill(P, nf, first, xs, W_first, none, B, T, s, true, &mo);
     if (rc) return rc;
-    BDL_HIP(bdl::launch_mlp_pack(g_u[0], act == BDLORA_ACT_SILU_MUL ? g_u[1] : nullptr, h, T, Ni, s));
+    if (P->last_path == BDLORA_PATH_TILE64)
+        BDL_HIP(bdl::launch_mlp_pack(mo.f32[0], act == BDLORA_ACT_SILU_MUL ? mo.f32[1] : nullptr, h, T, Ni, s));
     return forward_prefill(P, 1, dn, xs, wd, od, B, T, s, false);
 }
 

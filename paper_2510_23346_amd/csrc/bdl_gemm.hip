@@ -53,8 +53,9 @@ typedef __attribute__((address_space(3))) void lds_void;
 // keeps its LDS wait counts exact.
 template <int CP>
 struct BigSrc {
-    __amdgpu_buffer_rsrc_t rx, rw;
+    __amdgpu_buffer_rsrc_t rx, rw, rw2;
     int vo[CP];   // this lane's byte offset at k-step 0
+    bool two[CP]; // paired gate/up tiles: the copy reads the second weight (rw2)
 };
 
 // issue this thread's CP fragment copies of k-step ks into one stage
@@ -62,8 +63,9 @@ template <int CP, int NW>
 __device__ __forceinline__ void big_issue(const BigSrc<CP>& s, int ks, u32x4* stage, int w) {
 #pragma unroll
     for (int i = 0; i < CP; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(i < CP / 2 ? s.rx : s.rw, (lds_void*)(stage + (w + NW * i) * 64), 16,
-                                                 s.vo[i] + ks * 1024, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(i < CP / 2 ? s.rx : (s.two[i] ? s.rw2 : s.rw),
+                                                 (lds_void*)(stage + (w + NW * i) * 64), 16, s.vo[i] + ks * 1024, 0,
+                                                 0, 0);
 }
 
 // wait until at most n of this thread's copies (and none of its LDS reads)
@@ -123,7 +125,13 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     const int T = a.T, N = P.N, KS = P.K >> 5;
     const int nrb = (T + 15) >> 4, ncb = N >> 4;
     const int rbase = mt * kBigM + wr * 16 * RB; // first row of this wave
-    const int c0 = nt * kBigN + wc * 128;        // first column of this wave
+    // Paired tiles (the MLP's gate and up, equal shapes): the tile's 256
+    // columns are gate columns nt 128 .. + 127 (waves of column half 0) and
+    // the same up columns (half 1), so that H = silu(gate) * up is formed in
+    // the workgroup.  Projection p is gate, p + 1 up.
+    const bool pair = a.mlp_act == BDLORA_ACT_SILU_MUL;
+    const int c0 = pair ? nt * 128 : nt * kBigN + wc * 128;   // first column of this wave
+    const ProjLaunch& Pe = a.p[p + (pair && wc == 1 ? 1 : 0)];  // this wave's projection
 
     // expand inputs that do not depend on the base product: fetched first.
     // Octet lists are per 64-row block; a block wholly past T has none.
@@ -173,10 +181,16 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     BigSrc<CP> src;
     src.rx = __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
     src.rw = __builtin_amdgcn_make_buffer_rsrc((void*)P.W, 0, ncb * KS * 1024, kRawBufferWord3);
+    src.rw2 = pair ? __builtin_amdgcn_make_buffer_rsrc((void*)a.p[p + 1].W, 0, ncb * KS * 1024, kRawBufferWord3)
+                   : src.rw;
 #pragma unroll
     for (int i = 0; i < CP; ++i) {
         const int f = w + NW * i;
-        if (i < CP / 2 && a.rowtok) {
+        src.two[i] = pair && i >= CP / 2 && f - 16 >= 8;
+        if (i >= CP / 2 && pair) {
+            // weight fragment f - 16: column block (f - 16) mod 8 of gate (< 8) or up
+            src.vo[i] = min(nt * 8 + ((f - 16) & 7), ncb - 1) * KS * 1024 + k0 * 1024 + l * 16;
+        } else if (i < CP / 2 && a.rowtok) {
             // the lane's row is gathered: its token's fragment, lane slot
             // (token mod 16) + 16 (l / 16); rows past T repeat a valid token
             const int t = (int)min((unsigned)a.rowtok[min((mt * 16 + f) * 16 + lr, T - 1)], (unsigned)(T - 1));
@@ -284,7 +298,7 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         int sgm = 0;
 #pragma unroll
         for (int q = 1; q < kMaxSlices; ++q)
-            if (q < P.n_slices && c >= P.slice_col[q]) sgm = q;
+            if (q < Pe.n_slices && c >= Pe.slice_col[q]) sgm = q;
         sig[cb] = sgm;
     }
     const u32x4 zero4 = u32x4{0u, 0u, 0u, 0u};
@@ -299,7 +313,7 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
 #pragma unroll
             for (int cb = 0; cb < 8; ++cb) {
                 const int col = min(c0 + cb * 16 + lr, N - 1);
-                bv[cb] = cd >= 0 ? ld16(a.pool + (size_t)slot * a.slot_stride + P.b_off + (size_t)col * r8s + j0)
+                bv[cb] = cd >= 0 ? ld16(a.pool + (size_t)slot * a.slot_stride + Pe.b_off + (size_t)col * r8s + j0)
                                  : zero4;
             }
             u32x4 zh[4], zl[4];
@@ -310,9 +324,9 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
                     for (int rb = 0; rb < 4; ++rb) {
                         const bool match = cd >= 0 && rvid[4 * h + rb] == slot;
                         const uint16_t* zp =
-                            P.Z + (size_t)max(tok[4 * h + rb], 0) * P.zs + sig[cb] * a.r8max + j0;
+                            Pe.Z + (size_t)max(tok[4 * h + rb], 0) * Pe.zs + sig[cb] * a.r8max + j0;
                         zh[rb] = match ? ld16(zp) : zero4;
-                        zl[rb] = match ? ld16(zp + P.zplane) : zero4;
+                        zl[rb] = match ? ld16(zp + Pe.zplane) : zero4;
                     }
                 }
 #pragma unroll
@@ -329,6 +343,48 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
 
     // store: lane (lr, lg) of block (rb, cb) holds row rbase + 16 rb + lr
     // (token tok[rb]), columns c0 + 16 cb + 4 lg + i
+    if (a.mlp_act >= 0) {
+        // the MLP intermediate: H in bf16, once, in the fragment layout of the
+        // second projection's input (element [(t/16 KS + c/32) 512 + (t%16 +
+        // 16 ((c%32)/8)) 8 + c%8] for token t, column c); the 4 columns of a
+        // lane are contiguous there.  Paired tiles first hand the up values to
+        // the gate waves through LDS (the k-loop's stages are free: every
+        // copy has landed and every wave is past its last read).
+        f32x4* xl = reinterpret_cast<f32x4*>(lds);
+        if (pair) {
+            __syncthreads();
+            if (wc == 1) {
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                    for (int cb = 0; cb < 8; ++cb) xl[((wr * RB + rb) * 8 + cb) * 64 + l] = acc[rb][cb];
+            }
+            __syncthreads();
+            if (wc == 1) return;
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int row = tok[rb];
+            if (row < 0) continue;
+#pragma unroll
+            for (int cb = 0; cb < 8; ++cb) {
+                const int col = c0 + cb * 16 + 4 * lg;
+                if (col >= N) continue;
+                f32x4 v = acc[rb][cb];
+                if (pair) {
+                    const f32x4 u = xl[((wr * RB + rb) * 8 + cb) * 64 + l];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) v[i] = v[i] / (1.f + __expf(-v[i])) * u[i];
+                }
+                const size_t idx = ((size_t)(row >> 4) * a.h_KS + (col >> 5)) * kFrag +
+                                   ((row & 15) + 16 * ((col & 31) >> 3)) * 8 + (col & 7);
+                const uint32_t lo = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+                const uint32_t hi = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+                *reinterpret_cast<uint2*>(a.h_dst + idx) = make_uint2(lo, hi);
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
         const int row = tok[rb];
@@ -519,23 +575,23 @@ __device__ __forceinline__ void fma_ranks8(float (&acc)[CPT], const u32x4 (&b)[C
     }
 }
 
+// Workgroup rows and their LDS: RPW rows x 64 columns of B^T ranks 0..15.
 template <int CPT>
-__global__ __launch_bounds__(256) void mid_epi_kernel(FwdArgs a) {
-    static_assert(CPT == 4 || CPT == 8, "one or two 4-column lanes of a partial block");
-    constexpr int TPR = 64 / CPT, RPW = 256 / TPR, NQ = CPT / 4;   // threads per row, rows per workgroup
-    const int tile = blockIdx.x;
-    int p = 0;
-#pragma unroll
-    for (int q = 1; q < kMaxProjs; ++q)
-        if (q < a.n_proj && tile >= a.p[q].col_base) p = q;
-    const ProjLaunch& P = a.p[p];
+struct MidEpiLds {
+    static constexpr int TPR = 64 / CPT, RPW = 256 / TPR;   // threads per row, rows per workgroup
+    u32x4 bl[RPW * 64 * 2];
+    int rinfo[RPW];
+};
+
+// The outputs of row position pos (rowtok order; token tt) in columns
+// col .. col + CPT - 1 of 64-column tile `local` of projection P: the sum of
+// its partials in range order plus the expand of the token's own adapter,
+// in fp32.  Every thread of the workgroup calls it (it holds barriers).
+template <int CPT>
+__device__ __forceinline__ void mid_epi_sum(const FwdArgs& a, const ProjLaunch& P, int local, int pos, int col,
+                                            MidEpiLds<CPT>& sh, float (&acc)[CPT]) {
+    constexpr int TPR = MidEpiLds<CPT>::TPR, RPW = MidEpiLds<CPT>::RPW, NQ = CPT / 4;
     const int T = a.T, N = P.N;
-    // rows are positions in rowtok order (those of the main launch's tile)
-    const int pos = blockIdx.y * RPW + threadIdx.x / TPR;
-    const int col = (tile - P.col_base) * 64 + (threadIdx.x % TPR) * CPT;
-    // threads past the last row or column compute on clamped indices and
-    // store nothing (every load is issued without waiting on a branch)
-    const bool live = pos < T && col < N;
     const int pp = min(pos, T - 1), cc = min(col, N - CPT);
     // the row's adapter (slot and rank, from the plan's row table) and token,
     // loaded before the partials so that waiting for them leaves the
@@ -588,22 +644,21 @@ __global__ __launch_bounds__(256) void mid_epi_kernel(FwdArgs a) {
     // consecutive 32-byte slots (two-way bank conflicts; a padded slot would
     // avoid them but the extra LDS costs more in resident workgroups).
     constexpr int SLOT = 2;                      // u32x4 per column slot: rank halves 0, 1
-    __shared__ u32x4 bl[RPW * 64 * SLOT];
-    __shared__ int rinfo[RPW];
     const int rl = threadIdx.x / TPR;            // this thread's row in the workgroup
-    if (threadIdx.x % TPR == 0) rinfo[rl] = info;
+    __syncthreads();                             // a previous call's readers are done
+    if (threadIdx.x % TPR == 0) sh.rinfo[rl] = info;
     __syncthreads();
-    const int tile_c0 = (tile - P.col_base) * 64;
+    const int tile_c0 = local * 64;
 #pragma unroll
     for (int k = 0; k < RPW * 128 / 256; ++k) {
         const int idx = k * 256 + threadIdx.x, row = idx >> 7, pc = idx & 127, c = pc >> 1, h = pc & 1;
-        const int inf = rinfo[row];
+        const int inf = sh.rinfo[row];
         const int vs = inf >= 0 ? min(inf & 0xffff, a.max_slots - 1) : 0;
         const int rs = inf >= 0 ? min(inf >> 16, a.r8max) : 0;
         // columns past N and halves past the rank read a valid piece, unused
         const int col_c = min(tile_c0 + c, N - 1), hh = 8 * h < rs ? 8 * h : 0;
         const u32x4 piece = ld16(a.pool + (size_t)vs * a.slot_stride + P.b_off + (size_t)col_c * rs + hh);
-        bl[(row * 64 + (c % CPT) * (64 / CPT) + c / CPT) * SLOT + h] = piece;
+        sh.bl[(row * 64 + (c % CPT) * (64 / CPT) + c / CPT) * SLOT + h] = piece;
     }
     __syncthreads();
     u32x4 bq[2][CPT];
@@ -612,10 +667,9 @@ __global__ __launch_bounds__(256) void mid_epi_kernel(FwdArgs a) {
 #pragma unroll
         for (int c = 0; c < CPT; ++c)
 #pragma unroll
-            for (int h = 0; h < 2; ++h) bq[h][c] = bl[(rl * 64 + c * (64 / CPT) + g) * SLOT + h];
+            for (int h = 0; h < 2; ++h) bq[h][c] = sh.bl[(rl * 64 + c * (64 / CPT) + g) * SLOT + h];
     }
 
-    float acc[CPT];
 #pragma unroll
     for (int c = 0; c < CPT; ++c) acc[c] = 0.f;
 #pragma unroll
@@ -644,7 +698,52 @@ __global__ __launch_bounds__(256) void mid_epi_kernel(FwdArgs a) {
         for (int c = 0; c < CPT; ++c) br[c] = ld16(bb + (size_t)c * r8s + j0);
         fma_ranks8<CPT>(acc, br, ld16(zp + j0), ld16(zp + j0 + P.zplane));
     }
+}
+
+template <int CPT>
+__global__ __launch_bounds__(256) void mid_epi_kernel(FwdArgs a) {
+    static_assert(CPT == 4 || CPT == 8, "one or two 4-column lanes of a partial block");
+    constexpr int TPR = MidEpiLds<CPT>::TPR, RPW = MidEpiLds<CPT>::RPW, NQ = CPT / 4;
+    __shared__ MidEpiLds<CPT> sh;
+    const int tile = blockIdx.x;
+    int p = 0;
+#pragma unroll
+    for (int q = 1; q < kMaxProjs; ++q)
+        if (q < a.n_proj && tile >= a.p[q].col_base) p = q;
+    const ProjLaunch& P = a.p[p];
+    const int T = a.T, N = P.N;
+    // rows are positions in rowtok order (those of the main launch's tile)
+    const int pos = blockIdx.y * RPW + threadIdx.x / TPR;
+    const int col = (tile - P.col_base) * 64 + (threadIdx.x % TPR) * CPT;
+    // threads past the last row or column compute on clamped indices and
+    // store nothing (every load is issued without waiting on a branch)
+    const bool live = pos < T && col < N;
+    const int tt = (int)min((unsigned)a.rowtok[min(pos, T - 1)], (unsigned)(T - 1));
+    float acc[CPT];
+    mid_epi_sum<CPT>(a, P, tile - P.col_base, pos, col, sh, acc);
+    if (a.mlp_act == BDLORA_ACT_SILU_MUL) {
+        // gate's tiles only: up (projection p + 1) for the same outputs
+        float up[CPT];
+        mid_epi_sum<CPT>(a, a.p[p + 1], tile - P.col_base, pos, col, sh, up);
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) acc[c] = acc[c] / (1.f + __expf(-acc[c])) * up[c];
+    }
     if (!live) return;
+    if (a.mlp_act >= 0) {
+        // the MLP intermediate H in bf16 in the second projection's input
+        // layout (token tt, columns col ..): CPT / 4 pieces of 4 contiguous
+        // elements
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int c = col + 4 * q;
+            const size_t idx = ((size_t)(tt >> 4) * a.h_KS + (c >> 5)) * kFrag + ((tt & 15) + 16 * ((c & 31) >> 3)) * 8 +
+                               (c & 7);
+            const uint32_t lo = (uint32_t)f2bf(acc[4 * q]) | ((uint32_t)f2bf(acc[4 * q + 1]) << 16);
+            const uint32_t hi = (uint32_t)f2bf(acc[4 * q + 2]) | ((uint32_t)f2bf(acc[4 * q + 3]) << 16);
+            *reinterpret_cast<uint2*>(a.h_dst + idx) = make_uint2(lo, hi);
+        }
+        return;
+    }
     if (P.out_f32) {
         float* o = P.out_f32 + (size_t)tt * N + col;
 #pragma unroll

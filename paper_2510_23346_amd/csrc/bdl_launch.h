@@ -76,6 +76,15 @@ struct FwdArgs {
     int mid_items;            // medium-batch GEMM: work items (tile x k-range) over all projections
     int mid_col_tiles;        // medium-batch GEMM: 64-column epilogue tiles over all projections
     int max_slots;            // pool slots
+    // MLP intermediate (large-tile and medium-batch launches of the MLP's
+    // first projections): -1 writes out / out_f32; BDLORA_ACT_NONE writes
+    // H = projection 0's output, BDLORA_ACT_SILU_MUL H = silu(projection 0)
+    // * projection 1 (gate and up of equal shape; their tiles are paired so
+    // one workgroup holds both), in bf16 into h_dst in the fragment layout of
+    // the second projection's input (rows = tokens, h_KS k-steps)
+    int mlp_act;
+    uint16_t* h_dst;
+    int h_KS;
 };
 
 // Activation packing job of the prep launch.

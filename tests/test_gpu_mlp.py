@@ -105,9 +105,9 @@ def test_mlp_8b_shapes_decode(torch_cuda):
 def test_mlp_70b_shapes_medium_batch(torch_cuda, T):
     # Llama-3.1-70B MLP shard at 1/8 tensor parallelism: gate/up 8192 -> 3584,
     # down 3584 -> 8192.  At these batch sizes gate and up (117 MB of weight)
-    # take the medium-batch launches with fp32 outputs (the MLP's
-    # intermediate); from about 160 tokens their partials would exceed the
-    # byte rule.  Then H is packed and down runs on its own path.
+    # take the medium-batch launches, whose epilogue pairs gate's and up's
+    # column tiles and writes H = silu(gate) * up once, in bf16, as down's
+    # packed input; then down runs on its own path.
     torch = torch_cuda
     projs = [p for p in wl.model_projs("llama-3.1-70b", 8) if p.name in ("gate", "up", "down")]
     rng = np.random.default_rng(70 + T)
@@ -154,4 +154,42 @@ def test_mlp_argument_errors(torch_cuda):
     assert call(bd.ACT_NONE, [2], 0) == -1           # a row projection first
     assert call(bd.ACT_NONE, [0], 1) == -4           # gate's width is not up's d_in
     assert call(bd.ACT_NONE, [0], 5) == -1           # index out of range
+    pool.close()
+
+
+@pytest.mark.parametrize("act_name", ["silu_mul", "none"])
+@pytest.mark.parametrize("T", [300, 600])
+def test_mlp_8b_shapes_prefill_large_tiles(torch_cuda, T, act_name):
+    # Llama-3.1-8B MLP shard at 1/8 TP above one 256-row tile: gate and up
+    # take the large tiles, paired (each workgroup holds 128 gate and the
+    # same 128 up columns), and their epilogue writes H once in bf16; runs of
+    # requests sharing an adapter, as in prefill
+    torch = torch_cuda
+    projs = [p for p in wl.model_projs("llama-3.1-8b", 8) if p.name in ("gate", "up", "down")]
+    rng = np.random.default_rng(T)
+    ranks = [16, 32, 8, 16, 64, 24]
+    ids = np.repeat(rng.integers(-1, len(ranks), size=T // 50 + 1), 50)[:T]
+    spec = wl.custom_workload(f"mlp-8b-{T}", projs, T, ranks, ids=ids, seed=T + 3)
+    layer = wl.draw_layer(spec, slots=range(len(ranks)))
+    pool = make_pool(spec)
+    load_adapters(pool, spec, range(len(ranks)), cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    g = [torch.empty((T, 1792), dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    pool.forward_layer([0, 1], [dl.X[0], dl.X[0]], [dl.W[0], dl.W[1]], g, dl.ids)
+    torch.cuda.synchronize()
+    assert pool.last_path() == "large"
+    act, first = ACTS[act_name]
+    out = torch.full((T, 4096), float("nan"), dtype=torch.bfloat16, device="cuda")
+    pool.forward_mlp(act, first, 2, dl.X[0], [dl.W[p] for p in first], dl.W[2], out, dl.ids)
+    torch.cuda.synchronize()
+    _, ref = mlp.mlp_layer_forward(layer, first, 2, act_name)
+    e = bdlora.rel_errors(device_to_float(out), ref)
+    assert e["pointwise"] <= TOL, f"T={T} act={act_name}: {e}"
+    # the same batch as segments: the same bits
+    out2 = torch.full_like(out, float("nan"))
+    pool.forward_mlp(act, first, 2, dl.X[0], [dl.W[p] for p in first], dl.W[2], out2, None,
+                     segs=bd.Segments.from_ids(ids))
+    torch.cuda.synchronize()
+    assert np.array_equal(device_to_float(out).view(np.uint32), device_to_float(out2).view(np.uint32))
+    assert pool.device_error() == 0
     pool.close()
