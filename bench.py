@@ -588,7 +588,7 @@ def measure_mlp(index, K, warmup, eager=False):
 
 
 HEADLINE = 4                     # the largest single-GPU configuration
-OTHERS = (0, 1, 2, 3, 5)         # reported beside it in the same line
+OTHERS = (0, 1, 2, 3, 5, 6)      # reported beside it in the same line
 
 
 def main():
@@ -597,7 +597,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=HEADLINE,
-                    help=f"headline workload index 0..5 (default {HEADLINE}; 5 = workload 1 with an INT4 base)")
+                    help=f"headline workload index 0..6 (default {HEADLINE}; 5 = workload 1 with an INT4 base, "
+                         "6 = workload 1 with ranks 8 and 64)")
     ap.add_argument("--only", action="store_true", help="time the headline workload only")
     ap.add_argument("--rotate", type=int, default=0, help="input copies to rotate (0 = auto)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)

@@ -181,6 +181,7 @@ struct bdlora_pool {
     int* d_tr8 = nullptr;
     int* d_perm = nullptr;
     int* d_gslot = nullptr;
+    int* d_gr8 = nullptr;
     int* d_gstart = nullptr;
     int* d_gcount = nullptr;
     int4* d_items = nullptr;
@@ -230,6 +231,7 @@ void free_pool(bdlora_pool* P) {
     f(P->d_tr8);
     f(P->d_perm);
     f(P->d_gslot);
+    f(P->d_gr8);
     f(P->d_gstart);
     f(P->d_gcount);
     f(P->d_items);
@@ -473,6 +475,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     BDL_TRY(dev_alloc(&P->d_rowtok, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_rowslot, MT, &tot));
     BDL_TRY(dev_alloc(&P->d_gslot, S + 1, &tot));
+    BDL_TRY(dev_alloc(&P->d_gr8, bdl::kDecodeMaxT + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gstart, S + 1, &tot));
     BDL_TRY(dev_alloc(&P->d_gcount, S + 1, &tot));
     P->items_cap = (long long)S + MT / 16 + 2;
@@ -510,6 +513,7 @@ int bdlora_create_pool(const bdlora_proj_desc* projs, int32_t n_projs, int32_t m
     // plan tables: entries past a batch's counts are never written by the
     // plan; zero (slot 0) rather than whatever the allocation held
     if (int r = hipz(P->d_gslot, (size_t)(S + 1) * 4)) return r;
+    if (int r = hipz(P->d_gr8, (size_t)(bdl::kDecodeMaxT + 1) * 4)) return r;
     if (int r = hipz(P->d_gstart, (size_t)(S + 1) * 4)) return r;
     if (int r = hipz(P->d_gcount, (size_t)(S + 1) * 4)) return r;
     for (int p = 0; p < n_projs; ++p)
@@ -731,6 +735,7 @@ static void fill_plan_args(bdlora_pool_t P, const Batch& B, int T, bdl::PrepArgs
     a->rowslot = nullptr;
     a->oct_perm = 0;
     a->gslot = P->d_gslot;
+    a->gr8 = nullptr;
     a->gstart = P->d_gstart;
     a->gcount = P->d_gcount;
     a->items = P->d_items;
@@ -767,6 +772,7 @@ struct DecWs {
     int* tr8 = nullptr;               // [T] padded rank of each token's adapter
     int* tgrp = nullptr;              // [T] group of each token's adapter
     int* gslot = nullptr;             // [<= 64] slots of the adapters in use
+    int* gr8 = nullptr;               // [<= 64] their padded ranks
     int* meta = nullptr;              // [4] plan counts
     uint16_t* Xp[bdl::kMaxProjs] = {};   // packed activations of the call's i-th projection
     float* part = nullptr;            // fp32 partial tiles; null: carved from arena
@@ -781,6 +787,7 @@ static DecWs pool_dec_ws(bdlora_pool_t P, int n, const int32_t* projs) {
     w.tr8 = P->d_tr8;
     w.tgrp = P->d_tgrp;
     w.gslot = P->d_gslot;
+    w.gr8 = P->d_gr8;
     w.meta = P->d_meta;
     for (int i = 0; i < n; ++i) w.Xp[i] = P->d_Xp[projs[i]];
     w.part = P->d_part;
@@ -870,6 +877,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     da.tr8 = ws.tr8;
     da.tgrp = ws.tgrp;
     da.gslot = ws.gslot;
+    da.gr8 = ws.gr8;
     da.meta = ws.meta;
     da.act_max = act_max;
     da.part = part;
@@ -894,6 +902,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     pa.tr8 = ws.tr8;
     pa.tgrp = ws.tgrp;
     pa.gslot = ws.gslot;
+    pa.gr8 = ws.gr8;
     pa.meta = ws.meta;
     pa.perm = nullptr;
     pa.gstart = pa.gcount = nullptr;
@@ -1333,6 +1342,7 @@ int bdlora_forward_layer_static(bdlora_pool_t P, int32_t n, const int32_t* projs
     w.tr8 = reinterpret_cast<int*>(take(4LL * bdl::kDecodeMaxT));
     w.tgrp = reinterpret_cast<int*>(take(4LL * bdl::kDecodeMaxT));
     w.gslot = reinterpret_cast<int*>(take(4LL * (bdl::kDecodeMaxT + 1)));
+    w.gr8 = reinterpret_cast<int*>(take(4LL * (bdl::kDecodeMaxT + 1)));
     for (int i = 0; i < n; ++i) w.Xp[i] = reinterpret_cast<uint16_t*>(take(round_up(T, 16) * P->L.proj[projs[i]].K * 2LL));
     if (off > bdl::kStaticScratchBytes)
         return fail(BDLORA_ERR_SHAPE, "the call's packed activations need " + std::to_string(off) +

@@ -61,14 +61,44 @@ struct DecSeg {
     int wdt;          // blocks in the group (4, fewer at a projection's end)
     int k0, k1;
     bool valid;
+    int dmask;        // bit j: block j of the group holds data for this batch
 };
 
+// Which of the blocks 4 gl .. 4 gl + wdt - 1 of projection P's column list
+// hold data for this batch (bit j for block 4 gl + j): weight blocks always;
+// adapter block v (position v / nbA, block v mod nbA of it) when its
+// position is an adapter in use (below n_act) and the block lies within that
+// adapter's own rank (lane i of gr holds the padded rank of the i-th adapter
+// in use), so a rank-8 adapter in a pool sized for rank 64 streams its own
+// blocks only.  One division per group; the positions advance by counting.
+__device__ __forceinline__ int dec_group_mask(const DecProj& P, int gl, int wdt, int n_act, int gr) {
+    const int v0 = 4 * gl - P.nWb;
+    if (v0 + wdt <= 0) return (1 << wdt) - 1;        // weight blocks only
+    int ai = v0 > 0 ? v0 / P.nbA : 0, c = v0 > 0 ? v0 - ai * P.nbA : v0;
+    int m = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (j < wdt) {
+            if (c < 0) {
+                m |= 1 << j;                           // a weight block
+            } else if (ai < n_act && c < ((P.n_slices * __builtin_amdgcn_readlane(gr, ai) + 15) >> 4)) {
+                m |= 1 << j;
+            }
+        }
+        if (++c >= P.nbA && c >= 0) {
+            c = 0;
+            ++ai;
+        }
+    }
+    return m;
+}
+
 // cut the segment that starts at k-step g.k0 of the current group, moving to
-// the next group (and projection) when that group is used up; groups whose
-// first block belongs to an adapter position at or past n_act are skipped.
-// n_act arrives in a vector register (lane-uniform) and is read only for
-// adapter groups, so weight segments never wait for it.
-__device__ __forceinline__ void dec_cut(const DecArgs& a, int n_act_v, unsigned se, DecSeg& g) {
+// the next group (and projection) when that group is used up; groups with no
+// weight block and no adapter block holding data are skipped.  n_act and the
+// ranks arrive in vector registers (lane-uniform / per lane) and are read
+// only for adapter groups, so weight segments never wait for them.
+__device__ __forceinline__ void dec_cut(const DecArgs& a, int n_act_v, int gr, unsigned se, DecSeg& g) {
     for (;;) {
         if (g.k0 >= g.pp.KS) {
             if (++g.gl >= ((g.pp.nb + 3) >> 2)) {
@@ -89,16 +119,20 @@ __device__ __forceinline__ void dec_cut(const DecArgs& a, int n_act_v, unsigned 
         }
         g.k1 = (int)min((unsigned)g.pp.KS, (se - g.goff + g.wdt - 1) / (unsigned)g.wdt);
         g.valid = g.k1 > g.k0;
-        const int vb0 = 4 * g.gl - a.p[g.p].nWb;
-        if (!g.valid || vb0 < 0) return;
-        if (vb0 < __builtin_amdgcn_readfirstlane(n_act_v) * a.p[g.p].nbA) return;
+        if (!g.valid) return;
+        if (4 * g.gl + g.wdt <= a.p[g.p].nWb) {
+            g.dmask = (1 << g.wdt) - 1;                // weight blocks only
+            return;
+        }
+        g.dmask = dec_group_mask(a.p[g.p], g.gl, g.wdt, __builtin_amdgcn_readfirstlane(n_act_v), gr);
+        if (g.dmask) return;
         g.k0 = g.pp.KS;
     }
 }
 
 // first segment of the unit range [sb, se): the group holding unit sb, from
 // its first k-step starting at or after sb
-__device__ __forceinline__ DecSeg dec_first(const DecArgs& a, int n_act_v, unsigned sb, unsigned se) {
+__device__ __forceinline__ DecSeg dec_first(const DecArgs& a, int n_act_v, int gr, unsigned sb, unsigned se) {
     DecSeg g;
     g.p = 0;
 #pragma unroll
@@ -109,13 +143,13 @@ __device__ __forceinline__ DecSeg dec_first(const DecArgs& a, int n_act_v, unsig
     g.goff = g.pp.ub + 4u * g.gl * g.pp.KS;
     g.wdt = min(4, g.pp.nb - 4 * g.gl);
     g.k0 = (int)((sb - g.goff + g.wdt - 1) / (unsigned)g.wdt);
-    dec_cut(a, n_act_v, se, g);
+    dec_cut(a, n_act_v, gr, se, g);
     return g;
 }
 
-__device__ __forceinline__ void dec_next(const DecArgs& a, int n_act_v, unsigned se, DecSeg& g) {
+__device__ __forceinline__ void dec_next(const DecArgs& a, int n_act_v, int gr, unsigned se, DecSeg& g) {
     g.k0 = g.k1;
-    dec_cut(a, n_act_v, se, g);
+    dec_cut(a, n_act_v, gr, se, g);
 }
 
 // The k-steps of a segment that K-part kq of NKQ handles: [*kw, *kw + items).
@@ -233,9 +267,10 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
     // waited for only where an adapter segment first needs them, so the base
     // weight's loads start without waiting for the plan.
     const int gs = l < a.act_max ? a.gslot[l] : 0;
+    const int gr = l < a.act_max ? a.gr8[l] : 0;
     const int n_act_v = __builtin_amdgcn_raw_buffer_load_b32(
         __builtin_amdgcn_make_buffer_rsrc((void*)a.meta, 0, 4, kRawBufferWord3), 0, 0, 0);
-    DecSeg cs = dec_first(a, n_act_v, sb, se);
+    DecSeg cs = dec_first(a, n_act_v, gr, sb, se);
     if (!cs.valid) return;
 
     // load cursor: segment, this wave's first k-step and load count in it
@@ -257,9 +292,17 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
         for (int rb = 0; rb < MB; ++rb) xb[rb] = reinterpret_cast<const char*>(P.Xp + frag_index(rb, 0, KS));
         lq = Q4 && P.Ws && 4 * ls.gl < P.nWb;
         const size_t qs = (size_t)KS * kInt4FragBytes, ss = (size_t)(KS / kInt4Group) * 32;
+        // blocks that hold no data for this batch (past an adapter's own rank,
+        // or an adapter position not in use) load the group's first block
+        // that does instead: the same bytes, served by the caches, so only
+        // data blocks cost HBM traffic; their sums are never read.  (The
+        // segment's group passed dec_cut, so such a block exists; groups of
+        // INT4 weight blocks are never mixed with adapter blocks.)
+        const int vbf = 4 * ls.gl + __builtin_ctz((unsigned)ls.dmask | 16u);
 #pragma unroll
         for (int c = 0; c < NB; ++c) {
-            const int vb = 4 * ls.gl + min(cg * NB + c, ls.wdt - 1);
+            const int jc = min(cg * NB + c, ls.wdt - 1);
+            const int vb = (ls.dmask >> jc) & 1 ? 4 * ls.gl + jc : vbf;
             // both candidates are formed and one is selected (no branch: the
             // bases stay in registers)
             const char* wq = reinterpret_cast<const char*>(P.W) + vb * qs;
@@ -274,7 +317,7 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
     // so the loads that fill the pipeline's tail repeat a valid address.
     auto advance = [&]() __attribute__((always_inline)) {
         while (lrem == 0) {
-            dec_next(a, n_act_v, se, ls);
+            dec_next(a, n_act_v, gr, se, ls);
             if (!ls.valid) return;
             const int n = dec_items<NKQ>(ls, kq, &lkw);
             if (n > 0) {
@@ -344,7 +387,7 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
             }
         }
         dec_flush<MB, NB>(a, cs, acc, red, b);
-        dec_next(a, n_act_v, se, cs);
+        dec_next(a, n_act_v, gr, se, cs);
         if (!cs.valid) break;
     }
 }
@@ -499,7 +542,9 @@ __device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, i
                 expand8(acc, z, q[h], sc);
             }
         }
-        // ranks 16 and up, 8 at a time
+        // ranks 16 and up, 8 at a time (two octets per turn, so that the
+        // loads of both are in flight together)
+#pragma unroll 2
         for (int j0 = 16; j0 < r8s; j0 += 8) {
             u32x4 qr[8];
 #pragma unroll

@@ -118,6 +118,7 @@ struct PrepArgs {
     int* rowslot;             // optional [T], with rowtok: (rank8 << 16) | slot of each row's adapter, -1 for none
     int oct_perm;             // 1: octet lists for the 64-row blocks of rowtok order (large-tile GEMM)
     int* gslot;
+    int* gr8;                 // decode plan (optional): padded rank of each adapter in use
     int* gstart;
     int* gcount;
     int4* items;
@@ -174,6 +175,8 @@ struct DecArgs {
     const int* tr8;           // [T] padded rank of each token's adapter (0: none)
     const int* tgrp;          // [T] group (adapter in use) index of each token, -1: none
     const int* gslot;         // [groups] slot of each adapter in use
+    const int* gr8;           // [groups] its rank padded to 8 (its A^T blocks: n_slices gr8 / 16,
+                              // rounded up; positions past them hold no data)
     const int* meta;          // [0] number of adapters in use (n_act)
     int act_max;              // adapter positions in the column lists: the host's bound on n_act
     float* part;              // partial tiles: slot g + b for group g and workgroup b

@@ -101,7 +101,10 @@ __device__ void decode_plan(const PrepArgs& a, int* ids_lds) {
         const unsigned long long used =
             (unsigned long long)wave_or((unsigned)bit) | ((unsigned long long)wave_or((unsigned)(bit >> 32)) << 32);
         const unsigned long long below = (1ull << l) - 1ull;
-        if ((used >> l) & 1ull) a.gslot[__popcll(used & below)] = l;
+        if ((used >> l) & 1ull) {
+            a.gslot[__popcll(used & below)] = l;
+            if (a.gr8) a.gr8[__popcll(used & below)] = rt;   // lane l holds slot l's rank
+        }
         if (ok) mine = __popcll(used & (bit - 1ull));
         g = __popcll(used);
     } else {
@@ -110,7 +113,12 @@ __device__ void decode_plan(const PrepArgs& a, int* ids_lds) {
             const int m = wave_min(((rem >> l) & 1ull) ? v : 0x7fffffff);
             const bool eq = ok && v == m;
             if (eq) mine = g;
-            if (l == 0) a.gslot[g] = m;
+            // slot m's rank: held by every lane whose token uses it
+            const int rm = __builtin_amdgcn_readlane(r8v, __ffsll((long long)__ballot(eq)) - 1);
+            if (l == 0) {
+                a.gslot[g] = m;
+                if (a.gr8) a.gr8[g] = rm;
+            }
             ++g;
             rem &= ~__ballot(eq);
         }

@@ -370,3 +370,53 @@ def test_workload_parity(torch_cuda, index):
         _check(ys[p], refs[p], yb[p], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
     assert pool.device_error() == 0
     pool.close()
+
+
+@pytest.mark.parametrize("index", [5, 6])
+def test_decode_variants_parity(torch_cuda, index):
+    # the 8B decode layer with an INT4 base (5) and with ranks alternating 8
+    # and 64 in slots sized for 64 (6: a rank-8 adapter streams its own A^T
+    # blocks only), every slot loaded as in the benchmark, every row compared
+    torch = torch_cuda
+    from oracle import quant
+    spec = wl.workload(index)
+    slots = list(range(spec.n_slots))
+    layer = wl.draw_layer(spec, slots=slots)
+    pool = make_pool(spec)
+    load_adapters(pool, spec, slots, cache=layer.adapters)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    assert pool.last_path() == "decode"
+    yb = _base_only(torch, spec, dl, pool)
+    if spec.weight_format == "int4_g128":
+        refs = quant.layer_forward_w4(layer)
+        rbase = [pi.X.astype(np.float64) @ quant.dequantize(pi.Wq, pi.Ws_bits, pi.spec.d_in) for pi in layer.projs]
+    else:
+        refs = bdlora.layer_forward(layer)
+        rbase = _oracle_base(layer)
+    for p in range(len(spec.projs)):
+        _check(ys[p], refs[p], yb[p], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
+    assert pool.device_error() == 0
+    pool.close()
+
+
+def test_mixed_rank_decode_small_shapes(torch_cuda):
+    # own-rank blocks on shapes where weight and adapter blocks share groups
+    # (N / 16 not a multiple of 4) and adapters of ranks 1..64 sit in slots
+    # sized for 64; several batches on one pool, some ids unused or -1
+    torch = torch_cuda
+    ranks = [64, 1, 8, 0, 24, 64, 3, 16, 40, 8]
+    for T, seed in ((64, 1), (17, 2), (40, 3)):
+        rng = np.random.default_rng(seed)
+        ids = rng.integers(-1, len(ranks), size=T)
+        spec = wl.custom_workload(f"mixed-{T}", wl.tiny_projs(), T, ranks, ids=ids, seed=seed)
+        layer = wl.draw_layer(spec, slots=range(len(ranks)))
+        pool = make_pool(spec)
+        load_adapters(pool, spec, range(len(ranks)), cache=layer.adapters)
+        dl, ys = _run_layer(torch, spec, layer, pool)
+        yb = _base_only(torch, spec, dl, pool)
+        refs = bdlora.layer_forward(layer)
+        rb = _oracle_base(layer)
+        for p in range(len(spec.projs)):
+            _check(ys[p], refs[p], yb[p], rb[p], what=f"mixed T={T} {spec.projs[p].name}")
+        assert pool.device_error() == 0
+        pool.close()

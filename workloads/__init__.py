@@ -230,6 +230,13 @@ def workload(index: int) -> WorkloadSpec:
             w.ids_kind, w.seed, weight_format="int4_g128",
             description="workload 1 (Llama-3.1-8B layer shard, 64 decode tokens, 32 adapters "
                         "r_s=16, Zipf ids) with an INT4 base (one bf16 scale per 128 inputs)")
+    if index == 6:
+        w = workload(1)
+        return WorkloadSpec(
+            "8b-layer-decode-T64-r8r64", w.model, w.tp, w.projs, w.T, w.n_slots,
+            [8 if s % 2 == 0 else 64 for s in range(w.n_slots)], w.scales, w.ids_kind, 6,
+            description="Llama-3.1-8B layer shard, 64 decode tokens, 32 adapters whose ranks "
+                        "alternate 8 and 64 (slots sized for rank 64), Zipf ids")
     raise KeyError(index)
 
 
