@@ -1087,6 +1087,11 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         bdl::ProjLaunch& pl = fa.p[q];
         pl.X = (const uint16_t*)X[i];
         pl.Xp = P->d_Xp[projs[i]];
+        // the large tiles and their shrink gather rows of the caller's X
+        // directly (32-bit offsets: T K 2 < 2^31 is part of the path's
+        // condition); an intermediate already packed (pack false) is read
+        // from Xp
+        pl.x_rowmajor = big && pack ? 1 : 0;
         pl.W = (const uint16_t*)W[i];
         pl.Ws = int4_scales(pi, W[i]);
         pl.out = (uint16_t*)out[i];
@@ -1193,6 +1198,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     }
     int frags = 0, jobs = 0;
     for (int q = 0; q < n && pack; ++q) {
+        if (fa.p[q].x_rowmajor) continue;
         bdl::PackJob& J = pa.jobs[jobs++];
         J.src = fa.p[q].X;
         J.dst = P->d_Xp[projs[order[q]]];

@@ -523,9 +523,17 @@ __device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, i
 #pragma unroll
     for (int j = 0; j < kEpiSeg; ++j)
         if (b0 + j <= b1) add8(acc, y[j][0], y[j][1]);
-    for (int b = b0 + kEpiSeg; b <= b1; ++b) {
-        const float* src = ysrc + (size_t)(b - b0) * kPartElems;
-        add8(acc, ldf4(src), ldf4(src + 4));
+    for (int j0 = kEpiSeg; j0 <= b1 - b0; j0 += kEpiSeg) {
+        float4 yy[kEpiSeg][2];
+#pragma unroll
+        for (int j = 0; j < kEpiSeg; ++j) {
+            const size_t o = (size_t)min(j0 + j, b1 - b0) * kPartElems;
+            yy[j][0] = ldf4(ysrc + o);
+            yy[j][1] = ldf4(ysrc + o + 4);
+        }
+#pragma unroll
+        for (int j = 0; j < kEpiSeg; ++j)
+            if (j0 + j <= b1 - b0) add8(acc, yy[j][0], yy[j][1]);
     }
     if (lora) {
 #pragma unroll
@@ -535,9 +543,17 @@ __device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, i
 #pragma unroll
                 for (int j = 0; j < kEpiZSeg; ++j)
                     if (z0[h] + j <= z1[h]) add8(z, zp[h][j][0], zp[h][j][1]);
-                for (int b = z0[h] + kEpiZSeg; b <= z1[h]; ++b) {
-                    const float* src = zsrc[h] + (size_t)(b - z0[h]) * kPartElems;
-                    add8(z, ldf4(src), ldf4(src + 4));
+                for (int j0 = kEpiZSeg; j0 <= z1[h] - z0[h]; j0 += kEpiZSeg) {
+                    float4 zz[kEpiZSeg][2];
+#pragma unroll
+                    for (int j = 0; j < kEpiZSeg; ++j) {
+                        const size_t o = (size_t)min(j0 + j, z1[h] - z0[h]) * kPartElems;
+                        zz[j][0] = ldf4(zsrc[h] + o);
+                        zz[j][1] = ldf4(zsrc[h] + o + 4);
+                    }
+#pragma unroll
+                    for (int j = 0; j < kEpiZSeg; ++j)
+                        if (j0 + j <= z1[h] - z0[h]) add8(z, zz[j][0], zz[j][1]);
                 }
                 expand8(acc, z, q[h], sc);
             }
@@ -555,9 +571,17 @@ __device__ __forceinline__ void epi_acc(const DecArgs& a, int p, int n, int t, i
             group_wgs(pp, vb >> 2, U, G, &c0, &c1);
             const float* src = a.part + (size_t)(pp.gb + (vb >> 2)) * kPartElems + t * 64 + (vb & 3) * 16 + (vc & 15);
             float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            for (int b = c0; b <= c1; ++b) {
-                const float* s2 = src + (size_t)b * kPartElems;
-                add8(z, ldf4(s2), ldf4(s2 + 4));
+            for (int j0 = 0; j0 <= c1 - c0; j0 += kEpiZSeg) {
+                float4 zz[kEpiZSeg][2];
+#pragma unroll
+                for (int j = 0; j < kEpiZSeg; ++j) {
+                    const float* s2 = src + (size_t)(c0 + min(j0 + j, c1 - c0)) * kPartElems;
+                    zz[j][0] = ldf4(s2);
+                    zz[j][1] = ldf4(s2 + 4);
+                }
+#pragma unroll
+                for (int j = 0; j < kEpiZSeg; ++j)
+                    if (j0 + j <= c1 - c0) add8(z, zz[j][0], zz[j][1]);
             }
             expand8(acc, z, qr, sc);
         }

@@ -5,12 +5,16 @@
 // Large-tile GEMM.
 // One workgroup computes a 256 x 256 output tile (tokens x columns) of one
 // projection: out = X W_s + Zhat B, the base product, the adapter expand and
-// their sum of Alg. 1 / Alg. 2 in one pass over the tile.  The operands are
-// the packed fragment layouts (1 KB per 16 rows x 32 k), so a k-step of the
-// tile is 16 activation and 16 weight fragments.  They go from global memory
-// straight into LDS (buffer_load_dwordx4 ... lds: lane l of a wave writes the
-// 16 bytes at offset 16 l of the wave's 1 KB destination, which is exactly a
-// fragment), kBigStages k-steps deep, with one barrier per k-step.  Eight
+// their sum of Alg. 1 / Alg. 2 in one pass over the tile.  A k-step of the
+// tile is 16 activation and 16 weight fragments (1 KB per 16 rows x 32 k).
+// They go from global memory straight into LDS (buffer_load_dwordx4 ... lds:
+// lane l of a wave writes the 16 bytes at offset 16 l of the wave's 1 KB
+// destination, which is exactly a fragment), kBigStages k-steps deep, with
+// one barrier per k-step.  The weight is read in its packed fragment layout;
+// the activations straight from the caller's row-major X (each lane's global
+// offset picks the 16 bytes of its token's row that its fragment slot holds,
+// so no pass packs X first), or from a packed copy when X is an intermediate
+// already written in fragments.  Eight
 // waves, 4 row quarters x 2 column halves, each own a 64 x 128 sub-tile for
 // the whole K (no cross-wave reduction): per k-step a wave reads 4 + 8
 // fragments from LDS (half a k-step ahead of the MFMAs that use them) and
@@ -48,12 +52,15 @@ typedef __attribute__((address_space(3))) void lds_void;
 // Where this thread's copies of a k-step come from: copies i < CP / 2 are
 // activation fragments, the others weight fragments (fragment w + NW i of
 // the k-step's 32), each a buffer load of 16 bytes per lane at byte offset
-// vo[i] + 1024 ks.  Buffer loads (not global ones) so that the compiler's
-// wait-count bookkeeping treats them as plain vector-memory operations and
-// keeps its LDS wait counts exact.
+// vo[i] + 1024 ks (weights, packed X) or vo[i] + 64 ks (X row-major: the
+// lane's 8 inputs of its row).  Buffer loads (not global ones) so that the
+// compiler's wait-count bookkeeping treats them as plain vector-memory
+// operations and keeps its LDS wait counts exact; their bounds are the
+// operands' sizes, so no lane can read past X or W.
 template <int CP>
 struct BigSrc {
     __amdgpu_buffer_rsrc_t rx, rw, rw2;
+    int xstep;    // bytes between k-steps of an activation copy
     int vo[CP];   // this lane's byte offset at k-step 0
     bool two[CP]; // paired gate/up tiles: the copy reads the second weight (rw2)
 };
@@ -64,8 +71,8 @@ __device__ __forceinline__ void big_issue(const BigSrc<CP>& s, int ks, u32x4* st
 #pragma unroll
     for (int i = 0; i < CP; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(i < CP / 2 ? s.rx : (s.two[i] ? s.rw2 : s.rw),
-                                                 (lds_void*)(stage + (w + NW * i) * 64), 16, s.vo[i] + ks * 1024, 0,
-                                                 0, 0);
+                                                 (lds_void*)(stage + (w + NW * i) * 64), 16,
+                                                 s.vo[i] + ks * (i < CP / 2 ? s.xstep : 1024), 0, 0, 0);
 }
 
 // wait until at most n of this thread's copies (and none of its LDS reads)
@@ -179,7 +186,10 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     // blocks, 16..31 its weight column blocks (blocks past the edge are
     // clamped, their results are never stored)
     BigSrc<CP> src;
-    src.rx = __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
+    const bool xrm = P.x_rowmajor != 0;
+    src.rx = xrm ? __builtin_amdgcn_make_buffer_rsrc((void*)P.X, 0, T * P.K * 2, kRawBufferWord3)
+                 : __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
+    src.xstep = xrm ? 64 : 1024;
     src.rw = __builtin_amdgcn_make_buffer_rsrc((void*)P.W, 0, ncb * KS * 1024, kRawBufferWord3);
     src.rw2 = pair ? __builtin_amdgcn_make_buffer_rsrc((void*)a.p[p + 1].W, 0, ncb * KS * 1024, kRawBufferWord3)
                    : src.rw;
@@ -190,6 +200,13 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         if (i >= CP / 2 && pair) {
             // weight fragment f - 16: column block (f - 16) mod 8 of gate (< 8) or up
             src.vo[i] = min(nt * 8 + ((f - 16) & 7), ncb - 1) * KS * 1024 + k0 * 1024 + l * 16;
+        } else if (i < CP / 2 && xrm) {
+            // X row-major: the lane's row (its token, rows past T repeat a
+            // valid one) from input 32 k0 + 8 (l / 16), the 16 bytes the
+            // fragment holds at lane slot l
+            const int row = min((mt * 16 + f) * 16 + lr, T - 1);
+            const int t = a.rowtok ? (int)min((unsigned)a.rowtok[row], (unsigned)(T - 1)) : row;
+            src.vo[i] = t * (P.K * 2) + k0 * 64 + lg * 16;
         } else if (i < CP / 2 && a.rowtok) {
             // the lane's row is gathered: its token's fragment, lane slot
             // (token mod 16) + 16 (l / 16); rows past T repeat a valid token

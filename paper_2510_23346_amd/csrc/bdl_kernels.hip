@@ -78,12 +78,16 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
         const int nblk = (ncols + 15) >> 4;
         const uint16_t* abase = a.pool + (size_t)slot * a.slot_stride + P.a_off;
 
+        // the lane's row (token t) at k-step 0: in X row-major (k-steps 32
+        // elements apart) or in the packed X (k-steps a fragment apart)
+        const bool xrm = P.x_rowmajor != 0;
         const uint16_t* ap[MB];
         const uint16_t* bp[NB];
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb) {
             const int t = prow[min(rb * 16 + lr, nrows - 1)];
-            ap[rb] = P.Xp + frag_index(t >> 4, 0, KS) + ((t & 15) + 16 * (l >> 4)) * 8;
+            ap[rb] = xrm ? P.X + (size_t)t * P.K + 8 * (l >> 4)
+                         : P.Xp + frag_index(t >> 4, 0, KS) + ((t & 15) + 16 * (l >> 4)) * 8;
         }
 #pragma unroll
         for (int cb = 0; cb < NB; ++cb) bp[cb] = abase + frag_index(min((c0 >> 4) + cb, nblk - 1), 0, KS) + l * 8;
@@ -96,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
         const int ks0 = kp * KS / KP;
         int k0, nk;
         wave_krange((kp + 1) * KS / KP - ks0, w, &k0, &nk);
-        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, ks0 + k0, nk, kFrag, kFrag);
+        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, ks0 + k0, nk, xrm ? 32 : kFrag, kFrag);
         reduce_waves<MB, NB>(acc, red);
 
         if (KP > 1) {

@@ -13,6 +13,8 @@ constexpr int kMaxSlices = 4;
 constexpr int kMaxSlots = 8192;
 constexpr int kMaxRank8 = 128;       // largest supported rank, rounded up to 8
 constexpr int kPlanLdsTokens = 8192; // plan keeps validated ids in LDS up to this batch size
+constexpr int kPlanWaveGroups = 256;  // plan: placement by all waves for at most this many adapters
+constexpr int kPlanParMaxSlots = 4096; // ... in pools of at most this many slots (its LDS counts)
 constexpr int kMaxSeg = BDLORA_MAX_SEGMENTS;   // segments of a batch given in run-length form
 constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base GEMM (prefill)
 constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-tile GEMM's split tiles
@@ -25,6 +27,8 @@ constexpr long long kShrinkPartElems = 8LL << 20;   // fp32 partials of the spli
 struct ProjLaunch {
     const uint16_t* X;        // [T x K] bf16 activations (row-major)
     const uint16_t* Xp;       // packed activations, fragment layout, rows padded to 16
+    int x_rowmajor;           // large-tile path: the shrink and the GEMM read X (row-major, rows
+                              // gathered by token) and Xp is not written; else they read Xp
     const uint16_t* W;        // packed base weight, fragment layout ([N x K] nn.Linear rows)
     const uint16_t* Ws;       // INT4 base: its scales (null for a bf16 base)
     uint16_t* out;            // [T x N] bf16

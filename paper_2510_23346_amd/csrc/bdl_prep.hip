@@ -179,6 +179,112 @@ __device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
     }
 }
 
+// Stable placement by all 16 waves (batches of at most kPlanWaveGroups
+// adapters in pools of at most kPlanParMaxSlots slots, ids in LDS): wave w
+// takes the tokens [w C, (w + 1) C) and counts them per group into its LDS
+// row wh[w][g]; a prefix over the waves turns the counts into each wave's
+// first position per group (and for the tokens without an adapter); then
+// every wave places its tokens chunk by chunk in token order.  A 64-token
+// chunk of one adapter (prefill requests) is placed by one ballot; in a
+// chunk of several, each lane counts the lanes before it in its group from
+// the chunk's group ids staged in LDS (cgw), reads its group's position from
+// the wave's row, and the group's last lane moves it on.  The positions
+// equal those of the serial placement (stable in token order).
+__device__ void place_waves(const PrepArgs& a, const int* vid_l, const int* ldl, const int* r8l, int* wh,
+                            int* cg_l, const int* gstart_l, int* wnone, int n_groups, int n_ad) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const unsigned long long lt = (1ull << lane) - 1ull;
+    const int C = (a.T + 16 * 64 - 1) / (16 * 64) * 64;
+    const int t0 = min(wv * C, a.T), t1 = min(t0 + C, a.T);
+    int* row = wh + wv * kPlanWaveGroups;
+    int* cgw = cg_l + wv * 64;
+    for (int g = lane; g < n_groups; g += 64) row[g] = 0;
+    int nn = 0;
+    for (int base = t0; base < t1; base += 64) {
+        const int t = base + lane;
+        const int v = t < t1 ? vid_l[t] : -2;
+        const int g = v >= 0 ? ldl[v] : -1;
+        const unsigned long long act = __ballot(v >= 0);
+        if (act) {
+            const int gl = __builtin_amdgcn_readlane(g, __ffsll((long long)act) - 1);
+            const unsigned long long m = __ballot(v >= 0 && g == gl);
+            if (m == act) {
+                if (lane == 0) row[gl] += __popcll(m);
+            } else if (v >= 0) {
+                atomicAdd(&row[g], 1);
+            }
+        }
+        nn += __popcll(__ballot(v == -1));
+    }
+    if (lane == 0) wnone[wv] = nn;
+    __syncthreads();
+    for (int g = tid; g < n_groups; g += 1024) {
+        int r = gstart_l[g];
+        for (int w = 0; w < 16; ++w) {
+            const int c = wh[w * kPlanWaveGroups + g];
+            wh[w * kPlanWaveGroups + g] = r;
+            r += c;
+        }
+    }
+    if (tid == 0) {
+        int r = n_ad;
+        for (int w = 0; w < 16; ++w) {
+            const int c = wnone[w];
+            wnone[w] = r;
+            r += c;
+        }
+    }
+    __syncthreads();
+    int noff = wnone[wv];
+    for (int base = t0; base < t1; base += 64) {
+        const int t = base + lane;
+        const int v = t < t1 ? vid_l[t] : -2;
+        const int g = v >= 0 ? ldl[v] : -1;
+        const unsigned long long act = __ballot(v >= 0);
+        if (act) {
+            const int gl = __builtin_amdgcn_readlane(g, __ffsll((long long)act) - 1);
+            const unsigned long long m = __ballot(v >= 0 && g == gl);
+            if (m == act) {
+                // one group: its position from the row (one uniform read)
+                const int b0 = row[gl];
+                if (v >= 0) {
+                    const int pos = b0 + __popcll(m & lt);
+                    a.perm[pos] = t;
+                    if (a.rowtok) a.rowtok[pos] = t;
+                    if (a.rowslot) a.rowslot[pos] = (r8l[v] << 16) | v;
+                }
+                if (lane == 0) row[gl] = b0 + __popcll(m);
+            } else {
+                cgw[lane] = g;                        // (in order with the reads below)
+                int before = 0;
+                bool later = false;
+#pragma unroll 4
+                for (int j = 0; j < 64; j += 4) {
+                    const int4 q = *reinterpret_cast<const int4*>(cgw + j);
+                    before += (j < lane && q.x == g) + (j + 1 < lane && q.y == g) + (j + 2 < lane && q.z == g) +
+                              (j + 3 < lane && q.w == g);
+                    later = later || (j > lane && q.x == g) || (j + 1 > lane && q.y == g) ||
+                            (j + 2 > lane && q.z == g) || (j + 3 > lane && q.w == g);
+                }
+                if (v >= 0) {
+                    const int pos = row[g] + before;
+                    a.perm[pos] = t;
+                    if (a.rowtok) a.rowtok[pos] = t;
+                    if (a.rowslot) a.rowslot[pos] = (r8l[v] << 16) | v;
+                    if (!later) row[g] = pos + 1;     // the group's last lane in the chunk
+                }
+            }
+        }
+        const unsigned long long um = __ballot(v == -1);
+        if (v == -1 && a.rowtok) {
+            const int pos = noff + __popcll(um & lt);
+            a.rowtok[pos] = t;
+            if (a.rowslot) a.rowslot[pos] = -1;
+        }
+        noff += __popcll(um);
+    }
+}
+
 __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     if (blockIdx.x > 0) {
         if (a.total_frags >= kPackWideFrags)
@@ -202,6 +308,11 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     __shared__ int seg_s[kMaxSeg], seg_v[kMaxSeg];
     __shared__ int wsum[16][3];
     __shared__ int wpre[16][3];
+    __shared__ int gstart_l[kPlanWaveGroups];   // group tables (the first kPlanWaveGroups groups):
+    __shared__ int gcount_l[kPlanWaveGroups];   // start, count and slot, read by the
+    __shared__ int gslot_l[kPlanWaveGroups];    // placement and the octet lists
+    __shared__ int wnone[16];
+    __shared__ __align__(16) int cg_l[16 * 64];   // place_waves: a chunk's group ids, per wave
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const bool in_lds = a.T <= kPlanLdsTokens;
 
@@ -241,15 +352,27 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int t = t0 + j * 1024 + tid;
-            if (t >= a.T) break;
             const int id = idv[j];
-            const bool ok = id >= 0 && id < a.max_slots && ldl[id] != 0;
-            if (!ok && id != -1) s_err = 1;
-            const int v = ok ? id : -1;
-            a.vid[t] = v;
-            a.tr8[t] = ok ? r8l[id] : 0;
-            if (in_lds) vid_l[t] = v;
-            if (ok) atomicAdd(&cnt[id], 1);
+            const bool ok = t < a.T && id >= 0 && id < a.max_slots && ldl[id] != 0;
+            if (t < a.T) {
+                if (!ok && id != -1) s_err = 1;
+                const int v = ok ? id : -1;
+                a.vid[t] = v;
+                a.tr8[t] = ok ? r8l[id] : 0;
+                if (in_lds) vid_l[t] = v;
+            }
+            // a wave whose tokens share one adapter (a prefill request) adds
+            // its count once; others add per token
+            const unsigned long long act = __ballot(ok);
+            if (act) {
+                const int il = __builtin_amdgcn_readlane(id, __ffsll((long long)act) - 1);
+                const unsigned long long m = __ballot(ok && id == il);
+                if (m == act) {
+                    if (lane == 0) atomicAdd(&cnt[il], __popcll(m));
+                } else if (ok) {
+                    atomicAdd(&cnt[id], 1);
+                }
+            }
         }
     }
     __syncthreads();
@@ -286,6 +409,11 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
         const int c = cnt[s];
         if (c > 0) {
             ldl[s] = g_off;                   // group index of the slot (validation is done)
+            if (g_off < kPlanWaveGroups) {
+                gstart_l[g_off] = tok_off;
+                gcount_l[g_off] = c;
+                gslot_l[g_off] = s;
+            }
             a.gslot[g_off] = s;
             a.gstart[g_off] = tok_off;
             a.gcount[g_off] = c;
@@ -311,7 +439,11 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     // rowtok, the same order followed by the tokens without an adapter
     // (rowtok[n_ad + #{t' < t : no adapter}] = t), a permutation of all rows
     const int n_ad = wpre[15][0] + wsum[15][0];   // tokens with an adapter
-    if (a.T <= 1024) {
+    const int n_groups_all = wpre[15][1] + wsum[15][1];
+    if (in_lds && n_groups_all <= kPlanWaveGroups && a.max_slots <= kPlanParMaxSlots) {
+        place_waves(a, vid_l, ldl, r8l, tabs + 3 * a.max_slots + 15 * nwords, cg_l, gstart_l, wnone, n_groups_all,
+                    n_ad);
+    } else if (a.T <= 1024) {
         const int t = tid;
         const int v = t < a.T ? vid_l[t] : -1;
         if (v >= 0) {
@@ -371,11 +503,14 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
                 // read from the group tables (no need to wait for the
                 // placement)
                 const int r0 = m * mt, r1 = min(r0 + mt, n_ad);
+                const bool gl = n_groups <= kPlanWaveGroups;   // tables in LDS
                 int base = 0;
                 for (int g0 = 0; g0 < n_groups; g0 += 64) {
                     const int g = g0 + lane;
-                    const bool in = g < n_groups && a.gstart[g] < r1 && a.gstart[g] + a.gcount[g] > r0;
-                    const int slot = in ? a.gslot[g] : 0;
+                    const int gs = g < n_groups ? (gl ? gstart_l[g] : a.gstart[g]) : 0;
+                    const int gc = g < n_groups ? (gl ? gcount_l[g] : a.gcount[g]) : 0;
+                    const bool in = g < n_groups && gs < r1 && gs + gc > r0;
+                    const int slot = in ? (gl ? gslot_l[g] : a.gslot[g]) : 0;
                     const int r8s = in ? r8l[slot] : 0;
                     const int c = r8s >> 3;
                     const int inc = wave_incl_scan(c);
@@ -418,7 +553,8 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
     int pack_blocks = (a.total_frags + 16 * per - 1) / (16 * per);
     if (pack_blocks > 4096) pack_blocks = 4096;
     const int nwords = (a.max_slots + 31) >> 5;
-    const size_t lds = a.decode_plan ? 0 : 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
+    size_t lds = a.decode_plan ? 0 : 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
+    if (!a.decode_plan && a.max_slots <= kPlanParMaxSlots) lds += 16 * kPlanWaveGroups * sizeof(int);   // place_waves
     hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), lds, s, a);
     return hipGetLastError();
 }

@@ -140,12 +140,23 @@ def test_deterministic_and_shard_equals_layer(torch_cuda):
 # plan: bit-exact against the host plan and the oracle; error flag
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("T,n_slots", [(1, 4), (64, 32), (333, 20), (4288, 512)])
-def test_plan_device_bit_exact(torch_cuda, T, n_slots):
+# kinds: "uniform" ids over the pool; "runs": requests of 100 tokens sharing
+# an adapter, then 150 scattered decode tokens (prefill + decode batches).
+# The cases cover the plan's placement by all waves (at most 256 adapters in
+# pools of at most 4096 slots; chunks of one and of many adapters) and its
+# single-wave fallback (more adapters, or a larger pool).
+@pytest.mark.parametrize("T,n_slots,kind", [(1, 4, "uniform"), (64, 32, "uniform"), (333, 20, "uniform"),
+                                            (4288, 512, "uniform"), (4288, 128, "uniform"), (4288, 512, "runs"),
+                                            (1500, 4200, "runs"), (8192, 300, "runs")])
+def test_plan_device_bit_exact(torch_cuda, T, n_slots, kind):
     torch = torch_cuda
     import paper_2510_23346_amd as bd
     rng = np.random.default_rng(T + n_slots)
-    ids = rng.integers(-1, n_slots, size=T).astype(np.int32)
+    if kind == "uniform":
+        ids = rng.integers(-1, n_slots, size=T).astype(np.int32)
+    else:
+        ids = np.concatenate([np.repeat(rng.integers(-1, n_slots, size=T // 100 + 1), 100)[:T - 150],
+                              rng.integers(-1, n_slots, size=150)]).astype(np.int32)
     ids[::17] = n_slots + 3                  # out of range
     ids[1::29] = -7                          # negative, not -1
     unloaded = {1, n_slots - 1}
