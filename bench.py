@@ -600,6 +600,8 @@ def main():
                     help=f"headline workload index 0..6 (default {HEADLINE}; 5 = workload 1 with an INT4 base, "
                          "6 = workload 1 with ranks 8 and 64)")
     ap.add_argument("--only", action="store_true", help="time the headline workload only")
+    ap.add_argument("--mlp", action="store_true",
+                    help="time only the MLP shard (gate, up, H, down) of --workload 1 or 2 and print its line")
     ap.add_argument("--rotate", type=int, default=0, help="input copies to rotate (0 = auto)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -633,6 +635,12 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    if args.mlp:
+        if args.workload not in (1, 2):
+            print("bench.py: --mlp takes --workload 1 (decode) or 2 (prefill)", file=sys.stderr)
+            sys.exit(2)
+        print(json.dumps(measure_mlp(args.workload, args.steps, args.warmup, args.eager)), flush=True)
+        return
     head, spec, layer = measure(args.workload, args.steps, args.warmup, args.rotate, args.eager)
     print(f"bench: {spec.name} {head['ms_per_step']} ms/step", file=sys.stderr, flush=True)
     cpu = None if args.no_cpu_baseline else cpu_baseline(spec, layer, args.cpu_seconds)
