@@ -51,7 +51,9 @@ constexpr int kStages = 3;                    // k-steps of loads kept in flight
 //    order and writes Z.
 // --------------------------------------------------------------------------
 
-template <int MB, int NB>
+// XRM: the launch's projections read the caller's row-major X (the
+// large-tile path); else the packed X
+template <int MB, int NB, bool XRM>
 __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
     constexpr int MT = MB * 16, NT = NB * 16, LD = NT + 4;
     __shared__ float red[4 * MT * LD];
@@ -80,13 +82,12 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
 
         // the lane's row (token t) at k-step 0: in X row-major (k-steps 32
         // elements apart) or in the packed X (k-steps a fragment apart)
-        const bool xrm = P.x_rowmajor != 0;
         const uint16_t* ap[MB];
         const uint16_t* bp[NB];
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb) {
             const int t = prow[min(rb * 16 + lr, nrows - 1)];
-            ap[rb] = xrm ? P.X + (size_t)t * P.K + 8 * (l >> 4)
+            ap[rb] = XRM ? P.X + (size_t)t * P.K + 8 * (l >> 4)
                          : P.Xp + frag_index(t >> 4, 0, KS) + ((t & 15) + 16 * (l >> 4)) * 8;
         }
 #pragma unroll
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
         const int ks0 = kp * KS / KP;
         int k0, nk;
         wave_krange((kp + 1) * KS / KP - ks0, w, &k0, &nk);
-        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, ks0 + k0, nk, xrm ? 32 : kFrag, kFrag);
+        if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, ks0 + k0, nk, XRM ? 32 : kFrag, kFrag);
         reduce_waves<MB, NB>(acc, red);
 
         if (KP > 1) {
@@ -175,9 +176,17 @@ hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
     const int grid = total < 4096 ? total : 4096;
     if (grid <= 0) return hipSuccess;
     const int rgrid = tiles < 2048 ? tiles : 2048;
+    // every projection of a launch reads X the same way (the large-tile path
+    // reads the caller's row-major X)
+    const bool xrm = a.p[0].x_rowmajor != 0;
+    for (int i = 1; i < a.n_proj; ++i)
+        if ((a.p[i].x_rowmajor != 0) != xrm) return hipErrorInvalidValue;
 #define BDL_SHRINK_CASE(M, NN)                                                                          \
     if (mb == M && nb == NN) {                                                                          \
-        hipLaunchKernelGGL((shrink_kernel<M, NN>), dim3(grid), dim3(kThreads), 0, s, a);               \
+        if (xrm)                                                                                        \
+            hipLaunchKernelGGL((shrink_kernel<M, NN, true>), dim3(grid), dim3(kThreads), 0, s, a);     \
+        else                                                                                            \
+            hipLaunchKernelGGL((shrink_kernel<M, NN, false>), dim3(grid), dim3(kThreads), 0, s, a);    \
         if (KP > 1) hipLaunchKernelGGL((shrink_reduce_kernel<M, NN>), dim3(rgrid), dim3(256), 0, s, a); \
         return hipGetLastError();                                                                       \
     }

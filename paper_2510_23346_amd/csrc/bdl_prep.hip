@@ -179,8 +179,9 @@ __device__ void pack_activations(const PrepArgs& a, int blk, int nblk) {
     }
 }
 
-// Stable placement by all 16 waves (batches of at most kPlanWaveGroups
-// adapters in pools of at most kPlanParMaxSlots slots, ids in LDS): wave w
+// Stable placement by all 16 waves (batches of more than 1024 tokens, at
+// most kPlanWaveGroups adapters, pools of at most kPlanParMaxSlots slots,
+// ids in LDS; smaller batches count each token's rank directly): wave w
 // takes the tokens [w C, (w + 1) C) and counts them per group into its LDS
 // row wh[w][g]; a prefix over the waves turns the counts into each wave's
 // first position per group (and for the tokens without an adapter); then
@@ -351,6 +352,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
+            if (t0 + j * 1024 + (tid & ~63) >= a.T) break;   // the wave's tokens are all past T
             const int t = t0 + j * 1024 + tid;
             const int id = idv[j];
             const bool ok = t < a.T && id >= 0 && id < a.max_slots && ldl[id] != 0;
@@ -440,7 +442,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     // (rowtok[n_ad + #{t' < t : no adapter}] = t), a permutation of all rows
     const int n_ad = wpre[15][0] + wsum[15][0];   // tokens with an adapter
     const int n_groups_all = wpre[15][1] + wsum[15][1];
-    if (in_lds && n_groups_all <= kPlanWaveGroups && a.max_slots <= kPlanParMaxSlots) {
+    if (a.T > 1024 && in_lds && n_groups_all <= kPlanWaveGroups && a.max_slots <= kPlanParMaxSlots) {
         place_waves(a, vid_l, ldl, r8l, tabs + 3 * a.max_slots + 15 * nwords, cg_l, gstart_l, wnone, n_groups_all,
                     n_ad);
     } else if (a.T <= 1024) {
@@ -554,7 +556,8 @@ hipError_t launch_prep(const PrepArgs& a, hipStream_t s) {
     if (pack_blocks > 4096) pack_blocks = 4096;
     const int nwords = (a.max_slots + 31) >> 5;
     size_t lds = a.decode_plan ? 0 : 3 * (size_t)a.max_slots * sizeof(int) + 15 * (size_t)nwords * sizeof(unsigned);
-    if (!a.decode_plan && a.max_slots <= kPlanParMaxSlots) lds += 16 * kPlanWaveGroups * sizeof(int);   // place_waves
+    // place_waves' per-wave counts, for the batches that take it
+    if (!a.decode_plan && a.T > 1024 && a.max_slots <= kPlanParMaxSlots) lds += 16 * kPlanWaveGroups * sizeof(int);
     hipLaunchKernelGGL(prep_kernel, dim3(1 + pack_blocks), dim3(1024), lds, s, a);
     return hipGetLastError();
 }

@@ -142,9 +142,10 @@ def test_deterministic_and_shard_equals_layer(torch_cuda):
 
 # kinds: "uniform" ids over the pool; "runs": requests of 100 tokens sharing
 # an adapter, then 150 scattered decode tokens (prefill + decode batches).
-# The cases cover the plan's placement by all waves (at most 256 adapters in
-# pools of at most 4096 slots; chunks of one and of many adapters) and its
-# single-wave fallback (more adapters, or a larger pool).
+# The cases cover the plan's placement by all waves (batches over 1024
+# tokens with at most 256 adapters in pools of at most 4096 slots; chunks of
+# one and of many adapters), its single-wave fallback (more adapters, or a
+# larger pool) and the per-token count of smaller batches.
 @pytest.mark.parametrize("T,n_slots,kind", [(1, 4, "uniform"), (64, 32, "uniform"), (333, 20, "uniform"),
                                             (4288, 512, "uniform"), (4288, 128, "uniform"), (4288, 512, "runs"),
                                             (1500, 4200, "runs"), (8192, 300, "runs")])
