@@ -1080,6 +1080,13 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         const long long q = std::max(1LL, (work + units - 1) / units);
         for (int i = 0; i < n; ++i) ksplit[i] = (int)std::max(1LL, (long long)(L.proj[projs[i]].K / 32) / q);
     }
+    // row-major X (the caller's, on the large-tile path): its copies take the
+    // two k-steps of a pair at once, so K must hold whole pairs and every
+    // k-range at least one pair
+    bool xrm = big && pack;
+    for (int i = 0; i < n; ++i) xrm = xrm && L.proj[projs[i]].K % 64 == 0;
+    if (xrm)
+        for (int i = 0; i < n; ++i) ksplit[i] = std::min(ksplit[i], std::max(1, L.proj[projs[i]].K / 64));
     int tile = 0, cch = 1, fix = 0, pslot = 0, mid_cols = 0;
     for (int q = 0; q < n; ++q) {
         const int i = order[q];
@@ -1091,7 +1098,7 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         // directly (32-bit offsets: T K 2 < 2^31 is part of the path's
         // condition); an intermediate already packed (pack false) is read
         // from Xp
-        pl.x_rowmajor = big && pack ? 1 : 0;
+        pl.x_rowmajor = xrm ? 1 : 0;
         pl.W = (const uint16_t*)W[i];
         pl.Ws = int4_scales(pi, W[i]);
         pl.out = (uint16_t*)out[i];

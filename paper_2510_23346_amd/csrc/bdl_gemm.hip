@@ -60,8 +60,8 @@ typedef __attribute__((address_space(3))) void lds_void;
 template <int CP>
 struct BigSrc {
     __amdgpu_buffer_rsrc_t rx, rw, rw2;
-    int xstep;    // bytes between k-steps of an activation copy
     int vo[CP];   // this lane's byte offset at k-step 0
+    int xo[CP];   // row-major X: this lane's offsets of its CP half-fragment copies of pair 0
     bool two[CP]; // paired gate/up tiles: the copy reads the second weight (rw2)
 };
 
@@ -71,9 +71,38 @@ __device__ __forceinline__ void big_issue(const BigSrc<CP>& s, int ks, u32x4* st
 #pragma unroll
     for (int i = 0; i < CP; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(i < CP / 2 ? s.rx : (s.two[i] ? s.rw2 : s.rw),
-                                                 (lds_void*)(stage + (w + NW * i) * 64), 16,
-                                                 s.vo[i] + ks * (i < CP / 2 ? s.xstep : 1024), 0, 0, 0);
+                                                 (lds_void*)(stage + (w + NW * i) * 64), 16, s.vo[i] + ks * 1024, 0,
+                                                 0, 0);
 }
+
+// Row-major X (the caller's activations): one copy takes 8 rows x 128 bytes
+// of the tile, the two k-steps of a pair (whole lines).  A pair's 32 copies
+// (16 row blocks x 2 row halves) land in one slot of an activation ring, half
+// fragment h = 2 block + half at 1 KB each; lane l takes row l / 8 of its 8
+// and 16-byte chunk (l mod 8) ^ big_swz(row of the block), so that the
+// readers hit distinct LDS banks (16 lanes on distinct 16-byte bank groups
+// mod 16, each 8 of them mod 8).  The weights keep one k-step per slot of
+// their own ring.
+__device__ __forceinline__ int big_swz(int r) { return ((r >> 1) ^ ((r & 1) << 2)) & 7; }
+
+// the weight copies (i >= CP / 2) of k-step ks into its weight slot (16 fragments)
+template <int CP, int NW>
+__device__ __forceinline__ void big_issue_w(const BigSrc<CP>& s, int ks, u32x4* slot, int w) {
+#pragma unroll
+    for (int i = CP / 2; i < CP; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(s.two[i] ? s.rw2 : s.rw, (lds_void*)(slot + (w + NW * i - 16) * 64),
+                                                 16, s.vo[i] + ks * 1024, 0, 0, 0);
+}
+
+// this thread's CP copies of activation pair q into its slot (32 half fragments)
+template <int CP, int NW>
+__device__ __forceinline__ void big_issue_x(const BigSrc<CP>& s, int q, u32x4* slot, int w) {
+#pragma unroll
+    for (int j = 0; j < CP; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(s.rx, (lds_void*)(slot + (w + NW * j) * 64), 16, s.xo[j] + q * 128, 0,
+                                                 0, 0);
+}
+
 
 // wait until at most n of this thread's copies (and none of its LDS reads)
 // are in flight, then barrier: afterwards the k-step whose copies are older
@@ -102,13 +131,33 @@ __device__ __forceinline__ void big_wait_ahead(int ahead) {
         big_wait_barrier<0>();
 }
 
+// wait until at most n (0, 2, 4 or 6) of this thread's copies are in flight, then barrier
+__device__ __forceinline__ void big_wait_n(int n) {
+    if (n >= 6)
+        big_wait_barrier<6>();
+    else if (n >= 4)
+        big_wait_barrier<4>();
+    else if (n >= 2)
+        big_wait_barrier<2>();
+    else
+        big_wait_barrier<0>();
+}
+
 // RB = 16-row blocks per wave: 4 (eight waves, 4 x 2) or 8 (four waves, 2 x 2).
-template <int RB>
+// XRM: the activations come from the caller's row-major X in pairs of
+// k-steps (see big_issue_x), in a ring of kBigXPairs pair slots beside the
+// weights' ring of kBigStages k-step slots (all of the CU's 160 KB of LDS);
+// a pair is copied 4 k-steps ahead of its first k-step, so it is in LDS
+// before the weights of that k-step are.
+constexpr int kBigXPairs = 3;
+template <int RB, bool XRM>
 __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     constexpr int NWR = 16 / RB, NW = 2 * NWR;   // row waves, waves
     constexpr int CP = kBigFrags / NW;           // fragment copies per thread and k-step
     constexpr int NH = RB / 4;                   // 64-row blocks per wave
-    __shared__ u32x4 lds[kBigStages * kBigFrags * 64];
+    constexpr int ST = kBigStages;               // k-step stages (weight slots)
+    static_assert(!XRM || (NW == 8 && CP == 4), "the row-major form's wait counts assume 8 waves");
+    __shared__ u32x4 lds[(XRM ? ST * 16 + kBigXPairs * 32 : ST * kBigFrags) * 64];
     const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15, lg = l >> 4;
     const int wr = w % NWR, wc = w / NWR;        // rows 16 RB wr .., columns 128 wc .. of the tile
 
@@ -179,17 +228,22 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
                 for (int cb = 0; cb < 8; ++cb) acc[rb][cb] += src[(rb * 8 + cb) * 64];
         }
     } else {
-    // this item's k-steps [k0, k0 + NK)
-    const int k0 = split * KS / S, NK = (split + 1) * KS / S - k0;
+    // this item's k-steps [k0, k0 + NK); row-major X: even bounds, so every
+    // pair of k-steps starts a 128-byte line (the host keeps KS even and
+    // each range at least 2 k-steps long)
+    int k0 = split * KS / S, k1 = (split + 1) * KS / S;
+    if (XRM) {
+        k0 &= ~1;
+        k1 = split + 1 == S ? KS : k1 & ~1;
+    }
+    const int NK = k1 - k0;
 
     // staging: fragments 0..15 of a k-step are the tile's activation row
     // blocks, 16..31 its weight column blocks (blocks past the edge are
     // clamped, their results are never stored)
     BigSrc<CP> src;
-    const bool xrm = P.x_rowmajor != 0;
-    src.rx = xrm ? __builtin_amdgcn_make_buffer_rsrc((void*)P.X, 0, T * P.K * 2, kRawBufferWord3)
+    src.rx = XRM ? __builtin_amdgcn_make_buffer_rsrc((void*)P.X, 0, T * P.K * 2, kRawBufferWord3)
                  : __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
-    src.xstep = xrm ? 64 : 1024;
     src.rw = __builtin_amdgcn_make_buffer_rsrc((void*)P.W, 0, ncb * KS * 1024, kRawBufferWord3);
     src.rw2 = pair ? __builtin_amdgcn_make_buffer_rsrc((void*)a.p[p + 1].W, 0, ncb * KS * 1024, kRawBufferWord3)
                    : src.rw;
@@ -197,16 +251,12 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     for (int i = 0; i < CP; ++i) {
         const int f = w + NW * i;
         src.two[i] = pair && i >= CP / 2 && f - 16 >= 8;
+        src.xo[i] = 0;
         if (i >= CP / 2 && pair) {
             // weight fragment f - 16: column block (f - 16) mod 8 of gate (< 8) or up
             src.vo[i] = min(nt * 8 + ((f - 16) & 7), ncb - 1) * KS * 1024 + k0 * 1024 + l * 16;
-        } else if (i < CP / 2 && xrm) {
-            // X row-major: the lane's row (its token, rows past T repeat a
-            // valid one) from input 32 k0 + 8 (l / 16), the 16 bytes the
-            // fragment holds at lane slot l
-            const int row = min((mt * 16 + f) * 16 + lr, T - 1);
-            const int t = a.rowtok ? (int)min((unsigned)a.rowtok[row], (unsigned)(T - 1)) : row;
-            src.vo[i] = t * (P.K * 2) + k0 * 64 + lg * 16;
+        } else if (i < CP / 2 && XRM) {
+            // (row-major X: src.xo below)
         } else if (i < CP / 2 && a.rowtok) {
             // the lane's row is gathered: its token's fragment, lane slot
             // (token mod 16) + 16 (l / 16); rows past T repeat a valid token
@@ -217,9 +267,34 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
                         k0 * 1024 + l * 16;
         }
     }
+    if constexpr (XRM) {
+        // half fragment h = w + NW j of a pair: row block h / 2, rows 8 (h mod 2)
+        // + l / 8 (its token; rows past T repeat a valid one), chunk
+        // (l mod 8) ^ big_swz(row in block) of the pair's 128 bytes from input 32 k0
 #pragma unroll
-    for (int d = 0; d < kBigStages - 1; ++d)
-        if (d < NK) big_issue<CP, NW>(src, d, lds + d * kBigFrags * 64, w);
+        for (int j = 0; j < CP; ++j) {
+            const int h = w + NW * j, rr = 8 * (h & 1) + (l >> 3);
+            const int row = min((mt * 16 + (h >> 1)) * 16 + rr, T - 1);
+            const int t = a.rowtok ? (int)min((unsigned)a.rowtok[row], (unsigned)(T - 1)) : row;
+            src.xo[j] = t * (P.K * 2) + k0 * 64 + ((l & 7) ^ big_swz(rr)) * 16;
+        }
+    }
+    u32x4* const wring = lds;                     // row-major X: weight slots, then pair slots
+    u32x4* const xring = lds + ST * 16 * 64;
+    const int NP = NK >> 1;                       // row-major X: pairs (NK is even)
+    if constexpr (XRM) {
+        // pairs 0 and 1, then the weights of k-steps 0 .. ST - 2
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+            if (q < NP) big_issue_x<CP, NW>(src, q, xring + q * 32 * 64, w);
+#pragma unroll
+        for (int d = 0; d < ST - 1; ++d)
+            if (d < NK) big_issue_w<CP, NW>(src, d, wring + d * 16 * 64, w);
+    } else {
+#pragma unroll
+        for (int d = 0; d < ST - 1; ++d)
+            if (d < NK) big_issue<CP, NW>(src, d, lds + d * kBigFrags * 64, w);
+    }
 
     // Software pipeline over half k-steps (column blocks 0..3, then 4..7 of
     // the wave).  While the MFMAs of the first half run, the second half's
@@ -228,19 +303,36 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
     // the next k-step.  The barrier between the halves makes the next k-step
     // visible; the copies issued right after it refill the stage of k-step
     // ks - 1, whose LDS reads every wave finished before the previous barrier.
-    static_assert(kBigStages >= 3 && kBigStages <= 5, "big_wait_ahead covers up to three k-steps in flight");
+    static_assert(ST >= 3 && ST <= 5, "big_wait_ahead covers up to three k-steps in flight");
     auto stage = [&](int step) __attribute__((always_inline)) {
-        return lds + (step % kBigStages) * kBigFrags * 64;
+        return lds + (step % ST) * kBigFrags * 64;
     };
+    // row-major X: lane (lr, lg) of k-step 2 p + h finds its 8 inputs (row
+    // lr, chunk 4 h + lg of the pair) in pair p's slot, half fragment
+    // 2 block + lr / 8, position 8 (lr mod 8) + ((4 h + lg) ^ big_swz(lr))
+    const int xpos0 = (lr >> 3) * 64 + (lr & 7) * 8 + (lg ^ big_swz(lr));
+    const int xpos1 = (lr >> 3) * 64 + (lr & 7) * 8 + ((4 + lg) ^ big_swz(lr));
     auto read_x = [&](u32x4 (&x)[RB], int step) __attribute__((always_inline)) {
-        const u32x4* S0 = stage(step);
+        if constexpr (XRM) {
+            const u32x4* S0 = xring + ((step >> 1) % kBigXPairs) * 32 * 64 + ((step & 1) ? xpos1 : xpos0);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) x[rb] = S0[(wr * RB + rb) * 64 + l];
+            for (int rb = 0; rb < RB; ++rb) x[rb] = S0[(wr * RB + rb) * 128];
+        } else {
+            const u32x4* S0 = stage(step);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) x[rb] = S0[(wr * RB + rb) * 64 + l];
+        }
     };
     auto read_w = [&](u32x4 (&wv)[4], int step, int half) __attribute__((always_inline)) {
-        const u32x4* S0 = stage(step);
+        if constexpr (XRM) {
+            const u32x4* S0 = wring + (step % ST) * 16 * 64;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) wv[c] = S0[(16 + wc * 8 + 4 * half + c) * 64 + l];
+            for (int c = 0; c < 4; ++c) wv[c] = S0[(wc * 8 + 4 * half + c) * 64 + l];
+        } else {
+            const u32x4* S0 = stage(step);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) wv[c] = S0[(16 + wc * 8 + 4 * half + c) * 64 + l];
+        }
     };
     auto mma = [&](const u32x4 (&x)[RB], const u32x4 (&wv)[4], int half) __attribute__((always_inline)) {
 #pragma unroll
@@ -264,11 +356,22 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         }
         __builtin_amdgcn_sched_group_barrier(0x008, 4 * RB - 4, 0);
         __builtin_amdgcn_sched_barrier(0);
-        // k-step ks + 1 is complete once at most the copies issued after it
-        // (k-steps ks + 2 .. ks + kBigStages - 2 below NK) are in flight
-        big_wait_ahead<CP>(min(kBigStages - 3, NK - 2 - ks));
-        const int nx = ks + kBigStages - 1;
-        if (nx < NK) big_issue<CP, NW>(src, nx, stage(nx), w);
+        const int nx = ks + ST - 1;
+        if constexpr (XRM) {
+            // k-step ks + 1's weights are complete once at most the copies
+            // issued after them are in flight: the weights of ks + 2 (if any)
+            // and, after an even k-step, the pair issued there; its pair was
+            // issued before its weights
+            big_wait_n((ks + 2 <= NK - 1 ? 2 : 0) + ((ks & 1) && ((ks - 1) >> 1) + 2 < NP ? 4 : 0));
+            if (!(ks & 1) && (ks >> 1) + 2 < NP)
+                big_issue_x<CP, NW>(src, (ks >> 1) + 2, xring + (((ks >> 1) + 2) % kBigXPairs) * 32 * 64, w);
+            if (nx < NK) big_issue_w<CP, NW>(src, nx, wring + (nx % ST) * 16 * 64, w);
+        } else {
+            // k-step ks + 1 is complete once at most the copies issued after it
+            // (k-steps ks + 2 .. ks + ST - 2 below NK) are in flight
+            big_wait_ahead<CP>(min(ST - 3, NK - 2 - ks));
+            if (nx < NK) big_issue<CP, NW>(src, nx, stage(nx), w);
+        }
         read_x(xn, ks + 1);
         read_w(w0, ks + 1, 0);
         mma(x, w1, 1);
@@ -280,8 +383,13 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         }
         __builtin_amdgcn_sched_barrier(0);
     };
-    // k-step 0 is complete once at most the copies of k-steps 1 .. kBigStages - 2 are in flight
-    big_wait_ahead<CP>(min(kBigStages - 2, NK - 1));
+    // k-step 0 is complete once at most the copies of k-steps 1 .. ST - 2 are
+    // in flight (row-major X: the weights of k-steps 1 .. ST - 2; the pairs
+    // were issued first)
+    if (XRM)
+        big_wait_n(2 * min(ST - 2, NK - 1));
+    else
+        big_wait_ahead<CP>(min(ST - 2, NK - 1));
     read_x(xa, 0);
     read_w(w0, 0, 0);
     int ks = 0;
@@ -427,11 +535,19 @@ constexpr int kBigRB = 4;
 
 hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s) {
     if (a.total_tiles <= 0) return hipSuccess;
-    hipLaunchKernelGGL(gemm_big_kernel<kBigRB>, dim3(a.total_tiles), dim3(128 * (16 / kBigRB)), 0, s, a);
+    // every projection of a launch reads X the same way; row-major X needs
+    // an even number of k-steps (pairs share a 128-byte line)
+    const bool xrm = a.p[0].x_rowmajor != 0;
+    for (int i = 0; i < a.n_proj; ++i)
+        if ((a.p[i].x_rowmajor != 0) != xrm || (xrm && (a.p[i].K & 63) != 0)) return hipErrorInvalidValue;
+    if (xrm)
+        hipLaunchKernelGGL((gemm_big_kernel<kBigRB, true>), dim3(a.total_tiles), dim3(128 * (16 / kBigRB)), 0, s, a);
+    else
+        hipLaunchKernelGGL((gemm_big_kernel<kBigRB, false>), dim3(a.total_tiles), dim3(128 * (16 / kBigRB)), 0, s, a);
     if (a.total_fix > 0) {
         FwdArgs f = a;
         f.fixup = 1;
-        hipLaunchKernelGGL(gemm_big_kernel<kBigRB>, dim3(a.total_fix), dim3(128 * (16 / kBigRB)), 0, s, f);
+        hipLaunchKernelGGL((gemm_big_kernel<kBigRB, false>), dim3(a.total_fix), dim3(128 * (16 / kBigRB)), 0, s, f);
     }
     return hipGetLastError();
 }
