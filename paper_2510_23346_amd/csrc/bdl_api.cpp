@@ -1159,6 +1159,11 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     // traffic.
     fa.shrink_kp = 1;
     fa.shrinkpart = P->d_shrinkpart;
+    // the unsplit shrink's unit order: longest K first (its units' length),
+    // so the short ones fill the end
+    fa.queue = P->d_meta + 2;
+    for (int q = 0; q < n; ++q) fa.sorder[q] = q;
+    std::stable_sort(fa.sorder, fa.sorder + n, [&](int x, int y) { return fa.p[x].K > fa.p[y].K; });
     if (T <= 512 && T <= 8 * n_loaded && P->d_shrinkpart &&
         (long long)n * fa.items_bound * cch * bdl::kShrinkKP * mts * nts <= L.shrinkpart_elems)
         fa.shrink_kp = bdl::kShrinkKP;

@@ -41,6 +41,12 @@ constexpr int kStages = 3;                    // k-steps of loads kept in flight
 // 2. shrink: Z[t, sigma * r8max + j] = scale_a * sum_k X[t, k] A_a,sigma[k, j]
 //    work item = (projection, shrink item, 16*NB-column chunk of A^T_cat)
 //
+//    Unsplit (shrink_kp = 1): a resident set of workgroups takes the work
+//    units (projection in the order sorder, longest K first; item; chunk)
+//    one at a time from a counter that the plan zeroes, so the long units
+//    start first and no workgroup is spent on the host's padding of the
+//    item count.
+//
 //    Small batches (shrink_kp = kShrinkKP): an item's adapter group holds a
 //    few scattered tokens, and every item reads its rows out of the whole
 //    X, so each XCD would fetch most of X from HBM.  There each item's K is
@@ -58,14 +64,26 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
     constexpr int MT = MB * 16, NT = NB * 16, LD = NT + 4;
     __shared__ float red[4 * MT * LD];
     const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15;
-    const int n_items = a.meta[1];
-    const int per_proj = a.items_bound * a.cchunks;
+    // (clamped: the plan writes at most items_bound items)
+    const int n_items = min(a.meta[1], a.items_bound);
     const int KP = a.shrink_kp;
+    const bool queue = KP == 1;
+    const int per_proj = (queue ? n_items : a.items_bound) * a.cchunks;
     const int total = a.n_proj * per_proj * KP;
+    __shared__ int s_unit;
 
-    for (int flat = blockIdx.x; flat < total; flat += gridDim.x) {
+    for (int iter = 0;; ++iter) {
+        int flat = blockIdx.x + iter * gridDim.x;
+        if (queue) {
+            if (threadIdx.x == 0) s_unit = atomicAdd(a.queue, 1);
+            __syncthreads();
+            flat = s_unit;
+            __syncthreads();
+        }
+        if (flat >= total) break;
         const int f = flat / KP, kp = flat - f * KP;
-        const int p = f / per_proj, rem = f - p * per_proj;
+        const int ps = f / per_proj, rem = f - ps * per_proj;
+        const int p = queue ? a.sorder[ps] : ps;
         const int item = rem / a.cchunks, cc = rem - item * a.cchunks;
         const int4 it = a.items[item];       // in bounds for every item < items_bound
         if (item >= n_items) continue;
@@ -167,32 +185,62 @@ __global__ __launch_bounds__(256) void shrink_reduce_kernel(FwdArgs a) {
     }
 }
 
+// workgroups of the shrink kernel that the device holds at once (cached)
+template <int MB, int NB, bool XRM>
+int shrink_resident() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0, cu = 0, per = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, shrink_kernel<MB, NB, XRM>, kThreads, 0) != hipSuccess)
+            return 0;
+        n = cu * (per > 1 ? per : 1);
+    }
+    return n;
+}
+
 hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
     const int KP = a.shrink_kp;
     if (KP != 1 && (KP != kShrinkKP || !a.shrinkpart)) return hipErrorInvalidValue;
+    if (KP == 1 && !a.queue) return hipErrorInvalidValue;
+    for (int i = 0; i < a.n_proj; ++i)
+        if (a.sorder[i] < 0 || a.sorder[i] >= a.n_proj) return hipErrorInvalidValue;
     const int tiles = a.n_proj * a.items_bound * a.cchunks;
     const int total = tiles * KP;
-    // a multiple of 8 (with KP = 8 each workgroup keeps one k-range)
-    const int grid = total < 4096 ? total : 4096;
-    if (grid <= 0) return hipSuccess;
+    // split: a multiple of 8 (with KP = 8 each workgroup keeps one k-range);
+    // unsplit: the resident workgroups take units from the queue
+    const int cap = 4096;
+    if (total <= 0) return hipSuccess;
     const int rgrid = tiles < 2048 ? tiles : 2048;
     // every projection of a launch reads X the same way (the large-tile path
     // reads the caller's row-major X)
     const bool xrm = a.p[0].x_rowmajor != 0;
     for (int i = 1; i < a.n_proj; ++i)
         if ((a.p[i].x_rowmajor != 0) != xrm) return hipErrorInvalidValue;
+#define BDL_SHRINK_LAUNCH(M, NN, X)                                                                 \
+    {                                                                                               \
+        int grid = total < cap ? total : cap;                                                       \
+        if (KP == 1) {                                                                              \
+            const int r = shrink_resident<M, NN, X>();                          \
+            if (r <= 0) return hipErrorInvalidValue;                                                \
+            grid = total < r ? total : r;                                                           \
+        }                                                                                           \
+        hipLaunchKernelGGL((shrink_kernel<M, NN, X>), dim3(grid), dim3(kThreads), 0, s, a);         \
+    }
 #define BDL_SHRINK_CASE(M, NN)                                                                          \
     if (mb == M && nb == NN) {                                                                          \
         if (xrm)                                                                                        \
-            hipLaunchKernelGGL((shrink_kernel<M, NN, true>), dim3(grid), dim3(kThreads), 0, s, a);     \
+            BDL_SHRINK_LAUNCH(M, NN, true)                                                              \
         else                                                                                            \
-            hipLaunchKernelGGL((shrink_kernel<M, NN, false>), dim3(grid), dim3(kThreads), 0, s, a);    \
+            BDL_SHRINK_LAUNCH(M, NN, false)                                                             \
         if (KP > 1) hipLaunchKernelGGL((shrink_reduce_kernel<M, NN>), dim3(rgrid), dim3(256), 0, s, a); \
         return hipGetLastError();                                                                       \
     }
     BDL_SHRINK_CASE(1, 1) BDL_SHRINK_CASE(1, 2) BDL_SHRINK_CASE(1, 4)
     BDL_SHRINK_CASE(4, 1) BDL_SHRINK_CASE(4, 2) BDL_SHRINK_CASE(4, 4)
 #undef BDL_SHRINK_CASE
+#undef BDL_SHRINK_LAUNCH
     return hipErrorInvalidValue;
 }
 

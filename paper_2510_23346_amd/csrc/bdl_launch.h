@@ -68,6 +68,8 @@ struct FwdArgs {
     int cchunks;              // shrink: column chunks per item (upper bound)
     int shrink_kp;            // shrink: k-ranges per item (1, or kShrinkKP: fp32 partials in
                               // shrinkpart that a second launch sums into Z)
+    int* queue;               // unsplit shrink: unit counter, zeroed by the plan (meta[2])
+    int sorder[kMaxProjs];    // unsplit shrink: projections in unit order (longest K first)
     float* shrinkpart;        // split shrink: fp32 partials (kShrinkPartElems)
     const int* tile_oct;      // expand octet codes per row tile (-1 padded)
     int oct_cap;              // entries per row tile in tile_oct
@@ -127,7 +129,7 @@ struct PrepArgs {
     int* gcount;
     int4* items;
     int* tile_oct;
-    int* meta;                // [0] groups, [1] shrink items
+    int* meta;                // [0] groups, [1] shrink items, [2] the shrink's unit counter (zeroed)
     int* err;
     PackJob jobs[kMaxProjs];
     int n_jobs;

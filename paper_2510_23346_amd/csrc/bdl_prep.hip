@@ -429,6 +429,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
     if (tid == 1023) {
         a.meta[0] = g_off;
         a.meta[1] = i_off;
+        a.meta[2] = 0;
     }
     __syncthreads();
     if (a.tgrp)
