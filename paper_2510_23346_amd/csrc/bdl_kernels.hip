@@ -61,8 +61,10 @@ constexpr int kStages = 3;                    // k-steps of loads kept in flight
 // large-tile path); else the packed X
 template <int MB, int NB, bool XRM>
 __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
-    constexpr int MT = MB * 16, NT = NB * 16, LD = NT + 4;
-    __shared__ float red[4 * MT * LD];
+    constexpr int MT = MB * 16, NT = NB * 16, FR = MB * NB * 64;
+    // the waves' sums in lane order (fragment (rb, cb) of wave w at
+    // ((w MB + rb) NB + cb) 64 + lane), added in wave order after one barrier
+    __shared__ f32x4 red[kWaves * FR];
     const int w = wave_id(), l = threadIdx.x & 63, lr = l & 15;
     // (clamped: the plan writes at most items_bound items)
     const int n_items = min(a.meta[1], a.items_bound);
@@ -120,27 +122,35 @@ __global__ __launch_bounds__(kThreads) void shrink_kernel(FwdArgs a) {
         int k0, nk;
         wave_krange((kp + 1) * KS / KP - ks0, w, &k0, &nk);
         if (nk > 0) mma_range<MB, NB, kStages>(acc, ap, bp, ks0 + k0, nk, XRM ? 32 : kFrag, kFrag);
-        reduce_waves<MB, NB>(acc, red);
-
-        if (KP > 1) {
-            // partial tile of range kp (row-major MT x NT), summed by shrink_reduce_kernel
-            float* dst = a.shrinkpart + (size_t)flat * (MT * NT);
-            for (int idx = threadIdx.x; idx < MT * NT; idx += kThreads)
-                dst[idx] = red[(idx / NT) * LD + idx % NT];
-            __syncthreads();
-            continue;
-        }
-        for (int idx = threadIdx.x; idx < MT * NT; idx += kThreads) {
-            const int r = idx / NT, c = idx - (idx / NT) * NT;
-            const int cg = c0 + c;
-            if (r < nrows && cg < ncols) {
-                const int t = prow[r];
-                const int sig = cg / r8s, j = cg - sig * r8s;
-                const float z = sc * red[r * LD + c];
-                const uint16_t hi = f2bf(z);
-                const size_t zi = (size_t)t * P.zs + sig * a.r8max + j;
-                P.Z[zi] = hi;
-                P.Z[zi + P.zplane] = f2bf(z - bf2f(hi));
+#pragma unroll
+        for (int rb = 0; rb < MB; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < NB; ++cb) red[((w * MB + rb) * NB + cb) * 64 + l] = acc[rb][cb];
+        __syncthreads();
+        // thread = one fragment slot at a time: rows rb 16 + 4 (ln / 16) + i
+        // (i < 4), column cb 16 + ln mod 16
+        float* const part = a.shrinkpart + (size_t)flat * (MT * NT);
+        for (int e = threadIdx.x; e < FR; e += kThreads) {
+            f32x4 v = red[e];
+#pragma unroll
+            for (int ww = 1; ww < kWaves; ++ww) v += red[ww * FR + e];
+            const int fr = e >> 6, ln = e & 63, rb = fr / NB, cb = fr - rb * NB;
+            const int c = cb * 16 + (ln & 15), cg = c0 + c;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = rb * 16 + 4 * (ln >> 4) + i;
+                if (KP > 1) {
+                    // partial tile of range kp (row-major MT x NT), summed by shrink_reduce_kernel
+                    part[r * NT + c] = v[i];
+                } else if (r < nrows && cg < ncols) {
+                    const int t = prow[r];
+                    const int sig = cg / r8s, j = cg - sig * r8s;
+                    const float z = sc * v[i];
+                    const uint16_t hi = f2bf(z);
+                    const size_t zi = (size_t)t * P.zs + sig * a.r8max + j;
+                    P.Z[zi] = hi;
+                    P.Z[zi + P.zplane] = f2bf(z - bf2f(hi));
+                }
             }
         }
         __syncthreads();
