@@ -699,10 +699,11 @@ struct Shapes {
 // activations) that still leaves enough workgroups to occupy the chip.
 static Shapes pick_shapes(int T, long long col_blocks = 0, int r8max = bdl::kMaxRank8) {
     Shapes k;
-    k.smb = T <= 512 ? 1 : 4;
-    // prefill shrink items: 64 rank columns, or 32 when no adapter is wider
-    // (a rank-32 adapter's slice then fills its chunk instead of half of it)
-    k.snb = T <= 512 ? 1 : (r8max <= 32 ? 2 : 4);
+    // prefill shrink items: 64 rows x 64 rank columns; when no adapter is
+    // wider than rank 32, 32 rows x 96 columns, so that the three slices of
+    // a q/k/v projection come out of one pass over its rows of X
+    k.smb = T <= 512 ? 1 : (r8max <= 32 ? 2 : 4);
+    k.snb = T <= 512 ? 1 : (r8max <= 32 ? 6 : 4);
     k.gmb = T <= 16 ? 1 : (T <= 32 ? 2 : 4);
     const long long row_tiles = (T + 16 * k.gmb - 1) / (16 * k.gmb);
     const long long blocks = col_blocks * row_tiles;

@@ -248,7 +248,7 @@ hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
         return hipGetLastError();                                                                       \
     }
     BDL_SHRINK_CASE(1, 1) BDL_SHRINK_CASE(1, 2) BDL_SHRINK_CASE(1, 4)
-    BDL_SHRINK_CASE(4, 1) BDL_SHRINK_CASE(4, 2) BDL_SHRINK_CASE(4, 4)
+    BDL_SHRINK_CASE(4, 1) BDL_SHRINK_CASE(4, 2) BDL_SHRINK_CASE(4, 4) BDL_SHRINK_CASE(2, 6)
 #undef BDL_SHRINK_CASE
 #undef BDL_SHRINK_LAUNCH
     return hipErrorInvalidValue;
