@@ -363,9 +363,6 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
             // and, after an even k-step, the pair issued there; its pair was
             // issued before its weights
             big_wait_n((ks + 2 <= NK - 1 ? 2 : 0) + ((ks & 1) && ((ks - 1) >> 1) + 2 < NP ? 4 : 0));
-            if (!(ks & 1) && (ks >> 1) + 2 < NP)
-                big_issue_x<CP, NW>(src, (ks >> 1) + 2, xring + (((ks >> 1) + 2) % kBigXPairs) * 32 * 64, w);
-            if (nx < NK) big_issue_w<CP, NW>(src, nx, wring + (nx % ST) * 16 * 64, w);
         } else {
             // k-step ks + 1 is complete once at most the copies issued after it
             // (k-steps ks + 2 .. ks + ST - 2 below NK) are in flight
@@ -382,6 +379,14 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
             __builtin_amdgcn_sched_group_barrier(0x008, (4 * RB) / (RB + 4) > 0 ? (4 * RB) / (RB + 4) : 1, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
+        if constexpr (XRM) {
+            // the refills of the slots freed at this k-step's barrier follow
+            // its MFMAs: issued in a burst ahead of them they held them up
+            // (the next barrier's waits count them the same either way)
+            if (!(ks & 1) && (ks >> 1) + 2 < NP)
+                big_issue_x<CP, NW>(src, (ks >> 1) + 2, xring + (((ks >> 1) + 2) % kBigXPairs) * 32 * 64, w);
+            if (nx < NK) big_issue_w<CP, NW>(src, nx, wring + (nx % ST) * 16 * 64, w);
+        }
     };
     // k-step 0 is complete once at most the copies of k-steps 1 .. ST - 2 are
     // in flight (row-major X: the weights of k-steps 1 .. ST - 2; the pairs
