@@ -833,12 +833,16 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         units_max += (d.nWb + (long long)act_max * d.nbA) * (pi.K / 32);
         groups_max += (d.nWb + (long long)act_max * d.nbA + 3) / 4;
     }
-    // two workgroups per CU, each with at least 4 units (one k-step of a
-    // full group) whatever the number of adapters in use; the kernels' 32-bit
-    // schedule arithmetic needs units * workgroups < 2^32
+    // two workgroups per CU, each with at least 64 units (16 k-steps of a
+    // full group) whatever the number of adapters in use: a small layer
+    // (one 1792-column projection at 16 tokens) then runs on fewer, longer
+    // workgroups, so that each output group is split over fewer partial
+    // tiles, which its epilogue adds one by one (there 20.7 -> 17.5 us a
+    // step; larger layers keep two per CU); the kernels' 32-bit schedule
+    // arithmetic needs units * workgroups < 2^32
     // (at least one workgroup: one that owns every unit needs no minimum)
     const int grid = (int)std::min<long long>(
-        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, std::max(1LL, units_min / 4),
+        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, std::max(1LL, units_min / 64),
          0xffffffffLL / std::max(1LL, units_max)});
     if (grid < 1) return fail(BDLORA_ERR_SHAPE, "batch too large for the decode launch's schedule");
     float* part = ws.part;
