@@ -50,11 +50,12 @@ constexpr int kStages = 3;                    // k-steps of loads kept in flight
 //    Small batches (shrink_kp = kShrinkKP): an item's adapter group holds a
 //    few scattered tokens, and every item reads its rows out of the whole
 //    X, so each XCD would fetch most of X from HBM.  There each item's K is
-//    cut into kShrinkKP ranges, range k running on XCD k (workgroup b runs
-//    on XCD b mod 8, and the flat index keeps the range in its low bits):
-//    each XCD fetches only its range of X.  The ranges store fp32 partial
-//    tiles (their own workspace); shrink_reduce_kernel adds them in range
-//    order and writes Z.
+//    cut into kShrinkKP = 4 ranges, range k running on XCDs k and k + 4
+//    (workgroup b runs on XCD b mod 8, and the flat index keeps the range
+//    in its two low bits): each XCD fetches only its quarter of X.  (Eight
+//    ranges, one per XCD, leave each wave too few k-steps to stream.)  The
+//    ranges store fp32 partial tiles (their own workspace);
+//    shrink_reduce_kernel adds them in range order and writes Z.
 // --------------------------------------------------------------------------
 
 // XRM: the launch's projections read the caller's row-major X (the
@@ -218,7 +219,8 @@ hipError_t launch_shrink(const FwdArgs& a, int mb, int nb, hipStream_t s) {
         if (a.sorder[i] < 0 || a.sorder[i] >= a.n_proj) return hipErrorInvalidValue;
     const int tiles = a.n_proj * a.items_bound * a.cchunks;
     const int total = tiles * KP;
-    // split: a multiple of 8 (with KP = 8 each workgroup keeps one k-range);
+    // split: every unit at once, or a multiple of 8 workgroups (either way
+    // each workgroup keeps one k-range, so XCD b mod 8 gets range b mod 4);
     // unsplit: the resident workgroups take units from the queue
     const int cap = 4096;
     if (total <= 0) return hipSuccess;

@@ -20,7 +20,7 @@ constexpr int kBigM = 256, kBigN = 256;   // output tile of the large-tile base 
 constexpr int kBigPartSlots = 256;        // fp32 partial tiles of the large-tile GEMM's split tiles
 constexpr int kBigPartElems = kBigM * kBigN;
 constexpr int kMidMaxT = 256;             // medium-batch base GEMM: largest batch (all rows in one tile)
-constexpr int kShrinkKP = 8;              // shrink k-ranges per item when split (one per XCD)
+constexpr int kShrinkKP = 4;              // shrink k-ranges per item when split (range k on XCDs k, k + 4)
 constexpr long long kShrinkPartElems = 8LL << 20;   // fp32 partials of the split shrink (32 MiB)
 
 // One projection of a forward launch.
