@@ -86,6 +86,30 @@ def test_tiny_parity(torch_cuda, T):
     pool.close()
 
 
+def test_consecutive_batches_on_one_pool(torch_cuda):
+    """Two adapted batches of different sizes through one pool (the shrink's
+    unit counter, the plan tables and the partial workspaces are reused):
+    each matches the oracle on every row.  Rows are computed independently,
+    so the first 300 rows of the 700-token forward are the smaller batch's
+    reference."""
+    torch = torch_cuda
+    T = 700
+    rng = np.random.default_rng(77)
+    ids = rng.integers(-1, len(TINY_RANKS), size=T)
+    spec = wl.custom_workload("two-batches", wl.tiny_projs(), T, TINY_RANKS,
+                              scales=[0.5 + 0.25 * i for i in range(len(TINY_RANKS))], ids=ids, seed=77)
+    layer = wl.draw_layer(spec, slots=range(len(TINY_RANKS)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(TINY_RANKS)), cache=layer.adapters)
+    refs = bdlora.layer_forward(layer)
+    for t in (T, 300, T):
+        _, ys = _run_layer(torch, spec, layer, pool, T=t)
+        for p in range(len(spec.projs)):
+            _check(ys[p], refs[p][:t], what=f"T={t} proj={spec.projs[p].name}")
+    assert pool.device_error() == 0
+    pool.close()
+
+
 def test_base_only_rows_equal_no_adapter_rows(torch_cuda):
     torch = torch_cuda
     T = 48
