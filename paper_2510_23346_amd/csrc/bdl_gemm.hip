@@ -438,6 +438,8 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
         int cd = code[h];
         for (int e = 0;;) {
             if (!__any(cd >= 0)) break;
+            // the next four codes, in flight with this turn's operands
+            const int cdn = e + 8 <= a.oct_cap ? codes[e + 4 + lg] : -1;
             const int slot = cd >> 12, r8s = (cd >> 4) & 0xff, j0 = (cd & 15) * 8;
             u32x4 bv[8];
 #pragma unroll
@@ -467,7 +469,7 @@ __global__ __launch_bounds__(128 * (16 / RB)) void gemm_big_kernel(FwdArgs a) {
             }
             e += 4;
             if (e + 4 > a.oct_cap) break;
-            cd = codes[e + lg];
+            cd = cdn;
         }
     }
 
