@@ -9,12 +9,14 @@
 // tile is 16 activation and 16 weight fragments (1 KB per 16 rows x 32 k).
 // They go from global memory straight into LDS (buffer_load_dwordx4 ... lds:
 // lane l of a wave writes the 16 bytes at offset 16 l of the wave's 1 KB
-// destination, which is exactly a fragment), kBigStages k-steps deep, with
-// one barrier per k-step.  The weight is read in its packed fragment layout;
-// the activations straight from the caller's row-major X (each lane's global
-// offset picks the 16 bytes of its token's row that its fragment slot holds,
-// so no pass packs X first), or from a packed copy when X is an intermediate
-// already written in fragments.  Eight
+// destination), with one barrier per k-step.  The weight is read in its
+// packed fragment layout, a k-step per slot of a ring of kBigStages slots.
+// The activations come straight from the caller's row-major X (no pass packs
+// X first): a copy takes 8 rows x 128 bytes, the two k-steps of a pair, each
+// lane's global offset picking 16 bytes of its token's row, into a ring of
+// pair slots beside the weights' ring; or, when X is an intermediate already
+// written in fragments, from that packed copy, a k-step per stage of one
+// ring.  A k-step's refills are issued after its MFMAs.  Eight
 // waves, 4 row quarters x 2 column halves, each own a 64 x 128 sub-tile for
 // the whole K (no cross-wave reduction): per k-step a wave reads 4 + 8
 // fragments from LDS (half a k-step ahead of the MFMAs that use them) and
@@ -49,11 +51,12 @@ constexpr int kBigBand = 4;                      // row tiles per band of the ti
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Where this thread's copies of a k-step come from: copies i < CP / 2 are
+// Where this thread's copies come from: copies i < CP / 2 of a k-step are
 // activation fragments, the others weight fragments (fragment w + NW i of
 // the k-step's 32), each a buffer load of 16 bytes per lane at byte offset
-// vo[i] + 1024 ks (weights, packed X) or vo[i] + 64 ks (X row-major: the
-// lane's 8 inputs of its row).  Buffer loads (not global ones) so that the
+// vo[i] + 1024 ks (weights, packed X); with row-major X the activation
+// copies of pair q are at xo[j] + 128 q instead (see big_issue_x).  Buffer
+// loads (not global ones) so that the
 // compiler's wait-count bookkeeping treats them as plain vector-memory
 // operations and keeps its LDS wait counts exact; their bounds are the
 // operands' sizes, so no lane can read past X or W.
