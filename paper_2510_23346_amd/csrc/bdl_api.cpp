@@ -1018,8 +1018,8 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     bool mid = !big && T > bdl::kDecodeMaxT && T <= bdl::kMidMaxT && MT == 64 && P->d_bigpart != nullptr;
     for (int i = 0; i < n; ++i) {
         const ProjInfo& pi = L.proj[projs[i]];
-        const long long xb = ((long long)T + 15) / 16 * 16 * pi.K * 2;
-        mid = mid && pi.wfmt == BDLORA_WEIGHT_BF16 && xb < (1LL << 31);
+        const long long xb = ((long long)T + 15) / 16 * 16 * pi.K * 2, wb = (long long)pi.N * pi.K * 2;
+        mid = mid && pi.wfmt == BDLORA_WEIGHT_BF16 && xb < (1LL << 31) && wb < (1LL << 31);
     }
     const int mid_nb = 2, mid_rb = T <= 128 ? 8 : 16, mid_tn = 128 * mid_nb;
     int mid_split[bdl::kMaxProjs];
@@ -1092,6 +1092,9 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
     for (int i = 0; i < n; ++i) xrm = xrm && L.proj[projs[i]].K % 64 == 0;
     if (xrm)
         for (int i = 0; i < n; ++i) ksplit[i] = std::min(ksplit[i], std::max(1, L.proj[projs[i]].K / 64));
+    // the medium-batch GEMM's copies (one k-step of a row at a time) and its
+    // shrink read the caller's X too, for any K
+    if (mid && pack) xrm = true;
     int tile = 0, cch = 1, fix = 0, pslot = 0, mid_cols = 0;
     for (int q = 0; q < n; ++q) {
         const int i = order[q];
@@ -1099,10 +1102,10 @@ static int forward_prefill(bdlora_pool_t P, int n, const int32_t* projs, const v
         bdl::ProjLaunch& pl = fa.p[q];
         pl.X = (const uint16_t*)X[i];
         pl.Xp = P->d_Xp[projs[i]];
-        // the large tiles and their shrink gather rows of the caller's X
-        // directly (32-bit offsets: T K 2 < 2^31 is part of the path's
-        // condition); an intermediate already packed (pack false) is read
-        // from Xp
+        // the large and medium-batch tiles and their shrink gather rows of
+        // the caller's X directly (32-bit offsets: T K 2 < 2^31 is part of
+        // the paths' conditions); an intermediate already packed (pack
+        // false) is read from Xp
         pl.x_rowmajor = xrm ? 1 : 0;
         pl.W = (const uint16_t*)W[i];
         pl.Ws = int4_scales(pi, W[i]);

@@ -568,14 +568,16 @@ hipError_t launch_gemm_big(const FwdArgs& a, hipStream_t s) {
 // weight fragment is read from HBM once and meets all T rows.
 //
 // Work item = (projection, 8 NB column blocks, k-range).  Per k-step the RB
-// activation fragments (all rows) go from global memory into LDS by DMA,
-// kMidStages k-steps deep, and all eight waves read them there; each wave
-// streams its own NB weight fragments straight into registers through a
-// ring of the same depth, so the weight never passes through LDS.  A wave
-// issues RB NB MFMAs per k-step (weight fragment as the A operand: a lane
-// holds 4 consecutive columns of one row).  Every item stores its fp32 sum
-// as a partial tile in lane order ((wave RB + rb) NB + cb) 64 + lane.  The
-// k-ranges split long-K tiles so that the items fill the chip once.
+// activation fragments (all rows, gathered from the caller's row-major X)
+// go from global memory into LDS by DMA, kMidStages k-steps deep, and all
+// eight waves read them there; each wave copies its own NB weight fragments
+// into LDS the same way, so that every load a k-step waits for is such a
+// copy (the wait counts loads in flight, and a load into registers can
+// complete ahead of an older copy into LDS).  A wave issues RB NB MFMAs per
+// k-step (weight fragment as the A operand: a lane holds 4 consecutive
+// columns of one row).  Every item stores its fp32 sum as a partial tile in
+// lane order ((wave RB + rb) NB + cb) 64 + lane.  The k-ranges split long-K
+// tiles so that the items fill the chip once.
 //
 // mid_epi_kernel then computes each output: the sum of its partials in
 // range order plus the expand of the token's own adapter (steps "Y_adapter
@@ -594,8 +596,10 @@ __device__ __forceinline__ void mid_copy(__amdgpu_buffer_rsrc_t r, u32x4* dst, i
 template <int RB, int NB>
 __global__ __launch_bounds__(512) void gemm_mid_kernel(FwdArgs a) {
     constexpr int NW = 8, CPX = RB / NW, D = kMidStages;
+    constexpr int SF = RB + NW * NB;          // fragments per stage: activations, then each wave's weights
     static_assert(RB % NW == 0 && D >= 3, "each wave copies RB / 8 fragments per k-step");
-    __shared__ u32x4 lds[D * RB * 64];
+    static_assert(D * SF * 1024 <= 160 * 1024, "the stages fit the LDS");
+    __shared__ u32x4 lds[D * SF * 64];
     const int w = wave_id(), l = threadIdx.x & 63;
     const int bid = blockIdx.x;
     if (bid >= a.mid_items) return;
@@ -611,36 +615,50 @@ __global__ __launch_bounds__(512) void gemm_mid_kernel(FwdArgs a) {
     // activation copies of a k-step: row block w + 8 i, i < CPX, of the tile.
     // Tile rows are positions in rowtok order (tokens grouped by adapter, so
     // the epilogue's consecutive rows share adapters); each lane gathers its
-    // row's token through its buffer-load offset: the token's fragment, lane
-    // slot (token mod 16) + 16 (l / 16).  Rows past T repeat a valid token
-    // (their sums are never read).
+    // row's token through its buffer-load offset, and the copy puts lane l's
+    // 16 bytes at byte 16 l of the LDS fragment, so lane l = r + 16 c loads
+    // inputs 32 ks + 8 c .. + 7 of row r's token: in the caller's row-major
+    // X (k-steps 64 bytes apart; buffer bounds = X's size) or in the packed X
+    // (the token's fragment, lane slot (token mod 16) + 16 c; k-steps a
+    // fragment apart).  Rows past T repeat a valid token (their sums are
+    // never read).
+    const bool xrm = P.x_rowmajor != 0;
     const __amdgpu_buffer_rsrc_t rx =
-        __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
+        xrm ? __builtin_amdgcn_make_buffer_rsrc((void*)P.X, 0, T * P.K * 2, kRawBufferWord3)
+            : __builtin_amdgcn_make_buffer_rsrc((void*)P.Xp, 0, nrb * KS * 1024, kRawBufferWord3);
+    const int xst = xrm ? 64 : 1024;       // bytes from one k-step to the next
     int vo[CPX];
 #pragma unroll
     for (int i = 0; i < CPX; ++i) {
         const int pos = min((w + NW * i) * 16 + (l & 15), T - 1);
         const int t = (int)min((unsigned)a.rowtok[pos], (unsigned)(T - 1));
-        vo[i] = ((t >> 4) * KS + k0) * 1024 + ((t & 15) + 16 * (l >> 4)) * 16;
+        vo[i] = xrm ? (t * P.K + k0 * 32 + 8 * (l >> 4)) * 2
+                    : ((t >> 4) * KS + k0) * 1024 + ((t & 15) + 16 * (l >> 4)) * 16;
     }
-    // this wave's weight column blocks (clamped at the projection's edge)
-    const char* wp[NB];
+    // this wave's weight column blocks (clamped at the projection's edge):
+    // copied the same way into the wave's own fragments RB + w NB + c of the
+    // stage.  Every load of a turn is then a copy into LDS: a load into
+    // registers issued after a copy can complete before it, so a wait that
+    // counts outstanding loads over both kinds would not tell that the
+    // older copy has landed.
+    const __amdgpu_buffer_rsrc_t rw =
+        __builtin_amdgcn_make_buffer_rsrc((void*)P.W, 0, ncb * KS * 1024, kRawBufferWord3);
+    int wo[NB];
 #pragma unroll
-    for (int c = 0; c < NB; ++c)
-        wp[c] = reinterpret_cast<const char*>(P.W + frag_index(min((tile * NW + w) * NB + c, ncb - 1), k0, KS)) + l * 16;
+    for (int c = 0; c < NB; ++c) wo[c] = (int)frag_index(min((tile * NW + w) * NB + c, ncb - 1), k0, KS) * 2 + l * 16;
 
-    // one pipeline turn: the activations of k-step ks into LDS stage d, the
-    // weights into wr.  Past the range the last k-step is loaded again, so
-    // every turn issues the same number of loads and the wait counts below
-    // are exact.
-    auto issue = [&](int ks, int d, u32x4 (&wr)[NB]) __attribute__((always_inline)) {
+    // one pipeline turn: the activations and weights of k-step ks into LDS
+    // stage d.  Past the range the last k-step is loaded again, so every
+    // turn issues the same number of copies and the wait counts below are
+    // exact.
+    auto issue = [&](int ks, int d) __attribute__((always_inline)) {
         const int kk = min(ks, NK - 1);
-        u32x4* stg = lds + d * RB * 64;
+        u32x4* stg = lds + d * SF * 64;
 #pragma unroll
         for (int i = 0; i < CPX; ++i)
-            mid_copy(rx, stg + (w + NW * i) * 64, vo[i] + kk * 1024);
+            mid_copy(rx, stg + (w + NW * i) * 64, vo[i] + kk * xst);
 #pragma unroll
-        for (int c = 0; c < NB; ++c) wr[c] = *reinterpret_cast<const u32x4*>(wp[c] + (size_t)kk * 1024);
+        for (int c = 0; c < NB; ++c) mid_copy(rw, stg + (RB + w * NB + c) * 64, wo[c] + kk * 1024);
     };
 
     f32x4 acc[RB][NB];
@@ -648,23 +666,25 @@ __global__ __launch_bounds__(512) void gemm_mid_kernel(FwdArgs a) {
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
         for (int c = 0; c < NB; ++c) acc[rb][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    u32x4 wr[D][NB];
 #pragma unroll
-    for (int d = 0; d < D - 1; ++d) issue(d, d, wr[d]);
+    for (int d = 0; d < D - 1; ++d) issue(d, d);
 
-    // k-step ks uses stage and ring slot u = ks mod D.  Its loads are complete
-    // once at most the D - 2 later turns are in flight; the barrier makes every
-    // wave's copies visible and ends every wave's reads of k-step ks - 1, whose
-    // stage and ring slot the next turn refills.
+    // k-step ks uses stage u = ks mod D.  Its copies are complete once at
+    // most the D - 2 later turns are in flight; the barrier makes every
+    // wave's copies visible and ends every wave's reads of k-step ks - 1,
+    // whose stage the next turn refills.
     auto step = [&](int ks, int u) __attribute__((always_inline)) {
         big_wait_barrier<(D - 2) * (CPX + NB)>();
-        issue(ks + D - 1, (u + D - 1) % D, wr[(u + D - 1) % D]);
-        const u32x4* stg = lds + u * RB * 64;
+        issue(ks + D - 1, (u + D - 1) % D);
+        const u32x4* stg = lds + u * SF * 64;
+        u32x4 wv[NB];
+#pragma unroll
+        for (int c = 0; c < NB; ++c) wv[c] = stg[(RB + w * NB + c) * 64 + l];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
             const u32x4 x = stg[rb * 64 + l];
 #pragma unroll
-            for (int c = 0; c < NB; ++c) acc[rb][c] = mfma(wr[u][c], x, acc[rb][c]);
+            for (int c = 0; c < NB; ++c) acc[rb][c] = mfma(wv[c], x, acc[rb][c]);
         }
     };
     int ks = 0;

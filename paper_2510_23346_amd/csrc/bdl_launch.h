@@ -27,8 +27,8 @@ constexpr long long kShrinkPartElems = 8LL << 20;   // fp32 partials of the spli
 struct ProjLaunch {
     const uint16_t* X;        // [T x K] bf16 activations (row-major)
     const uint16_t* Xp;       // packed activations, fragment layout, rows padded to 16
-    int x_rowmajor;           // large-tile path: the shrink and the GEMM read X (row-major, rows
-                              // gathered by token) and Xp is not written; else they read Xp
+    int x_rowmajor;           // large-tile and medium-batch paths: the shrink and the GEMM read X
+                              // (row-major, rows gathered by token) and Xp is not written; else Xp
     const uint16_t* W;        // packed base weight, fragment layout ([N x K] nn.Linear rows)
     const uint16_t* Ws;       // INT4 base: its scales (null for a bf16 base)
     uint16_t* out;            // [T x N] bf16
