@@ -18,6 +18,8 @@ Covered here:
   256-column tiles, with ranks from 1 to 64 (the expand's loop past 16
   ranks);
 - edge batches: no adapted token, and one rank-64 adapter for every token;
+- five forwards with the caches flushed before each (the k-step wait of the
+  main launch with activations arriving slowly from memory);
 - the path each shape takes (the rule that keeps small layers with few
   adapters on the 64-row kernel).
 Every case checks that the path ran (pool.last_path()).  The error rule is
@@ -143,6 +145,50 @@ def test_medium_edge_batches(torch_cuda, T, case):
     layer, ys, yb, path = _run(torch_cuda, spec, [0, 1])
     assert path == "medium", f"{case} T={T}: the batch took the {path} path"
     _check_all(layer, ids, ys, yb, f"{case} T={T}")
+
+
+def _small_projs():
+    return [
+        wl.ProjSpec("qkv", "column", 128, (272, 256, 16)),
+        wl.ProjSpec("o", "row", 160, (528,)),                 # K of 5 k-steps
+        wl.ProjSpec("up", "column", 96, (256,)),
+    ]
+
+
+def test_medium_parity_cold_caches(torch_cuda):
+    """The main launch's k-step wait must hold when the activations arrive
+    slowly from memory: the caches are flushed (1 GiB written) before each
+    of five forwards of a 65-token batch over small projections and twelve
+    adapters, and every forward matches the oracle.  (A form whose wait
+    counted copies into LDS together with loads into registers gave wrong
+    outputs in about half of such runs.)"""
+    torch = torch_cuda
+    ranks = [0, 1, 8, 16, 24, 33, 64, 5, 40, 12, 56, 32]
+    T = 65
+    rng = np.random.default_rng(1000 + T)
+    ids = rng.integers(-1, len(ranks), size=T)
+    spec = wl.custom_workload("mid-cold-65", _small_projs(), T, ranks,
+                              scales=[0.5 + 0.125 * i for i in range(len(ranks))], ids=ids, seed=T)
+    layer = wl.draw_layer(spec, slots=range(len(ranks)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(ranks)), cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    refs = bdlora.layer_forward(layer)
+    flush = torch.empty(1 << 29, dtype=torch.float16, device="cuda")
+    projs = list(range(len(spec.projs)))
+    for it in range(5):
+        for o in dl.out:
+            o.fill_(float("nan"))
+        flush.fill_(it)
+        pool.forward_layer(projs, dl.X, dl.W, dl.out, dl.ids)
+        torch.cuda.synchronize()
+        assert pool.last_path() == "medium"
+        ys = dl.outputs()
+        for p, pi in enumerate(layer.projs):
+            e = bdlora.rel_errors(ys[p], refs[p])
+            assert e["pointwise"] <= TOL, f"run {it} {pi.spec.name}: {e}"
+    assert pool.device_error() == 0
+    pool.close()
 
 
 @pytest.mark.parametrize("model,T,n_slots,path", [
