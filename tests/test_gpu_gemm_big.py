@@ -5,14 +5,16 @@ Batches above 256 tokens with bf16 base weights take that kernel; when a
 batch has too few tiles to fill the chip, long-K tiles are split into
 k-ranges whose fp32 partials a fix-up launch adds (the small shapes above
 256 tokens here are all split; the full-size prefill workloads in
-test_gpu_parity are not).  65 and 130 tokens check the 64-row kernel on the
-same shapes.  The
+test_gpu_parity are not).  On the same shapes, 65 tokens take the
+medium-batch launches and 130 the 64-row kernel.  The
 projections here are wider than one 256-column tile, with a ragged column
 tail, slice boundaries inside a tile, and more row tiles than one with a
 ragged row tail, so that the clamped edge blocks, the per-64-row octet lists
 and the slice lookup of the expand are all exercised.  Ranks go up to 64
 (eight octets per adapter) and a 64-row block holds many adapters, so the
-expand loop runs several passes.  Error rule as in test_gpu_parity.
+expand loop runs several passes.  One case repeats a forward five times
+with the caches flushed before each (the k-step waits with operands arriving
+slowly from memory).  Error rule as in test_gpu_parity.
 """
 import numpy as np
 import pytest
@@ -112,5 +114,47 @@ def test_big_tile_edge_batches(torch_cuda, T, case):
     for p, pi in enumerate(layer.projs):
         e = bdlora.rel_errors(ys[p], refs[p])
         assert e["pointwise"] <= TOL, f"{case} T={T} {pi.spec.name}: {e}"
+    assert pool.device_error() == 0
+    pool.close()
+
+
+def _projs_k64():
+    return [
+        wl.ProjSpec("qkv", "column", 128, (272, 256, 16)),
+        wl.ProjSpec("o", "row", 192, (528,)),                 # K of 6 k-steps
+        wl.ProjSpec("up", "column", 256, (256,)),
+    ]
+
+
+def test_big_tile_parity_cold_caches(torch_cuda):
+    """The large tiles' k-step waits with activations and weights arriving
+    slowly from memory: every K a multiple of 64, so the launch and its
+    shrink read the caller's row-major X; the caches are flushed (1 GiB
+    written) before each of five forwards of a 520-token batch, and every
+    forward matches the oracle."""
+    torch = torch_cuda
+    T = 520
+    rng = np.random.default_rng(7520)
+    ids = rng.integers(-1, len(RANKS), size=T)
+    spec = wl.custom_workload("big-cold-520", _projs_k64(), T, RANKS,
+                              scales=[0.5 + 0.125 * i for i in range(len(RANKS))], ids=ids, seed=T)
+    layer = wl.draw_layer(spec, slots=range(len(RANKS)))
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, range(len(RANKS)), cache=layer.adapters)
+    dl = DeviceLayer(layer)
+    refs = bdlora.layer_forward(layer)
+    flush = torch.empty(1 << 29, dtype=torch.float16, device="cuda")
+    projs = list(range(len(spec.projs)))
+    for it in range(5):
+        for o in dl.out:
+            o.fill_(float("nan"))
+        flush.fill_(it)
+        pool.forward_layer(projs, dl.X, dl.W, dl.out, dl.ids)
+        torch.cuda.synchronize()
+        assert pool.last_path() == "large"
+        ys = dl.outputs()
+        for p, pi in enumerate(layer.projs):
+            e = bdlora.rel_errors(ys[p], refs[p])
+            assert e["pointwise"] <= TOL, f"run {it} {pi.spec.name}: {e}"
     assert pool.device_error() == 0
     pool.close()
