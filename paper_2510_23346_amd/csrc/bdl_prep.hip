@@ -11,13 +11,16 @@
 //   items       shrink work items {slot, first perm index, rows <= mts, r8}
 //   tile_oct    (when asked for) per base-GEMM row tile: the 8-rank octets of
 //               every adapter present in the tile, slots ascending, code =
-//               slot<<12 | r8<<4 | octet, padded with -1 to oct_cap entries
+//               slot<<12 | r8<<4 | octet, followed by kOctTail entries of -1
+//               (fewer at the end of the tile's oct_cap entries)
 // Tokens are grouped by adapter (a counting sort over slots) so that every
 // adapter's factors are streamed once per batch (heterogeneous batching of
 // unmerged adapters, paper Sec. 1 and Sec. 2).
 #include "bdl_device.h"
 
 namespace bdl {
+
+constexpr int kOctTail = 36;   // -1 entries after an octet list's last code (see the octet lists below)
 
 // inclusive prefix sum over the 64 lanes of a wave (DPP row shifts, then row
 // broadcasts of lanes 15 and 31)
@@ -493,7 +496,12 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
         }
     }
 
-    // expand octet lists of the base-GEMM row tiles, one tile per wave
+    // expand octet lists of the base-GEMM row tiles, one tile per wave.  A
+    // list ends with kOctTail entries of -1: its readers take the codes in
+    // groups of 4, the 64-row kernel's 8 waves a group each, 32 entries
+    // apart, and stop at their first group of -1 (so they read at most 35
+    // entries past the last code); the large tiles read the groups in order,
+    // one group ahead.
     if (a.tile_oct && wv > 0) {
         const int mt = a.gemm_mt;
         const int tiles = (a.T + mt - 1) / mt;
@@ -523,7 +531,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
                     for (int j = 0; j < c; ++j) dst[o++] = (slot << 12) | (r8s << 4) | j;
                     base += wave_total(inc);
                 }
-                for (int i = base + lane; i < a.oct_cap; i += 64) dst[i] = -1;
+                for (int i = base + lane; i < min(a.oct_cap, base + kOctTail); i += 64) dst[i] = -1;
                 continue;
             }
             for (int i = lane; i < nwords; i += 64) bm[i] = 0u;
@@ -547,7 +555,7 @@ __global__ __launch_bounds__(1024) void prep_kernel(PrepArgs a) {
                 }
                 base += wave_total(inc);
             }
-            for (int i = base + lane; i < a.oct_cap; i += 64) dst[i] = -1;
+            for (int i = base + lane; i < min(a.oct_cap, base + kOctTail); i += 64) dst[i] = -1;
         }
     }
     if (tid == 0 && s_err) atomicOr(a.err, 1);
