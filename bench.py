@@ -454,6 +454,8 @@ def measure(index, K, warmup, rotate=0, eager=False):
         # base partials), epilogue (partial sums + expand); main moves the
         # weights and dominates
         names = ("prep", "main", "epilogue")
+        if spec.T <= bd.DECODE_PLAN_IN_MAIN_T:
+            names = ("", "main", "epilogue")    # planned inside the main launch: no prep launch
         dom, dom_name = 1, "bdl::dec_main_kernel"
         algo = m_bytes
         achieved = algo / (k_ms[dom] * 1e-3) / 1e9
@@ -515,7 +517,7 @@ def measure(index, K, warmup, rotate=0, eager=False):
             "TFLOP/s": round((g_flops + s_flops) / (ms_per_step * 1e-3) / 1e12, 2),
             "frac": round((g_flops + s_flops) / (ms_per_step * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4),
         },
-        "kernel_ms": {nm: round(v, 5) for nm, v in zip(names, k_ms)},
+        "kernel_ms": {nm: round(v, 5) for nm, v in zip(names, k_ms) if nm},
         "roofline": roof,
     }
     for pool, _ in sets:

@@ -17,7 +17,7 @@ import numpy as np
 
 __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
-    "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T",
+    "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T", "DECODE_PLAN_IN_MAIN_T",
     "ACT_NONE", "ACT_SILU_MUL", "WEIGHT_BF16", "WEIGHT_INT4_G128", "pack_weight_int4",
     "packed_weight_bytes", "MAX_SEGMENTS", "Segments", "layout_slot_bytes", "pack_adapter_layout",
 ]
@@ -25,6 +25,7 @@ __all__ = [
 COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
+DECODE_PLAN_IN_MAIN_T = 16   # BDLORA_DECODE_PLAN_IN_MAIN_T: decode batches planned inside the K-split launch
 MAX_SEGMENTS = 256      # BDLORA_MAX_SEGMENTS: most segments of a batch given as segments
 STATIC_SCRATCH_BYTES = 32 << 20   # BDLORA_STATIC_SCRATCH_BYTES: static scratch of forward_layer_static
 ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections

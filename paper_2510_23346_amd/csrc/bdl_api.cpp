@@ -754,7 +754,9 @@ static void fill_plan_args(bdlora_pool_t P, const Batch& B, int T, bdl::PrepArgs
 // reusing the first's plan and reading the intermediate the first's epilogue
 // packed.
 struct DecMode {
-    bool prep = true;              // run the prep launch (plan + activation packing)
+    bool prep = true;              // plan the batch and pack the activations (false: the tables hold this
+                                   // batch's plan and Xp its activations); at most 16 tokens the main
+                                   // launch plans it and reads the caller's X, with no prep launch
     int mlp_act = -1;              // >= 0: the epilogue writes the MLP intermediate
     uint16_t* h_dst = nullptr;     // where (fragment layout of the second projection's input)
     int h_KS = 0;
@@ -800,6 +802,12 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
                           const void* const* W, void* const* out, const Batch& B, int T, hipStream_t s,
                           const DecWs& ws, const DecMode& mode = DecMode()) {
     const Layout& L = P->L;
+    // batches of one row block: the main launch plans the batch in every
+    // wave and reads the caller's X, so no prep launch runs (the gathered
+    // rows cost that launch less than the prep launch takes; with more row
+    // blocks they cost more)
+    static_assert(BDLORA_DECODE_PLAN_IN_MAIN_T == 16, "the folded plan runs the one-row-block kernel");
+    const bool fold = mode.prep && T <= BDLORA_DECODE_PLAN_IN_MAIN_T;
     // adapter positions of the launches: the loaded adapters bound the
     // distinct ones a batch can use (the plan treats any past that bound as
     // none and raises the error flag).  Both forms of the batch (ids,
@@ -815,6 +823,7 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
     for (int i = 0; i < n; ++i) {
         const ProjInfo& pi = L.proj[projs[i]];
         bdl::DecProj& d = da.p[i];
+        d.X = fold ? (const uint16_t*)X[i] : nullptr;
         d.Xp = ws.Xp[i];
         d.W = (const uint16_t*)W[i];
         d.Ws = int4_scales(pi, W[i]);
@@ -940,8 +949,22 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         ++P->prof_used;
         --P->prof_left;
     }
+    if (fold) {
+        // the plan's inputs for the main launch
+        da.plan = 1;
+        da.ids = B.ids;
+        da.n_seg = B.ids ? 0 : B.n_seg;
+        if (da.n_seg > bdl::kDecodeMaxT) return fail(BDLORA_ERR_INVALID_ARG, "more segments than tokens");
+        for (int i = 0; i < da.n_seg; ++i) {
+            da.seg_start[i] = B.seg_start[i];
+            da.seg_slot[i] = B.seg_slot[i];
+        }
+        da.loaded = P->d_loaded;
+        da.r8 = P->d_r8;
+        da.max_slots = L.max_slots;
+    }
     if (ev) BDL_HIP(hipEventRecord(ev[0], s));
-    if (mode.prep) BDL_HIP(bdl::launch_prep(pa, s));
+    if (mode.prep && !fold) BDL_HIP(bdl::launch_prep(pa, s));
     if (ev) BDL_HIP(hipEventRecord(ev[1], s));
     if (ev) BDL_HIP(hipEventRecord(ev[2], s));
     BDL_HIP(bdl::launch_dec_main(da, k.gmb, s));

@@ -1,5 +1,7 @@
 // Decode path (batches of at most kDecodeMaxT tokens): two launches after
-// the prep launch (plan + activation packing).
+// the prep launch (plan + activation packing); batches of at most 16 tokens
+// skip the prep launch (the main launch plans the batch in every wave and
+// reads the caller's X).
 //
 //  dec_main_kernel -- one split-K GEMM of the packed activations X [T x K]
 //                     against a virtual column list per projection: the
@@ -174,6 +176,108 @@ __device__ __forceinline__ const uint16_t* dec_block(const DecArgs& a, const Dec
     return a.pool + (size_t)slot * a.slot_stride + P.a_off + frag_index(c, 0, KS);
 }
 
+// The batch's plan, computed by a wave of the main launch (lane t holds
+// token t; T <= 64), with the prep launch's decode plan's results: ids
+// checked against the loaded slots, the adapters in use in ascending slot
+// order ("groups"; at most act_max of them: any past that bound, possible
+// only when a captured forward replays after more adapters were loaded, are
+// treated as none and raise the error flag), each token's group.  Lane g
+// gets the slot and padded rank of group g (0 from the count on); the count
+// is returned.  Pools of at most 64 slots keep the slot tables in lanes (one
+// load round trip) and send each slot in use to the lane of its rank among
+// them; larger pools look the tables up per token and take the smallest
+// remaining slot per pass.  With store set the wave also writes the
+// per-token tables the epilogue reads (vid, tr8, tgrp), the group tables and
+// count, and the error flag.
+__device__ __forceinline__ int dec_plan(const DecArgs& a, bool store, int* gs_out, int* gr_out) {
+    const int l = threadIdx.x & 63;
+    const bool in = l < a.T;
+    const bool small = a.max_slots <= 64;
+    const int lt = small && l < a.max_slots ? a.loaded[l] : 0;
+    const int rt = small && l < a.max_slots ? a.r8[l] : 0;
+    int id = -1;
+    if (a.ids) {
+        id = in ? a.ids[l] : -1;
+    } else {
+        // segments in token order: the last one starting at or before t
+        for (int i = 0; i < a.n_seg; ++i)
+            if (l >= a.seg_start[i]) id = a.seg_slot[i];
+        if (!in) id = -1;
+    }
+    const bool in_range = id >= 0 && id < a.max_slots;
+    int ld, r8v;
+    if (small) {
+        ld = __shfl(lt, in_range ? id : 0);
+        r8v = __shfl(rt, in_range ? id : 0);
+        if (!in_range) ld = r8v = 0;
+    } else {
+        ld = in_range ? a.loaded[id] : 0;
+        r8v = in_range ? a.r8[id] : 0;
+    }
+    bool ok = in_range && ld != 0;
+    bool bad = __ballot(in && !ok && id != -1) != 0ull;
+    int g = 0, mine = -1, gs = 0, gr = 0;
+    const int v = ok ? id : -1;
+    if (small) {
+        const unsigned long long bit = ok ? 1ull << v : 0ull;
+        const unsigned long long used =
+            (unsigned long long)wave_or((unsigned)bit) | ((unsigned long long)wave_or((unsigned)(bit >> 32)) << 32);
+        g = __popcll(used);
+        // lane l holds slot l: a slot in use goes to the lane of its rank
+        // among them, the other lanes to the lanes from g on (together a
+        // permutation of the 64 lanes)
+        const int below = __popcll(used & ((1ull << l) - 1ull));
+        const int to = ((used >> l) & 1ull) ? below : g + (l - below);
+        gs = __builtin_amdgcn_ds_permute(to * 4, l);
+        gr = __builtin_amdgcn_ds_permute(to * 4, rt);
+        if (ok) mine = __popcll(used & (bit - 1ull));
+    } else {
+        unsigned long long rem = __ballot(ok);
+        while (rem) {
+            const int m = wave_min(((rem >> l) & 1ull) ? v : 0x7fffffff);
+            const bool eq = ok && v == m;
+            if (eq) mine = g;
+            // slot m's rank: held by every lane whose token uses it
+            const int rm = __builtin_amdgcn_readlane(r8v, __ffsll((long long)__ballot(eq)) - 1);
+            if (l == g) {
+                gs = m;
+                gr = rm;
+            }
+            ++g;
+            rem &= ~__ballot(eq);
+        }
+    }
+    if (g > a.act_max) {
+        const bool over = ok && mine >= a.act_max;
+        bad = bad || __ballot(over) != 0ull;
+        if (over) {
+            ok = false;
+            mine = -1;
+        }
+        g = a.act_max;
+    }
+    if (l >= g) gs = gr = 0;
+    if (store) {
+        if (in) {
+            a.vid[l] = ok ? v : -1;
+            a.tr8[l] = ok ? r8v : 0;
+            a.tgrp[l] = mine;
+        }
+        if (l < g) {
+            a.gslot[l] = gs;
+            a.gr8[l] = gr;
+        }
+        if (l == 0) {
+            a.meta[0] = g;
+            a.meta[1] = 0;
+            if (bad) atomicOr(a.err, 1);
+        }
+    }
+    *gs_out = gs;
+    *gr_out = gr;
+    return g;
+}
+
 // Four waves per workgroup as 4 / NB column groups x NB parts of the
 // segment's k-range; a wave takes NB of the group's 4 blocks (4 for bf16
 // weights, 2 in launches with an INT4 base, whose unpacking needs the
@@ -253,9 +357,12 @@ __device__ __forceinline__ void mma_nb_int4(f32x4 (&acc)[MB][NB], const u32x4 (&
 // moves, so the steady state costs one vector add per k-step.
 //
 // Q4: some projection of the launch has an INT4 base (the kernel then handles
-// both operand types; without it the INT4 code is compiled out).
-template <int MB, bool Q4>
+// both operand types; without it the INT4 code is compiled out).  XR (one
+// row block): every wave plans the batch itself and the activations are
+// gathered from the caller's row-major X, so no prep launch runs before.
+template <int MB, bool Q4, bool XR>
 __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))) void dec_main_kernel(DecArgs a) {
+    static_assert(!XR || MB == 1, "row-major activations: one row block");
     constexpr int NB = Q4 ? 2 : 4, NCG = 4 / NB, NKQ = kDecWaves / NCG;
     __shared__ float red[NKQ * MB * 16 * kRedLd];
     const int w = wave_id(), l = threadIdx.x & 63, cg = w % NCG, kq = w / NCG;
@@ -265,11 +372,17 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
     // The plan's outputs (n_act, the slots of the adapters in use; at most
     // kDecodeMaxT = 64 of them) are read with vector loads issued here and
     // waited for only where an adapter segment first needs them, so the base
-    // weight's loads start without waiting for the plan.
-    const int gs = l < a.act_max ? a.gslot[l] : 0;
-    const int gr = l < a.act_max ? a.gr8[l] : 0;
-    const int n_act_v = __builtin_amdgcn_raw_buffer_load_b32(
-        __builtin_amdgcn_make_buffer_rsrc((void*)a.meta, 0, 4, kRawBufferWord3), 0, 0, 0);
+    // weight's loads start without waiting for the plan; with XR every wave
+    // computes them (one load round trip for pools of at most 64 slots).
+    int gs, gr, n_act_v;
+    if constexpr (XR) {
+        n_act_v = dec_plan(a, b == 0 && w == 0, &gs, &gr);
+    } else {
+        gs = l < a.act_max ? a.gslot[l] : 0;
+        gr = l < a.act_max ? a.gr8[l] : 0;
+        n_act_v = __builtin_amdgcn_raw_buffer_load_b32(
+            __builtin_amdgcn_make_buffer_rsrc((void*)a.meta, 0, 4, kRawBufferWord3), 0, 0, 0);
+    }
     DecSeg cs = dec_first(a, n_act_v, gr, sb, se);
     if (!cs.valid) return;
 
@@ -288,8 +401,15 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
     auto point = [&]() __attribute__((always_inline)) {
         const DecProj& P = a.p[ls.p];
         const int KS = ls.pp.KS;
+        if constexpr (XR) {
+            // the caller's row-major X: lane (r, c) of the fragment reads
+            // inputs 32 ks + 8 c .. + 7 of token r (tokens past T read token
+            // T - 1 again; their sums are never stored)
+            xb[0] = reinterpret_cast<const char*>(P.X + (size_t)min(l & 15, a.T - 1) * P.K) + 16 * (l >> 4);
+        } else {
 #pragma unroll
-        for (int rb = 0; rb < MB; ++rb) xb[rb] = reinterpret_cast<const char*>(P.Xp + frag_index(rb, 0, KS));
+            for (int rb = 0; rb < MB; ++rb) xb[rb] = reinterpret_cast<const char*>(P.Xp + frag_index(rb, 0, KS));
+        }
         lq = Q4 && P.Ws && 4 * ls.gl < P.nWb;
         const size_t qs = (size_t)KS * kInt4FragBytes, ss = (size_t)(KS / kInt4Group) * 32;
         // blocks that hold no data for this batch (past an adapter's own rank,
@@ -357,7 +477,7 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
             for (int c = 0; c < NB; ++c) wb[c] = *reinterpret_cast<const u32x4*>(wbp[c] + fo);
         }
-        const unsigned xo = (unsigned)kk * 1024u + lo16;
+        const unsigned xo = XR ? (unsigned)kk * 64u : (unsigned)kk * 1024u + lo16;
 #pragma unroll
         for (int rb = 0; rb < MB; ++rb) xa[rb] = *reinterpret_cast<const u32x4*>(xb[rb] + xo);
     };
@@ -397,12 +517,23 @@ hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s) {
     if (grid <= 0 || grid > kDecMaxGrid) return hipErrorInvalidValue;
     bool q4 = false;
     for (int i = 0; i < a.n_proj; ++i) q4 = q4 || a.p[i].Ws != nullptr;
-#define BDL_DEC_CASE(M)                                                                                  \
-    case M:                                                                                              \
-        if (q4)                                                                                          \
-            hipLaunchKernelGGL((dec_main_kernel<M, true>), dim3(grid), dim3(kDecThreads), 0, s, a);      \
-        else                                                                                             \
-            hipLaunchKernelGGL((dec_main_kernel<M, false>), dim3(grid), dim3(kDecThreads), 0, s, a);     \
+    if (a.plan) {
+        // the planning form reads one row block of the caller's X
+        if (mb != 1) return hipErrorInvalidValue;
+        for (int i = 0; i < a.n_proj; ++i)
+            if (!a.p[i].X) return hipErrorInvalidValue;
+        if (q4)
+            hipLaunchKernelGGL((dec_main_kernel<1, true, true>), dim3(grid), dim3(kDecThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((dec_main_kernel<1, false, true>), dim3(grid), dim3(kDecThreads), 0, s, a);
+        return hipGetLastError();
+    }
+#define BDL_DEC_CASE(M)                                                                                   \
+    case M:                                                                                               \
+        if (q4)                                                                                           \
+            hipLaunchKernelGGL((dec_main_kernel<M, true, false>), dim3(grid), dim3(kDecThreads), 0, s, a);  \
+        else                                                                                              \
+            hipLaunchKernelGGL((dec_main_kernel<M, false, false>), dim3(grid), dim3(kDecThreads), 0, s, a); \
         break;
     switch (mb) {
         BDL_DEC_CASE(1)

@@ -149,6 +149,8 @@ constexpr int kDecMaxGrid = 1024;    // most workgroups of the main launch
 constexpr int kPartElems = 64 * 64;  // fp32 partial tile: 64 rows x 64 virtual columns
 
 struct DecProj {
+    const uint16_t* X;        // the caller's activations [T x K], row-major (batches of at most 16
+                              // tokens planned in the main launch); else null and Xp is read
     const uint16_t* Xp;       // packed activations (fragment layout)
     const uint16_t* W;        // packed base weight
     const uint16_t* Ws;       // INT4 base: its scales (null for a bf16 base)
@@ -177,14 +179,27 @@ struct DecArgs {
     const uint16_t* pool;
     long long slot_stride;
     const float* scale;       // [max_slots]
-    const int* vid;           // [T] validated ids
-    const int* tr8;           // [T] padded rank of each token's adapter (0: none)
-    const int* tgrp;          // [T] group (adapter in use) index of each token, -1: none
-    const int* gslot;         // [groups] slot of each adapter in use
-    const int* gr8;           // [groups] its rank padded to 8 (its A^T blocks: n_slices gr8 / 16,
+    // The batch's plan.  plan = 0: the prep launch wrote it into the tables
+    // below.  plan = 1 (batches of at most 16 tokens): every wave of the main
+    // launch computes it from the batch (ids, or segments) and the slot
+    // tables, and the first wave of workgroup 0 stores the tables below.
+    int plan;
+    const int* ids;           // [T] per-token slot ids, or null: the segments below
+    int n_seg;                // segments (ids null): token t takes seg_slot[i] of the last i with
+    int seg_start[kDecodeMaxT];   // seg_start[i] <= t (the host checked that they tile 0..T-1)
+    int seg_slot[kDecodeMaxT];
+    const int* loaded;        // [max_slots] nonzero: the slot holds an adapter
+    const int* r8;            // [max_slots] padded rank of each slot
+    int max_slots;
+    int* vid;                 // [T] validated ids
+    int* tr8;                 // [T] padded rank of each token's adapter (0: none)
+    int* tgrp;                // [T] group (adapter in use) index of each token, -1: none
+    int* gslot;               // [groups] slot of each adapter in use
+    int* gr8;                 // [groups] its rank padded to 8 (its A^T blocks: n_slices gr8 / 16,
                               // rounded up; positions past them hold no data)
-    const int* meta;          // [0] number of adapters in use (n_act)
-    int act_max;              // adapter positions in the column lists: the host's bound on n_act
+    int* meta;                // [0] number of adapters in use (n_act)
+    int act_max;              // adapter positions in the column lists: the host's bound on n_act;
+                              // the plan treats adapters past it (slot order) as none and raises *err
     float* part;              // partial tiles: slot g + b for group g and workgroup b
     int part_slots;
     int main_grid;            // workgroups of the main launch

@@ -33,7 +33,8 @@ def _bits(outs):
     return [device_to_float(o).view(np.uint32).copy() for o in outs]
 
 
-@pytest.mark.parametrize("model,T,path", [("llama-3.1-8b", 64, "decode"), ("llama-3.1-8b", 100, "tile64"),
+@pytest.mark.parametrize("model,T,path", [("llama-3.1-8b", 64, "decode"), ("llama-3.1-8b", 16, "decode"),
+                                          ("llama-3.1-8b", 100, "tile64"),
                                           ("llama-3.1-70b", 200, "medium"), ("llama-3.1-8b", 300, "large")])
 def test_graph_replays_match_eager(torch_cuda, model, T, path):
     torch = torch_cuda

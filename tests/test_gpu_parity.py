@@ -217,9 +217,10 @@ def test_plan_device_bit_exact(torch_cuda, T, n_slots, kind):
     pool.close()
 
 
-def test_invalid_ids_are_base_only_and_flagged(torch_cuda):
+@pytest.mark.parametrize("T", [40, 12])
+def test_invalid_ids_are_base_only_and_flagged(torch_cuda, T):
+    # 12 tokens: batches of at most 16 plan inside the decode launch itself
     torch = torch_cuda
-    T = 40
     ids = np.array([t % 4 for t in range(T)])
     ids[5] = 99
     ids[6] = 3                                # slot 3 will be unloaded
@@ -238,13 +239,14 @@ def test_invalid_ids_are_base_only_and_flagged(torch_cuda):
     pool.close()
 
 
+@pytest.mark.parametrize("T", [60, 14])
 @pytest.mark.parametrize("n_slots", [64, 150])
-def test_decode_plan_pool_sizes(torch_cuda, n_slots):
+def test_decode_plan_pool_sizes(torch_cuda, n_slots, T):
     # decode batches plan in one wave: pools of up to 64 slots keep the slot
     # tables in lanes (slot 63 is the mask's top bit), larger pools take the
-    # per-pass minimum; unloaded and out-of-range ids must read as -1
+    # per-pass minimum; unloaded and out-of-range ids must read as -1.  At 14
+    # tokens the plan runs inside the decode launch, at 60 in its own launch
     torch = torch_cuda
-    T = 60
     rng = np.random.default_rng(n_slots)
     loaded = sorted(set(rng.choice(n_slots, size=min(40, n_slots - 1), replace=False).tolist()) | {0, n_slots - 1})
     ids = rng.choice(loaded, size=T)

@@ -171,14 +171,15 @@ def test_pool_byte_budget_sizes_the_slots(torch_cuda):
     pool.close()
 
 
-def test_captured_decode_bounds_adapters_loaded_later(torch_cuda):
+@pytest.mark.parametrize("T", [24, 10])
+def test_captured_decode_bounds_adapters_loaded_later(torch_cuda, T):
     # A decode forward captured while 2 adapters were loaded replays with ids
     # that use 4: the adapters past the bound (slots 2 and 3, ascending slot
     # order) get the base output and the device error flag is raised; the
-    # others stay exact.  The segments form has no such bound.
+    # others stay exact.  The segments form has no such bound.  At 10 tokens
+    # the plan runs inside the decode launch.
     torch = torch_cuda
     import paper_2510_23346_amd as bd
-    T = 24
     ranks = [8, 16, 8, 16, 8, 8]
     ids0 = np.array([[0, 1, -1][t % 3] for t in range(T)], np.int32)
     ids1 = np.array([[0, 1, 2, 3, -1][t % 5] for t in range(T)], np.int32)
