@@ -57,7 +57,7 @@ def test_mlp_parity(torch_cuda, T, act_name):
     pool.close()
 
 
-@pytest.mark.parametrize("T", [40, 200])
+@pytest.mark.parametrize("T", [12, 40, 200])
 def test_mlp_equals_layer_calls_and_is_deterministic(torch_cuda, T):
     # act=none: H is the bf16 output of the first projection either way, so
     # the MLP entry point must reproduce, bit for bit, forward_layer on the
