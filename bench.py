@@ -454,7 +454,7 @@ def measure(index, K, warmup, rotate=0, eager=False):
         # base partials), epilogue (partial sums + expand); main moves the
         # weights and dominates
         names = ("prep", "main", "epilogue")
-        if spec.T <= bd.DECODE_PLAN_IN_MAIN_T:
+        if bd.decode_plans_in_main(spec.T, [p.d_in for p in spec.projs]):
             names = ("", "main", "epilogue")    # planned inside the main launch: no prep launch
         dom, dom_name = 1, "bdl::dec_main_kernel"
         algo = m_bytes

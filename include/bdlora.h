@@ -71,11 +71,14 @@ extern "C" {
  * expand fused in, or for medium batches on large layers base partials and
  * an epilogue; see bdlora_last_path). */
 #define BDLORA_DECODE_MAX_T 64
-/* Decode batches of at most this many tokens (one 16-row block) skip the
- * plan and packing launch: every wave of the K-split launch plans the batch
- * from the ids (or segments) itself and reads the caller's row-major
- * activations.  Results are the same bits either way. */
-#define BDLORA_DECODE_PLAN_IN_MAIN_T 16
+/* Decode batches skip the plan and packing launch when T <= 16, or when
+ * T <= BDLORA_DECODE_PLAN_IN_MAIN_T and T x (the sum of d_in over the
+ * call's projections) x 2 bytes <= BDLORA_DECODE_PLAN_IN_MAIN_BYTES: every
+ * wave of the K-split launch then plans the batch from the ids (or
+ * segments) itself and gathers the caller's row-major activations, which
+ * slows that launch more the more activation bytes it gathers. */
+#define BDLORA_DECODE_PLAN_IN_MAIN_T 32
+#define BDLORA_DECODE_PLAN_IN_MAIN_BYTES 1572864
 /* Largest number of segments a bdlora_segments batch may have (the segments
  * travel with the launch, by value). */
 #define BDLORA_MAX_SEGMENTS 256

@@ -18,6 +18,7 @@ import numpy as np
 __all__ = [
     "COLUMN", "ROW", "BDLoRAError", "lib", "lib_path", "Pool", "ProjDesc", "build_plan",
     "adapter_elems", "pool_size", "pack_weight", "HEADER_FUNCTIONS", "DECODE_MAX_T", "DECODE_PLAN_IN_MAIN_T",
+    "DECODE_PLAN_IN_MAIN_BYTES", "decode_plans_in_main",
     "ACT_NONE", "ACT_SILU_MUL", "WEIGHT_BF16", "WEIGHT_INT4_G128", "pack_weight_int4",
     "packed_weight_bytes", "MAX_SEGMENTS", "Segments", "layout_slot_bytes", "pack_adapter_layout",
 ]
@@ -25,7 +26,15 @@ __all__ = [
 COLUMN, ROW = 0, 1
 MAX_SLICES = 4
 DECODE_MAX_T = 64       # BDLORA_DECODE_MAX_T: largest batch that takes the decode launches
-DECODE_PLAN_IN_MAIN_T = 16   # BDLORA_DECODE_PLAN_IN_MAIN_T: decode batches planned inside the K-split launch
+DECODE_PLAN_IN_MAIN_T = 32            # BDLORA_DECODE_PLAN_IN_MAIN_T
+DECODE_PLAN_IN_MAIN_BYTES = 1572864    # BDLORA_DECODE_PLAN_IN_MAIN_BYTES
+
+
+def decode_plans_in_main(T, d_ins):
+    """Whether a decode call of T tokens over projections with inputs
+    ``d_ins`` skips the plan launch (the rule stated in bdlora.h)."""
+    act = 2 * T * sum(int(k) for k in d_ins)
+    return 1 <= T <= 16 or (T <= DECODE_PLAN_IN_MAIN_T and act <= DECODE_PLAN_IN_MAIN_BYTES)
 MAX_SEGMENTS = 256      # BDLORA_MAX_SEGMENTS: most segments of a batch given as segments
 STATIC_SCRATCH_BYTES = 32 << 20   # BDLORA_STATIC_SCRATCH_BYTES: static scratch of forward_layer_static
 ACT_NONE, ACT_SILU_MUL = 0, 1   # BDLORA_ACT_*: activation between the MLP's projections

@@ -802,12 +802,17 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
                           const void* const* W, void* const* out, const Batch& B, int T, hipStream_t s,
                           const DecWs& ws, const DecMode& mode = DecMode()) {
     const Layout& L = P->L;
-    // batches of one row block: the main launch plans the batch in every
-    // wave and reads the caller's X, so no prep launch runs (the gathered
-    // rows cost that launch less than the prep launch takes; with more row
-    // blocks they cost more)
-    static_assert(BDLORA_DECODE_PLAN_IN_MAIN_T == 16, "the folded plan runs the one-row-block kernel");
-    const bool fold = mode.prep && T <= BDLORA_DECODE_PLAN_IN_MAIN_T;
+    // small batches: the main launch plans the batch in every wave and
+    // gathers the caller's X, so no prep launch runs.  The gathered rows
+    // slow the main launch with the activation bytes (measured: a 17..32
+    // token batch of the 70B layer shard, 58 KB of activations per token,
+    // gains up to about 28 tokens, the 8B shard, 29 KB per token, at every
+    // size up to 32; at 64 tokens the prep launch is cheaper)
+    static_assert(BDLORA_DECODE_PLAN_IN_MAIN_T <= 32, "the planning kernel takes at most two row blocks");
+    long long act_bytes = 0;
+    for (int i = 0; i < n; ++i) act_bytes += 2LL * T * L.proj[projs[i]].K;
+    const bool fold = mode.prep && (T <= 16 || (T <= BDLORA_DECODE_PLAN_IN_MAIN_T &&
+                                                act_bytes <= BDLORA_DECODE_PLAN_IN_MAIN_BYTES));
     // adapter positions of the launches: the loaded adapters bound the
     // distinct ones a batch can use (the plan treats any past that bound as
     // none and raises the error flag).  Both forms of the batch (ids,

@@ -1,7 +1,7 @@
 // Decode path (batches of at most kDecodeMaxT tokens): two launches after
-// the prep launch (plan + activation packing); batches of at most 16 tokens
-// skip the prep launch (the main launch plans the batch in every wave and
-// reads the caller's X).
+// the prep launch (plan + activation packing); small batches (at most 32
+// tokens, by the host's rule) skip the prep launch (the main launch plans
+// the batch in every wave and gathers the caller's X).
 //
 //  dec_main_kernel -- one split-K GEMM of the packed activations X [T x K]
 //                     against a virtual column list per projection: the
@@ -358,11 +358,11 @@ __device__ __forceinline__ void mma_nb_int4(f32x4 (&acc)[MB][NB], const u32x4 (&
 //
 // Q4: some projection of the launch has an INT4 base (the kernel then handles
 // both operand types; without it the INT4 code is compiled out).  XR (one
-// row block): every wave plans the batch itself and the activations are
-// gathered from the caller's row-major X, so no prep launch runs before.
+// or two row blocks): every wave plans the batch itself and the activations
+// are gathered from the caller's row-major X, so no prep launch runs before.
 template <int MB, bool Q4, bool XR>
 __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))) void dec_main_kernel(DecArgs a) {
-    static_assert(!XR || MB == 1, "row-major activations: one row block");
+    static_assert(!XR || MB <= 2, "row-major activations: at most two row blocks");
     constexpr int NB = Q4 ? 2 : 4, NCG = 4 / NB, NKQ = kDecWaves / NCG;
     __shared__ float red[NKQ * MB * 16 * kRedLd];
     const int w = wave_id(), l = threadIdx.x & 63, cg = w % NCG, kq = w / NCG;
@@ -402,10 +402,13 @@ __global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2))
         const DecProj& P = a.p[ls.p];
         const int KS = ls.pp.KS;
         if constexpr (XR) {
-            // the caller's row-major X: lane (r, c) of the fragment reads
-            // inputs 32 ks + 8 c .. + 7 of token r (tokens past T read token
-            // T - 1 again; their sums are never stored)
-            xb[0] = reinterpret_cast<const char*>(P.X + (size_t)min(l & 15, a.T - 1) * P.K) + 16 * (l >> 4);
+            // the caller's row-major X: lane (r, c) of row block rb reads
+            // inputs 32 ks + 8 c .. + 7 of token 16 rb + r (tokens past T
+            // read token T - 1 again; their sums are never read)
+#pragma unroll
+            for (int rb = 0; rb < MB; ++rb)
+                xb[rb] = reinterpret_cast<const char*>(P.X + (size_t)min(16 * rb + (l & 15), a.T - 1) * P.K) +
+                         16 * (l >> 4);
         } else {
 #pragma unroll
             for (int rb = 0; rb < MB; ++rb) xb[rb] = reinterpret_cast<const char*>(P.Xp + frag_index(rb, 0, KS));
@@ -518,14 +521,18 @@ hipError_t launch_dec_main(const DecArgs& a, int mb, hipStream_t s) {
     bool q4 = false;
     for (int i = 0; i < a.n_proj; ++i) q4 = q4 || a.p[i].Ws != nullptr;
     if (a.plan) {
-        // the planning form reads one row block of the caller's X
-        if (mb != 1) return hipErrorInvalidValue;
+        // the planning form reads one or two row blocks of the caller's X
+        if (mb != 1 && mb != 2) return hipErrorInvalidValue;
         for (int i = 0; i < a.n_proj; ++i)
             if (!a.p[i].X) return hipErrorInvalidValue;
-        if (q4)
+        if (mb == 1 && q4)
             hipLaunchKernelGGL((dec_main_kernel<1, true, true>), dim3(grid), dim3(kDecThreads), 0, s, a);
-        else
+        else if (mb == 1)
             hipLaunchKernelGGL((dec_main_kernel<1, false, true>), dim3(grid), dim3(kDecThreads), 0, s, a);
+        else if (q4)
+            hipLaunchKernelGGL((dec_main_kernel<2, true, true>), dim3(grid), dim3(kDecThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((dec_main_kernel<2, false, true>), dim3(grid), dim3(kDecThreads), 0, s, a);
         return hipGetLastError();
     }
 #define BDL_DEC_CASE(M)                                                                                   \

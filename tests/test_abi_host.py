@@ -42,6 +42,7 @@ def test_binding_constants_match_header():
     macros = dict(re.findall(r"^#define (BDLORA_\w+)\s+\(?(-?\d+)\)?", text, re.M))
     assert int(macros["BDLORA_DECODE_MAX_T"]) == bd.DECODE_MAX_T
     assert int(macros["BDLORA_DECODE_PLAN_IN_MAIN_T"]) == bd.DECODE_PLAN_IN_MAIN_T
+    assert int(macros["BDLORA_DECODE_PLAN_IN_MAIN_BYTES"]) == bd.DECODE_PLAN_IN_MAIN_BYTES
     assert (int(macros["BDLORA_ACT_NONE"]), int(macros["BDLORA_ACT_SILU_MUL"])) == (bd.ACT_NONE, bd.ACT_SILU_MUL)
     assert int(macros["BDLORA_MAX_SLICES"]) == bd.MAX_SLICES
     assert (int(macros["BDLORA_COLUMN"]), int(macros["BDLORA_ROW"])) == (bd.COLUMN, bd.ROW)

@@ -54,7 +54,7 @@ def _run(torch, spec, layer, pool, ids=None):
     return dl, [device_to_float(o) for o in outs]
 
 
-@pytest.mark.parametrize("T", [1, 16, 37, 64, 100, 300])
+@pytest.mark.parametrize("T", [1, 16, 24, 37, 64, 100, 300])
 def test_int4_parity(torch_cuda, T):
     torch = torch_cuda
     spec, layer, pool = _layer(T, 40 + T)

@@ -43,7 +43,7 @@ def _run_mlp(torch, pool, dl, act, first, T):
 
 
 @pytest.mark.parametrize("act_name", ["none", "silu_mul"])
-@pytest.mark.parametrize("T", [1, 16, 37, 64, 100, 300])
+@pytest.mark.parametrize("T", [1, 16, 24, 37, 64, 100, 300])
 def test_mlp_parity(torch_cuda, T, act_name):
     torch = torch_cuda
     spec, layer, pool = _setup(T, 100 + T, act_name)

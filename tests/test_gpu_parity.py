@@ -7,6 +7,8 @@ output's rms as floor, after allowing the two bf16 output roundings the
 difference of two GPU outputs carries (2^-8 (|y| + |y_base|)).  Integer plan
 results are compared exactly.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -66,7 +68,7 @@ def _oracle_base(layer, rows=None):
 TINY_RANKS = [0, 1, 3, 8, 16, 24, 5, 32]
 
 
-@pytest.mark.parametrize("T", [1, 5, 16, 37, 64, 100, 300, 700])
+@pytest.mark.parametrize("T", [1, 5, 16, 24, 37, 64, 100, 300, 700])
 def test_tiny_parity(torch_cuda, T):
     torch = torch_cuda
     rng = np.random.default_rng(T)
@@ -431,6 +433,35 @@ def test_decode_variants_parity(torch_cuda, index):
     else:
         refs = bdlora.layer_forward(layer)
         rbase = _oracle_base(layer)
+    for p in range(len(spec.projs)):
+        _check(ys[p], refs[p], yb[p], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
+    assert pool.device_error() == 0
+    pool.close()
+
+
+@pytest.mark.parametrize("model,T,in_main", [("llama-3.1-8b", 32, True), ("llama-3.1-70b", 24, True),
+                                             ("llama-3.1-70b", 32, False), ("llama-3.1-70b", 17, True)])
+def test_decode_plan_in_main_boundary(torch_cuda, model, T, in_main):
+    # decode batches of two row blocks plan inside the K-split launch while
+    # their activations stay small (the 8B layer shard at 32 tokens, the 70B
+    # one up to about 26) and take the plan launch above that; both forms
+    # are compared with the oracle on every row
+    torch = torch_cuda
+    import paper_2510_23346_amd as bd
+    ranks = [16, 8, 32, 64, 16, 8]
+    base = wl.workload(3) if model == "llama-3.1-70b" else wl.workload(1)
+    spec = dataclasses.replace(base, name=f"boundary-{model}-{T}", T=T, n_slots=len(ranks), ranks=ranks,
+                               scales=[2.0, 1.0, 0.5, 1.5, 1.0, 0.75], seed=700 + T)
+    assert bd.decode_plans_in_main(T, [p.d_in for p in spec.projs]) == in_main
+    slots = list(range(len(ranks)))
+    layer = wl.draw_layer(spec, slots=slots)
+    pool = make_pool(spec, max_tokens=T)
+    load_adapters(pool, spec, slots, cache=layer.adapters)
+    dl, ys = _run_layer(torch, spec, layer, pool)
+    assert pool.last_path() == "decode"
+    yb = _base_only(torch, spec, dl, pool)
+    refs = bdlora.layer_forward(layer)
+    rbase = _oracle_base(layer)
     for p in range(len(spec.projs)):
         _check(ys[p], refs[p], yb[p], rbase[p], what=f"{spec.name} {spec.projs[p].name}")
     assert pool.device_error() == 0
