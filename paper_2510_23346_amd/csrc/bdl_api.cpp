@@ -848,15 +848,20 @@ static int forward_decode(bdlora_pool_t P, int n, const int32_t* projs, const vo
         groups_max += (d.nWb + (long long)act_max * d.nbA + 3) / 4;
     }
     // two workgroups per CU, each with at least 64 units (16 k-steps of a
-    // full group) whatever the number of adapters in use: a small layer
-    // (one 1792-column projection at 16 tokens) then runs on fewer, longer
-    // workgroups, so that each output group is split over fewer partial
-    // tiles, which its epilogue adds one by one (there 20.7 -> 17.5 us a
-    // step; larger layers keep two per CU); the kernels' 32-bit schedule
-    // arithmetic needs units * workgroups < 2^32
+    // full group) whatever the number of adapters in use; fewer, longer
+    // workgroups split each output group over fewer partial tiles, which its
+    // epilogue adds one by one.  Measured with the data streamed from HBM: a
+    // layer whose base weights give one to two such workgroups per CU is
+    // fastest on one per CU of at least 128 units (the 8B MLP's gate and up
+    // at 64 tokens, 448 64-unit workgroups: 54.1 -> 51.1 us a step); a
+    // smaller one keeps 64-unit workgroups (one 1792-column projection at 16
+    // tokens: 20.7 -> 17.5 us from two per CU, 18.1 with 128-unit ones); a
+    // larger one two per CU (the 8B decode layer, 832 64-unit workgroups).
+    // The kernels' 32-bit schedule arithmetic needs units * workgroups < 2^32
     // (at least one workgroup: one that owns every unit needs no minimum)
+    const long long min_units = units_min >= 64LL * P->n_cu && units_min < 64LL * 2 * P->n_cu ? 128 : 64;
     const int grid = (int)std::min<long long>(
-        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, std::max(1LL, units_min / 64),
+        {2LL * P->n_cu, (long long)bdl::kDecMaxGrid, std::max(1LL, units_min / min_units),
          0xffffffffLL / std::max(1LL, units_max)});
     if (grid < 1) return fail(BDLORA_ERR_SHAPE, "batch too large for the decode launch's schedule");
     float* part = ws.part;
